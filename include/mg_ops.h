@@ -1,0 +1,47 @@
+/*
+ * mg_ops.h -- op-level entry points of libmg.so, exported so the test-suite can
+ * check single kernels against the CPU oracle.  Not part of the decode step.
+ * Same conventions as mg.h: [device] pointers owned by the caller, work enqueued
+ * on `stream` (hipStream_t as void*), host-checked arguments return an error and
+ * enqueue nothing.
+ */
+#ifndef MG_OPS_H
+#define MG_OPS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "mg.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* out[i] = bf16 round-to-nearest-even of in[i] (NaN -> quiet NaN), the device
+ * conversion used at every bf16 rounding point.  in fp32 [n], out uint16 [n]. */
+mg_status mg_op_probe_bf16(int64_t n, const float* in, uint16_t* out, void* stream);
+/* out[i] = the verifier's EXP(in[i]): Cody-Waite reduction with a two-part ln 2,
+ * degree-7 Taylor polynomial (Horner, fma), scaling by 2^n; +inf above n = 127,
+ * +0 below n = -126. */
+mg_status mg_op_probe_exp(int64_t n, const float* in, float* out, void* stream);
+/* q[i] = a[i] / b[i] and r[i] = sqrt(a[i]), IEEE correctly rounded fp32. */
+mg_status mg_op_probe_divsqrt(int64_t n, const float* a, const float* b, float* q, float* r, void* stream);
+
+/* Y[r][j] = sum_k X[r][k] * W[j][k] in fp32 (no bias, no rounding to bf16), for
+ * r < n <= 256, N % 16 == 0, K % 8 == 0.  canon = 1: the verifier's canonical
+ * GEMV (CDOT order, bit-reproducible); canon = 0: the fast path's MFMA GEMM with
+ * its split-K choice for this shape, which needs a workspace of
+ * mg_op_linear_workspace_bytes(n, N, K) bytes (ignored when canon = 1).
+ * bias must be NULL.  X bf16 [n][K], W bf16 [N][K], Y fp32 [n][N]. */
+size_t mg_op_linear_workspace_bytes(int n, int N, int K);
+mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const uint16_t* W, const uint16_t* bias,
+                       float* Y, void* workspace, size_t workspace_bytes, void* stream);
+
+/* y[r] = RMSNorm(x[r]) * gamma with the canonical sum of squares (one wave per
+ * row, CDOT order), r < n; d % 8 == 0.  bf16 in, bf16 out. */
+mg_status mg_op_rmsnorm(int n, int d, const uint16_t* x, const uint16_t* gamma, float eps, uint16_t* y, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,380 @@
+// k_misc.hip -- embedding gather, RMSNorm, RoPE + K/V placement, SwiGLU, the
+// top-1/top-2 margin gate, the K/V column repair, step bookkeeping, numerics probes.
+#include "mg_device.h"
+#include "mg_kernels.h"
+
+namespace mg {
+
+// ------------------------------------------------------------------ embedding
+// x[i][:] = embed[token of item i][:]
+__global__ __launch_bounds__(256) void embed_kernel(Items it, const uint16_t* __restrict__ E, int d,
+                                                    uint16_t* __restrict__ x) {
+    const int i = blockIdx.x;
+    if (i >= items_n(it)) return;
+    const int tok = items_tok(it, i);
+    const uint4* src = reinterpret_cast<const uint4*>(E + (size_t)tok * d);
+    uint4* dst = reinterpret_cast<uint4*>(x + (size_t)i * d);
+    for (int t = threadIdx.x; t < d / 8; t += blockDim.x) dst[t] = src[t];
+}
+
+hipError_t launch_embed(const Items& it, const uint16_t* embed, int d, uint16_t* x, hipStream_t s) {
+    if (it.n_host <= 0) return hipSuccess;
+    hipLaunchKernelGGL(embed_kernel, dim3(it.n_host), dim3(256), 0, s, it, embed, d, x);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ RMSNorm
+// One wave per row.  ss = CDOT(x, x) (lane l owns groups l, l+64, ...; fma in
+// element order; xor butterfly), m = ss / d, r = 1 / sqrt(m + eps),
+// y_i = bf16((x_i * r) * gamma_i).  Used by both paths (it is batch-invariant).
+__global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ g,
+                                                      RowCount rc, int d, float eps, uint16_t* __restrict__ y) {
+    const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+    const int row = blockIdx.x * 4 + wave;
+    if (row >= rc.get()) return;
+    const uint4* xr = reinterpret_cast<const uint4*>(x + (size_t)row * d);
+    const int G = d >> 3;
+    float a = 0.0f;
+    for (int gi = lane; gi < G; gi += 64) {
+        const uint4 v = xr[gi];
+        const float e[8] = {bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y),
+                            bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w)};
+#pragma unroll
+        for (int k = 0; k < 8; ++k) a = __builtin_fmaf(e[k], e[k], a);
+    }
+    const float ss = butterfly_sum(a);
+    const float m = ieee_div(ss, (float)d);
+    const float r = ieee_div(1.0f, ieee_sqrt(m + eps));
+    const uint4* gr = reinterpret_cast<const uint4*>(g);
+    uint4* yr = reinterpret_cast<uint4*>(y + (size_t)row * d);
+    for (int gi = lane; gi < G; gi += 64) {
+        const uint4 v = xr[gi], gv = gr[gi];
+        uint4 o;
+        o.x = pack_bf2((bf_lo(v.x) * r) * bf_lo(gv.x), (bf_hi(v.x) * r) * bf_hi(gv.x));
+        o.y = pack_bf2((bf_lo(v.y) * r) * bf_lo(gv.y), (bf_hi(v.y) * r) * bf_hi(gv.y));
+        o.z = pack_bf2((bf_lo(v.z) * r) * bf_lo(gv.z), (bf_hi(v.z) * r) * bf_hi(gv.z));
+        o.w = pack_bf2((bf_lo(v.w) * r) * bf_lo(gv.w), (bf_hi(v.w) * r) * bf_hi(gv.w));
+        yr[gi] = o;
+    }
+}
+
+hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, int n_host, const int32_t* n_dev, int cap, int d,
+                          float eps, uint16_t* y, hipStream_t s) {
+    const int rows = n_dev ? cap : n_host;
+    if (rows <= 0) return hipSuccess;
+    RowCount rc{n_dev, n_host, cap};
+    hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, x, gamma, rc, d, eps, y);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ RoPE + K/V placement
+// Rotate-half RoPE: pair (i, i + hd/2) of every q and k head is rotated by the
+// angle pos * theta^(-2i/hd), using the fp32 cos/sin table built on the host in
+// float64.  q'_i = bf16(q_i c - q_(i+h) s), q'_(i+h) = bf16(q_(i+h) c + q_i s),
+// products and sums separately rounded.  K' and V go to the verifier's own column
+// (kv_col != NULL) or into the paged cache at the item's position.
+__global__ __launch_bounds__(256) void rope_kv_kernel(Items it, ModelDims m, int layer, const uint16_t* __restrict__ qkv,
+                                                      const float* __restrict__ cs, uint16_t* __restrict__ qrot,
+                                                      uint16_t* __restrict__ kv_pool, uint16_t* __restrict__ kv_col) {
+    const int i = blockIdx.x;
+    if (i >= items_n(it)) return;
+    const int r = items_row(it, i);
+    const int pos = items_pos(it, i);
+    const int hd = m.hd, h2 = hd / 2, Nq = m.Hq * hd, Nk = m.Hkv * hd;
+    const uint16_t* src = qkv + (size_t)i * (Nq + 2 * Nk);
+    const float* csp = cs + (size_t)pos * hd;  // [pos][i][cos, sin]
+    uint16_t *kdst, *vdst;
+    if (kv_col) {
+        kdst = kv_col + ((size_t)i * m.L + layer) * 2 * Nk;
+        vdst = kdst + Nk;
+    } else {
+        const int page = it.page_table[(size_t)r * m.max_pages_per_row + pos / m.page_size];
+        const int slot = pos % m.page_size;
+        // [layer][page][K|V][Hkv][page_size][hd]: head kh's row is at +kh*page_size*hd
+        kdst = kv_pool + (((size_t)layer * m.n_pages + page) * 2) * (size_t)Nk * m.page_size + (size_t)slot * hd;
+        vdst = kdst + (size_t)Nk * m.page_size;
+    }
+    const int kv_head_stride = kv_col ? hd : hd * m.page_size;
+    const int nq_pairs = m.Hq * h2, nk_pairs = m.Hkv * h2;
+    for (int t = threadIdx.x; t < nq_pairs + nk_pairs; t += blockDim.x) {
+        const bool isq = t < nq_pairs;
+        const int tt = isq ? t : t - nq_pairs;
+        const int head = tt / h2, ii = tt % h2;
+        const uint16_t* s = isq ? src + head * hd : src + Nq + head * hd;
+        const float a = bf2f(s[ii]), b = bf2f(s[ii + h2]);
+        const float c = csp[2 * ii], sn = csp[2 * ii + 1];
+        const float ac = a * c, bs = b * sn, bc = b * c, as = a * sn;
+        const uint16_t o1 = (uint16_t)f2bf(ac - bs), o2 = (uint16_t)f2bf(bc + as);
+        if (isq) {
+            qrot[(size_t)i * Nq + head * hd + ii] = o1;
+            qrot[(size_t)i * Nq + head * hd + ii + h2] = o2;
+        } else {
+            kdst[(size_t)head * kv_head_stride + ii] = o1;
+            kdst[(size_t)head * kv_head_stride + ii + h2] = o2;
+        }
+    }
+    const uint16_t* vs = src + Nq + Nk;
+    for (int t = threadIdx.x; t < Nk; t += blockDim.x) {
+        const int head = t / hd, dd = t % hd;
+        vdst[(size_t)head * kv_head_stride + dd] = vs[t];
+    }
+}
+
+hipError_t launch_rope_kv(const Items& it, const ModelDims& m, int layer, const uint16_t* qkv, const float* rope_cs,
+                          uint16_t* qrot, uint16_t* kv_pool, uint16_t* kv_col, hipStream_t s) {
+    if (it.n_host <= 0) return hipSuccess;
+    hipLaunchKernelGGL(rope_kv_kernel, dim3(it.n_host), dim3(256), 0, s, it, m, layer, qkv, rope_cs, qrot, kv_pool,
+                       kv_col);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ SwiGLU
+// a = bf16(silu(g) * u), silu(g) = g / (1 + e^-g); gu row = [gate F | up F].
+// canon: the verifier's EXP and IEEE division; otherwise the hardware exp.
+__global__ __launch_bounds__(256) void swiglu_kernel(const uint16_t* __restrict__ gu, RowCount rc, int F, int canon,
+                                                     uint16_t* __restrict__ a) {
+    const int row = blockIdx.y;
+    if (row >= rc.get()) return;
+    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= F) return;
+    const float g = bf2f(gu[(size_t)row * 2 * F + k]);
+    const float u = bf2f(gu[(size_t)row * 2 * F + F + k]);
+    const float t = canon ? canon_exp(-g) : __expf(-g);
+    const float sg = ieee_div(g, 1.0f + t);
+    a[(size_t)row * F + k] = (uint16_t)f2bf(sg * u);
+}
+
+hipError_t launch_swiglu(const uint16_t* gu, int n_host, const int32_t* n_dev, int cap, int F, int canon, uint16_t* a,
+                         hipStream_t s) {
+    const int rows = n_dev ? cap : n_host;
+    if (rows <= 0) return hipSuccess;
+    RowCount rc{n_dev, n_host, cap};
+    hipLaunchKernelGGL(swiglu_kernel, dim3((F + 255) / 256, rows), dim3(256), 0, s, gu, rc, F, canon, a);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ top-1 / top-2
+// Partial state of a top-2 scan: best value/index and the runner-up value of the
+// multiset seen so far.  Merging two states is associative and commutative: the
+// winner is the larger value, the lower index on equal values; the runner-up is
+// the larger of the winner's runner-up and the loser's best.  NaN entries are
+// skipped and only flagged.
+struct Top2 {
+    float v1, v2;
+    int i1;
+    int nan;
+};
+
+__device__ __forceinline__ Top2 top2_merge(const Top2& a, const Top2& b) {
+    if (a.i1 < 0) return Top2{b.v1, b.v2, b.i1, b.nan | a.nan};
+    if (b.i1 < 0) return Top2{a.v1, a.v2, a.i1, a.nan | b.nan};
+    const bool aw = (a.v1 > b.v1) || (a.v1 == b.v1 && a.i1 < b.i1);
+    Top2 o;
+    if (aw) {
+        o.v1 = a.v1; o.i1 = a.i1; o.v2 = fmaxf(a.v2, b.v1);
+    } else {
+        o.v1 = b.v1; o.i1 = b.i1; o.v2 = fmaxf(b.v2, a.v1);
+    }
+    o.nan = a.nan | b.nan;
+    return o;
+}
+
+__device__ __forceinline__ void top2_push(Top2& s, float v, int j) {
+    if (v != v) { s.nan = 1; return; }
+    if (s.i1 < 0) { s.v1 = v; s.i1 = j; return; }
+    if (v > s.v1) { s.v2 = s.v1; s.v1 = v; s.i1 = j; }   // j increases within a thread: ties keep the old index
+    else if (v > s.v2) s.v2 = v;
+}
+
+__device__ __forceinline__ Top2 top2_shfl(const Top2& s, int o) {
+    Top2 t;
+    t.v1 = __shfl_xor(s.v1, o, MG_WAVE);
+    t.v2 = __shfl_xor(s.v2, o, MG_WAVE);
+    t.i1 = __shfl_xor(s.i1, o, MG_WAVE);
+    t.nan = __shfl_xor(s.nan, o, MG_WAVE);
+    return t;
+}
+
+// One block per row: 256 threads scan the row with 16-byte loads, merge by wave
+// shuffles then across waves.  With `gate` set, the last block to finish also
+// writes the ordered list of gated rows and their count.
+__global__ __launch_bounds__(256) void top2_kernel(int B, int V, const float* __restrict__ logits,
+                                                   const uint8_t* __restrict__ prot, float tau, int32_t* top1,
+                                                   float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated,
+                                                   int32_t* ticket, const int32_t* n_dev) {
+    const int b = blockIdx.x;
+    const int nrows = n_dev ? min(max(*n_dev, 0), B) : B;
+    __shared__ Top2 ws[4];
+    __shared__ int last;
+    __shared__ uint8_t flags[1024];
+    if (b < nrows) {
+        const float* row = logits + (size_t)b * V;
+        Top2 s{-__builtin_inff(), -__builtin_inff(), -1, 0};
+        const int t = threadIdx.x;
+        if ((V & 3) == 0) {
+            const float4* r4 = reinterpret_cast<const float4*>(row);
+            for (int q = t; q < V / 4; q += 256) {
+                const float4 v = r4[q];
+                top2_push(s, v.x, 4 * q);
+                top2_push(s, v.y, 4 * q + 1);
+                top2_push(s, v.z, 4 * q + 2);
+                top2_push(s, v.w, 4 * q + 3);
+            }
+        } else {
+            for (int q = t; q < V; q += 256) top2_push(s, row[q], q);
+        }
+#pragma unroll
+        for (int o = 32; o >= 1; o >>= 1) s = top2_merge(s, top2_shfl(s, o));
+        if ((t & 63) == 0) ws[t >> 6] = s;
+        __syncthreads();
+        if (t == 0) {
+            Top2 f = top2_merge(top2_merge(ws[0], ws[1]), top2_merge(ws[2], ws[3]));
+            const int i1 = f.i1 < 0 ? 0 : f.i1;
+            const float g = f.nan ? __builtin_nanf("") : f.v1 - f.v2;
+            top1[b] = i1;
+            if (margin) margin[b] = g;
+            if (gate) {
+                const int p = prot ? (prot[b] != 0) : 1;
+                const int fire = p && !(g >= tau);
+                gate[b] = (uint8_t)fire;
+                if (gated_rows) ticket[1 + b] = fire;
+            }
+        }
+    }
+    if (!gate || !gated_rows) return;
+    // ordered compaction by the last block to finish; ticket[0] counts finished
+    // blocks, ticket[1 + b] holds row b's decision
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        last = (atomicAdd(ticket, 1) == (int)gridDim.x - 1);
+    }
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    for (int q = threadIdx.x; q < nrows; q += blockDim.x)
+        flags[q] = (uint8_t)__hip_atomic_load(ticket + 1 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int n = 0;
+        for (int q = 0; q < nrows; ++q)
+            if (flags[q]) gated_rows[n++] = q;
+        *n_gated = n;
+        __hip_atomic_store(ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1, float* margin,
+                       uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* ticket, const int32_t* n_dev,
+                       hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    hipLaunchKernelGGL(top2_kernel, dim3(B), dim3(256), 0, s, B, V, logits, prot, tau, top1, margin, gate, gated_rows,
+                       n_gated, ticket, n_dev);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ single-column repair
+// One block per listed row.  The decision is taken once (v_tok vs top1, read
+// before anything is written, so emitted may alias top1); on a mismatch the
+// verifier column [L][K|V][Hkv][hd] is copied to the row's current position in
+// every layer, then emitted and the repair counter are updated.
+__global__ __launch_bounds__(256) void repair_kernel(RowCount rc, const int32_t* __restrict__ rows,
+                                                     const int32_t* __restrict__ positions,
+                                                     const int32_t* __restrict__ page_table, const int32_t* top1,
+                                                     const int32_t* __restrict__ v_tok,
+                                                     const uint16_t* __restrict__ v_kvcol, ModelDims m,
+                                                     uint16_t* __restrict__ kv_pool, int32_t* emitted,
+                                                     int32_t* n_repaired) {
+    const int i = blockIdx.x;
+    if (i >= rc.get()) return;
+    __shared__ int decide[2];
+    const int r = rows[i];
+    if (threadIdx.x == 0) {
+        decide[0] = v_tok[i];
+        decide[1] = (v_tok[i] != top1[r]);
+    }
+    __syncthreads();
+    const int vt = decide[0];
+    if (decide[1]) {
+        const int pos = positions[r];
+        const int page = page_table[(size_t)r * m.max_pages_per_row + pos / m.page_size];
+        const int slot = pos % m.page_size;
+        const int hd = m.hd, per_head = hd / 8;  // uint4 per head row
+        const int segs = m.L * 2 * m.Hkv;
+        const uint4* src = reinterpret_cast<const uint4*>(v_kvcol + (size_t)i * segs * hd);
+        for (int t = threadIdx.x; t < segs * per_head; t += blockDim.x) {
+            const int seg = t / per_head, u = t % per_head;
+            const int layer = seg / (2 * m.Hkv), kv = (seg / m.Hkv) % 2, kh = seg % m.Hkv;
+            uint16_t* dst = kv_pool + ((((size_t)layer * m.n_pages + page) * 2 + kv) * m.Hkv + kh) * (size_t)m.page_size * hd +
+                            (size_t)slot * hd;
+            reinterpret_cast<uint4*>(dst)[u] = src[t];
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        emitted[r] = vt;
+        if (decide[1]) atomicAdd(n_repaired, 1);
+    }
+}
+
+hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_t* rows, const int32_t* positions,
+                         const int32_t* page_table, const int32_t* top1, const int32_t* v_tok, const uint16_t* v_kvcol,
+                         const ModelDims& m, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired, hipStream_t s) {
+    const int grid = n_dev ? cap : n_host;
+    if (grid <= 0) return hipSuccess;
+    RowCount rc{n_dev, n_host, cap};
+    hipLaunchKernelGGL(repair_kernel, dim3(grid), dim3(256), 0, s, rc, rows, positions, page_table, top1, v_tok,
+                       v_kvcol, m, kv_pool, emitted, n_repaired);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ bookkeeping
+__global__ void advance_kernel(int B, const int32_t* __restrict__ emitted, int32_t* tokens, int32_t* positions) {
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b < B) {
+        tokens[b] = emitted[b];
+        positions[b] += 1;
+    }
+}
+
+hipError_t launch_advance(int B, const int32_t* emitted, int32_t* tokens, int32_t* positions, hipStream_t s) {
+    if (B <= 0) return hipSuccess;
+    hipLaunchKernelGGL(advance_kernel, dim3((B + 255) / 256), dim3(256), 0, s, B, emitted, tokens, positions);
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ numerics probes
+__global__ void probe_bf16_kernel(int64_t n, const float* in, uint16_t* out) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        out[i] = (uint16_t)f2bf(in[i]);
+}
+__global__ void probe_exp_kernel(int64_t n, const float* in, float* out) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        out[i] = canon_exp(in[i]);
+}
+__global__ void probe_divsqrt_kernel(int64_t n, const float* a, const float* b, float* q, float* r) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x) {
+        q[i] = ieee_div(a[i], b[i]);
+        r[i] = ieee_sqrt(a[i]);
+    }
+}
+
+static int probe_grid(int64_t n) { return (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096); }
+
+hipError_t launch_probe_bf16(int64_t n, const float* in, uint16_t* out, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(probe_bf16_kernel, dim3(probe_grid(n)), dim3(256), 0, s, n, in, out);
+    return hipGetLastError();
+}
+hipError_t launch_probe_exp(int64_t n, const float* in, float* out, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(probe_exp_kernel, dim3(probe_grid(n)), dim3(256), 0, s, n, in, out);
+    return hipGetLastError();
+}
+hipError_t launch_probe_divsqrt(int64_t n, const float* a, const float* b, float* q, float* r, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(probe_divsqrt_kernel, dim3(probe_grid(n)), dim3(256), 0, s, n, a, b, q, r);
+    return hipGetLastError();
+}
+
+}  // namespace mg

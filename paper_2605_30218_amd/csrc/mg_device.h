@@ -1,0 +1,91 @@
+// mg_device.h -- device helpers of libmg (gfx950): bf16 conversion, the verifier's
+// EXP, wave reductions.  Compiled with -ffp-contract=off: a*b+c is two roundings
+// unless written as __builtin_fmaf.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define MG_WAVE 64
+
+namespace mg {
+
+__device__ __forceinline__ float bf2f(uint32_t h16) { return __uint_as_float(h16 << 16); }
+__device__ __forceinline__ float bf_lo(uint32_t pair) { return __uint_as_float(pair << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t pair) { return __uint_as_float(pair & 0xffff0000u); }
+
+// fp32 -> bf16, round to nearest even; NaN becomes a quiet NaN with the same sign
+// and upper payload bits.  Adding 0x7fff plus the kept lsb carries into the upper
+// half exactly when the discarded half exceeds one half ulp, or equals it with an
+// odd kept lsb.
+__device__ __forceinline__ uint32_t f2bf(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) { return f2bf(lo) | (f2bf(hi) << 16); }
+
+// The verifier's exponential: x = n ln2 + r with n = rint(x log2e), r reduced by
+// the two-part ln2 (fp32 head + fp32 tail) with fused multiply-adds; e^r by the
+// degree-7 Taylor polynomial in Horner form with fma; then r scaled by 2^n.
+// n > 127 -> +inf, n < -126 -> +0.  Constants: log2e, ln2 and 1/k! each rounded to
+// fp32; the tail is the fp32 rounding of (ln2 - fp32(ln2)).
+__device__ __forceinline__ float canon_exp(float x) {
+    if (x != x) return x;
+    const float n = __builtin_rintf(x * 0x1.715476p+0f);
+    if (n > 127.0f) return __builtin_inff();
+    if (n < -126.0f) return 0.0f;
+    float r = __builtin_fmaf(-n, 0x1.62e430p-1f, x);
+    r = __builtin_fmaf(-n, -0x1.05c610p-29f, r);
+    float p = 0x1.a01a02p-13f;              // 1/7!
+    p = __builtin_fmaf(p, r, 0x1.6c16c2p-10f);  // 1/6!
+    p = __builtin_fmaf(p, r, 0x1.111112p-7f);   // 1/5!
+    p = __builtin_fmaf(p, r, 0x1.555556p-5f);   // 1/4!
+    p = __builtin_fmaf(p, r, 0x1.555556p-3f);   // 1/3!
+    p = __builtin_fmaf(p, r, 0x1.0p-1f);        // 1/2!
+    p = __builtin_fmaf(p, r, 1.0f);             // 1/1!
+    p = __builtin_fmaf(p, r, 1.0f);             // 1/0!
+    return __builtin_ldexpf(p, (int)n);
+}
+
+// Correctly rounded fp32 division and square root (IEEE), as used by the
+// verifier's RMSNorm, SwiGLU and attention normalisation.  The library is built
+// with -fhip-fp32-correctly-rounded-divide-sqrt, so plain '/' and sqrtf are the
+// IEEE operations; the GPU tests check them against the host bit for bit.
+__device__ __forceinline__ float ieee_div(float a, float b) { return a / b; }
+__device__ __forceinline__ float ieee_sqrt(float a) { return __builtin_sqrtf(a); }
+
+// xor butterfly over the 64 lanes: a_l <- a_l + a_(l xor o), o = 32..1.
+// IEEE addition is commutative, so every lane ends with the same bits.
+__device__ __forceinline__ float butterfly_sum(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = v + __shfl_xor(v, o, MG_WAVE);
+    return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, MG_WAVE));
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum_fast(float v) {
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, MG_WAVE);
+    return v;
+}
+
+// Row set of a launch: `n` rows, or the count read on the device (capped).
+struct RowCount {
+    const int32_t* dev;
+    int host;
+    int cap;
+    __device__ __forceinline__ int get() const {
+        if (!dev) return host;
+        int n = *dev;
+        return n < 0 ? 0 : (n > cap ? cap : n);
+    }
+};
+
+}  // namespace mg

@@ -1,0 +1,115 @@
+// mg_kernels.h -- launch interfaces of libmg's HIP kernels (host side).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mg {
+
+// Which rows a kernel works on.  Row i of a launch is "item" i: its activations
+// live at row i of the compact buffers; `rows` (may be NULL = identity) maps it to
+// the batch row whose token / position / page-table row it uses.
+struct Items {
+    const int32_t* rows;     // [n] batch-row index per item, or NULL
+    const int32_t* n_dev;    // device count, or NULL
+    int n_host;              // host count, or the cap when n_dev is used
+    const int32_t* tokens;   // [batch] token per batch row
+    const int32_t* positions;// [batch] position per batch row
+    const int32_t* page_table; // [batch][max_pages_per_row]
+    int per_item;            // 1: tokens / positions indexed by item (prefill), else by batch row
+};
+
+__device__ __forceinline__ int items_n(const Items& it) {
+    if (!it.n_dev) return it.n_host;
+    const int n = *it.n_dev;
+    return n < 0 ? 0 : (n > it.n_host ? it.n_host : n);
+}
+__device__ __forceinline__ int items_row(const Items& it, int i) { return it.rows ? it.rows[i] : i; }
+__device__ __forceinline__ int items_tok(const Items& it, int i) {
+    return it.per_item ? it.tokens[i] : it.tokens[items_row(it, i)];
+}
+__device__ __forceinline__ int items_pos(const Items& it, int i) {
+    return it.per_item ? it.positions[i] : it.positions[items_row(it, i)];
+}
+
+struct ModelDims {
+    int L, d, Hq, Hkv, hd, F, V;
+    int page_size, max_pages_per_row, n_pages;
+    float eps;
+};
+
+// ---------------------------------------------------------------- canonical GEMV
+enum { EPI_BF16 = 0, EPI_RESID = 1, EPI_F32 = 2 };
+struct GemvArgs {
+    const uint16_t* X;         // [n][K] bf16 (compact rows)
+    int K;
+    const uint16_t* W[3];      // up to three weight matrices, concatenated along the output
+    const uint16_t* bias[3];   // per segment, or NULL
+    int Nseg[3];               // features per segment (0 = unused)
+    int N;                     // total features
+    void* Y;                   // EPI_BF16: bf16 [n][N]; EPI_F32: fp32 [n][N]; EPI_RESID: bf16 residual [n][N] (in/out)
+    int n_host, cap;           // rows
+    const int32_t* n_dev;
+};
+hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
+
+// ---------------------------------------------------------------- fast MFMA GEMM
+enum { FEPI_BF16 = 0, FEPI_RESID = 1, FEPI_F32 = 2 };
+struct FastGemmArgs {
+    const uint16_t* X;         // [M][K] bf16; with swiglu_x: [M][2K] = [gate | up]
+    int M, K;
+    int swiglu_x;              // 1: X row = silu(gate) * up, computed on load
+    const uint16_t* W[3];
+    const uint16_t* bias[3];
+    int Nseg[3];
+    int N;
+    void* Y;
+    float* part;               // split-K partials [S][M][N] fp32 (workspace)
+    int32_t* tickets;          // [N/64] zero-initialised counters (workspace)
+    int S;                     // split-K factor
+};
+hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s);
+int fast_gemm_splits(int M, int N, int K, int n_cu);
+
+// ---------------------------------------------------------------- small kernels
+hipError_t launch_embed(const Items& it, const uint16_t* embed, int d, uint16_t* x, hipStream_t s);
+hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, int n_host, const int32_t* n_dev, int cap, int d,
+                          float eps, uint16_t* y, hipStream_t s);
+// RoPE of q and k for each item, q' -> qrot; K', V -> destination:
+//  kv_col != NULL: the verifier's own column [item][layer][K|V][Hkv][hd] (layer `layer`)
+//  kv_col == NULL: the paged cache at the item's position (fast path / prefill)
+hipError_t launch_rope_kv(const Items& it, const ModelDims& m, int layer, const uint16_t* qkv, const float* rope_cs,
+                          uint16_t* qrot, uint16_t* kv_pool, uint16_t* kv_col, hipStream_t s);
+hipError_t launch_swiglu(const uint16_t* gu, int n_host, const int32_t* n_dev, int cap, int F, int canon,
+                         uint16_t* a, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+    Items it;
+    ModelDims m;
+    int layer;
+    const uint16_t* qrot;      // [n][Hq*hd]
+    const uint16_t* kv_pool;
+    const uint16_t* own_col;   // verifier scratch columns [n][L][2][Hkv][hd], or NULL (read the cache)
+    float* part;               // [n][Hq][max_chunks][hd + 2]
+    int chunk;                 // positions per chunk (canonical: 256)
+    int max_chunks;
+    uint16_t* out;             // [n][Hq*hd]
+};
+hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s);
+
+// ---------------------------------------------------------------- gate / repair / misc
+hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1,
+                       float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* ticket,
+                       const int32_t* n_dev, hipStream_t s);
+hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_t* rows, const int32_t* positions,
+                         const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
+                         const uint16_t* v_kvcol, const ModelDims& m, uint16_t* kv_pool, int32_t* emitted,
+                         int32_t* n_repaired, hipStream_t s);
+hipError_t launch_advance(int B, const int32_t* emitted, int32_t* tokens, int32_t* positions, hipStream_t s);
+
+// element-wise numerics probes used by the tests
+hipError_t launch_probe_bf16(int64_t n, const float* in, uint16_t* out, hipStream_t s);
+hipError_t launch_probe_exp(int64_t n, const float* in, float* out, hipStream_t s);
+hipError_t launch_probe_divsqrt(int64_t n, const float* a, const float* b, float* q, float* r, hipStream_t s);
+
+}  // namespace mg

@@ -1,0 +1,114 @@
+"""Host-side sequencing of the MarginGate decode loop over libmg (arXiv 2605.30218, Sec. 4).
+
+Per step: the fast batched forward (tentative K/V append), the margin gate, one
+device-to-host read of the gated-row count, the verifier on exactly those rows, and
+the commit / single-column repair.  Modes: "off" (fast path only, r_verify = 0),
+"gated" (MarginGate), "always" (the verifier on every protected row, r_verify = 1:
+the always-on baseline of Sec. 4.3).  All arithmetic runs in libmg; this module only
+orders calls and keeps counters.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from .mg import Engine
+
+
+class GatedDecoder:
+    def __init__(self, engine: Engine, page_table, protected=None, tau: float = 0.5):
+        self.e = engine
+        dev = engine.device
+        self.page_table = torch.as_tensor(page_table, dtype=torch.int32).to(dev).contiguous()
+        self.B = self.page_table.shape[0]
+        B, V = self.B, engine.shape.vocab
+        self.tau = float(tau)
+        self.protected = None if protected is None else torch.as_tensor(protected, dtype=torch.uint8).to(dev)
+        prot = np.ones(B, bool) if protected is None else np.asarray(protected, bool)
+        self.always_rows = torch.as_tensor(np.nonzero(prot)[0].astype(np.int32)).to(dev)
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.tokens = torch.zeros(B, **i32)
+        self.positions = torch.zeros(B, **i32)
+        self.logits = torch.empty((B, V), dtype=torch.float32, device=dev)
+        self.top1 = torch.empty(B, **i32)          # also the emitted tokens (repair rewrites gated rows)
+        self.margin = torch.empty(B, dtype=torch.float32, device=dev)
+        self.gate = torch.empty(B, dtype=torch.uint8, device=dev)
+        self.gated_rows = torch.empty(B, **i32)
+        self.n_gated = torch.zeros(1, **i32)
+        self.v_tok = torch.empty(B, **i32)
+        self.v_kvcol = torch.empty((B, engine.col_elems), dtype=torch.int16, device=dev)
+        self.n_repaired = torch.zeros(1, **i32)
+        self._n_host = torch.zeros(1, dtype=torch.int32, pin_memory=True)
+        self._ev = torch.cuda.Event()
+        self.steps = 0
+        self.protected_row_steps = 0
+        self.verified_row_steps = 0
+        self.hist = []
+
+    def set_state(self, tokens, positions):
+        self.tokens.copy_(torch.as_tensor(np.asarray(tokens, np.int32)))
+        self.positions.copy_(torch.as_tensor(np.asarray(positions, np.int32)))
+
+    def step(self, mode: str = "gated", keep=None):
+        """One decode step.  keep: optional dict that receives host copies of the step's
+        logits / top1 / margin / gate / rows / v_tok (tests)."""
+        e, B = self.e, self.B
+        e.decode_step(B, self.tokens, self.positions, self.page_table, self.logits)
+        e.margin_gate(B, self.logits, self.protected, self.tau, self.top1, self.margin, self.gate, self.gated_rows,
+                      self.n_gated)
+        if mode == "off":
+            n, rows = 0, self.gated_rows
+        elif mode == "always":
+            rows = self.always_rows
+            n = int(rows.numel())
+        else:
+            self._n_host.copy_(self.n_gated, non_blocking=True)
+            self._ev.record()
+            self._ev.synchronize()
+            n, rows = int(self._n_host[0]), self.gated_rows
+        if keep is not None:
+            keep.update(logits=self.logits.cpu().numpy(), top1=self.top1.cpu().numpy(),
+                        margin=self.margin.cpu().numpy(), gate=self.gate.cpu().numpy(),
+                        positions=self.positions.cpu().numpy(), tokens=self.tokens.cpu().numpy())
+        if n:
+            e.verify_rows(n, rows, None, self.tokens, self.positions, self.page_table, None, self.v_tok, self.v_kvcol)
+            e.repair_kv_column(n, rows, None, self.positions, self.page_table, self.top1, self.v_tok, self.v_kvcol,
+                               self.top1, self.n_repaired)
+            if keep is not None:
+                keep.update(rows=rows[:n].cpu().numpy(), v_tok=self.v_tok[:n].cpu().numpy())
+        elif keep is not None:
+            keep.update(rows=np.zeros(0, np.int32), v_tok=np.zeros(0, np.int32))
+        e.advance(B, self.top1, self.tokens, self.positions)
+        self.steps += 1
+        self.protected_row_steps += int(self.always_rows.numel())
+        self.verified_row_steps += n
+        self.hist.append(n)
+        return n
+
+    @property
+    def r_verify(self):
+        return self.verified_row_steps / max(self.protected_row_steps, 1)
+
+    def r_repair(self):
+        return int(self.n_repaired.item()) / max(self.protected_row_steps, 1)
+
+
+def prefill_rows(engine: Engine, prompts, page_table, max_items: int = 1024):
+    """Canonical prefill of positions 0..len-2 of every prompt (the last prompt token is
+    consumed by the first decode step).  Items are issued in increasing position order, so
+    every earlier position of a row is in the cache before a later one attends to it."""
+    dev = engine.device
+    items = [(t, p, r) for r, pr in enumerate(prompts) for p, t in enumerate(pr[:-1])]
+    items.sort(key=lambda x: (x[1], x[2]))
+    pt = torch.as_tensor(np.asarray(page_table, np.int32)).to(dev).contiguous()
+    arr = np.asarray(items, np.int32).reshape(-1, 3)
+    for o in range(0, len(arr), max_items):
+        chunk = arr[o:o + max_items]
+        tok = torch.as_tensor(np.ascontiguousarray(chunk[:, 0])).to(dev)
+        pos = torch.as_tensor(np.ascontiguousarray(chunk[:, 1])).to(dev)
+        row = torch.as_tensor(np.ascontiguousarray(chunk[:, 2])).to(dev)
+        engine.prefill(len(chunk), tok, pos, row, pt)
+    torch.cuda.synchronize()
+    last = np.array([pr[-1] for pr in prompts], np.int32)
+    pos0 = np.array([len(pr) - 1 for pr in prompts], np.int32)
+    return last, pos0

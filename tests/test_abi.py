@@ -1,0 +1,95 @@
+"""The C-ABI library loads, exports every symbol include/*.h declares, and rejects bad
+host arguments without touching a GPU (no compute calls here)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2605_30218_amd import mg, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for f in os.listdir(os.path.join(ROOT, "include")):
+        if f.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", f)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(mg_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
+
+
+def test_every_declared_symbol_is_exported():
+    lib = mg.load()
+    names = declared_functions()
+    assert len(names) >= 20
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_binding_covers_every_declared_symbol():
+    assert sorted(mg.SIGNATURES) == declared_functions()
+
+
+def test_sizes_and_status_strings():
+    lib = mg.load()
+    cfg = mg.make_cfg(synth.TINY, 4, 4, 16)
+    assert lib.mg_weight_count(C.byref(cfg)) == 3 + 12 * synth.TINY.n_layers
+    s = synth.TINY
+    assert lib.mg_kv_pool_bytes(C.byref(cfg)) == s.n_layers * 16 * 2 * s.n_kv_heads * 16 * s.head_dim * 2
+    assert lib.mg_kv_col_elems(C.byref(cfg)) == s.kv_col_elems
+    assert lib.mg_workspace_bytes(C.byref(cfg)) > 0
+    assert lib.mg_status_string(-3) == b"workspace or KV pool too small"
+    assert lib.mg_status_string(0) == b"ok"
+
+
+@pytest.mark.parametrize("field,value", [("page_size", 8), ("head_dim", 96), ("max_batch", 0), ("max_batch", 300),
+                                         ("n_kv_heads", 3), ("d_model", 200)])
+def test_unsupported_shapes_have_no_workspace(field, value):
+    lib = mg.load()
+    cfg = mg.make_cfg(synth.TINY, 4, 4, 16)
+    setattr(cfg, field, value)
+    assert lib.mg_workspace_bytes(C.byref(cfg)) == 0
+
+
+def test_null_arguments_are_rejected_before_any_work():
+    lib = mg.load()
+    cfg = mg.make_cfg(synth.TINY, 4, 4, 16)
+    out = C.c_void_p()
+    assert lib.mg_create(None, None, None, 0, None, 0, C.byref(out)) == -1
+    assert lib.mg_create(C.byref(cfg), None, None, 0, None, 0, C.byref(out)) == -1
+    assert lib.mg_decode_step(None, 1, None, None, None, None, None) == -1
+    assert lib.mg_margin_gate(None, 1, None, None, 0.5, None, None, None, None, None, None) == -1
+    assert lib.mg_verify_rows(None, 1, None, None, None, None, None, None, None, None, None) == -1
+    assert lib.mg_repair_kv_column(None, 1, None, None, None, None, None, None, None, None, None, None) == -1
+    assert lib.mg_prefill(None, 1, None, None, None, None, None) == -1
+    assert lib.mg_advance(None, 1, None, None, None, None) == -1
+    assert lib.mg_profile_begin(None, 0, 1) == -1
+    assert lib.mg_destroy(None) == -1
+    assert lib.mg_op_linear(1, 0, 16, 8, None, None, None, None, None, 0, None) == -1
+    assert lib.mg_op_linear(1, 4, 15, 8, 1, 1, None, 1, None, 0, None) == -1   # N % 16
+    assert lib.mg_op_linear(1, 4, 16, 12, 1, 1, None, 1, None, 0, None) == -1  # K % 8
+    assert lib.mg_op_probe_exp(-1, None, None, None) == -1
+
+
+def test_create_rejects_small_buffers_and_missing_weights():
+    lib = mg.load()
+    cfg = mg.make_cfg(synth.TINY, 4, 4, 16)
+    nw = lib.mg_weight_count(C.byref(cfg))
+    fake = (C.c_void_p * nw)(*([1] * nw))
+    out = C.c_void_p()
+    kvb = lib.mg_kv_pool_bytes(C.byref(cfg))
+    wsb = lib.mg_workspace_bytes(C.byref(cfg))
+    assert lib.mg_create(C.byref(cfg), fake, 1, kvb - 2, 1, wsb, C.byref(out)) == -3
+    assert lib.mg_create(C.byref(cfg), fake, 1, kvb, 1, wsb - 1, C.byref(out)) == -3
+    fake[2] = None  # layer 0 wq (entry 1 + 12*0 + 1)
+    assert lib.mg_create(C.byref(cfg), fake, 1, kvb, 1, wsb, C.byref(out)) == -1
+
+
+def test_load_raises_when_library_missing(monkeypatch, tmp_path):
+    monkeypatch.setattr(mg, "_lib", None)
+    monkeypatch.setattr(mg, "LIB_PATH", str(tmp_path / "libmg.so"))
+    with pytest.raises(RuntimeError, match="no fallback"):
+        mg.load()

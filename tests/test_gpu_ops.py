@@ -1,0 +1,102 @@
+"""Op-level parity of the HIP kernels against the CPU oracle (GPU).
+
+Bit-exact: the device bf16 rounding, the verifier's EXP, IEEE fp32 division and square
+root, the canonical GEMV (CDOT order) and the canonical RMSNorm.  Tolerance: the fast
+MFMA GEMM, whose summation order is free; with small-integer inputs every order is exact,
+so it must then match bit for bit as well."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import mgo
+from paper_2605_30218_amd import mg, synth
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def to_dev_bf16(a_u16):
+    return torch.from_numpy(np.ascontiguousarray(a_u16).view(np.int16)).to(DEV)
+
+
+def test_bf16_rounding_bitexact():
+    upper = np.arange(1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF], np.uint32)
+    u = np.concatenate([(upper[:, None] | lows[None, :]).ravel(),
+                        np.random.default_rng(1).integers(0, 1 << 32, 2_000_000, dtype=np.uint64).astype(np.uint32)])
+    x = u.view(np.float32)
+    got = mg.op_probe_bf16(torch.from_numpy(x.copy()).to(DEV)).cpu().numpy().view(np.uint16)
+    np.testing.assert_array_equal(got, mgo.bf16_from_f32(x))
+
+
+def test_exp_bitexact_against_oracle():
+    x = np.concatenate([np.linspace(-104.0, 90.0, 4_000_001).astype(np.float32),
+                        np.float32([0.0, -0.0, np.inf, -np.inf, np.nan, 88.72, -87.33, -86.9, 1e-30, -1e-30]),
+                        (np.random.default_rng(2).standard_normal(1_000_000) * 10).astype(np.float32)])
+    got = mg.op_probe_exp(torch.from_numpy(x).to(DEV)).cpu().numpy()
+    ref = mgo.exp(x)
+    np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
+def test_division_and_sqrt_are_ieee():
+    rng = np.random.default_rng(3)
+    a = (rng.standard_normal(2_000_000) * np.exp2(rng.integers(-140, 120, 2_000_000))).astype(np.float32)
+    b = (rng.standard_normal(2_000_000) * np.exp2(rng.integers(-120, 120, 2_000_000))).astype(np.float32)
+    a = np.abs(a)
+    q, r = mg.op_probe_divsqrt(torch.from_numpy(a).to(DEV), torch.from_numpy(b).to(DEV))
+    with np.errstate(all="ignore"):
+        np.testing.assert_array_equal(q.cpu().numpy().view(np.uint32), (a / b).view(np.uint32))
+        np.testing.assert_array_equal(r.cpu().numpy().view(np.uint32), np.sqrt(a).view(np.uint32))
+
+
+@pytest.mark.parametrize("n,N,K", [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
+                                   (24, 16, 512), (5, 4096, 256)])
+def test_canonical_gemv_bitexact(n, N, K):
+    X = synth.random_bf16((n, K), seed=n * 7 + 1)
+    W = synth.random_bf16((N, K), seed=N + K, std=0.05)
+    Y = mg.op_linear(True, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
+    for r in range(n):
+        ref = mgo.linear(mgo.CANON, X[r], W, fp32=True)
+        np.testing.assert_array_equal(Y[r].view(np.uint32), ref.view(np.uint32), err_msg=f"row {r}")
+
+
+def test_canonical_gemv_row_result_independent_of_row_count_and_place():
+    K, N = 1032, 48
+    X = synth.random_bf16((40, K), seed=11)
+    W = synth.random_bf16((N, K), seed=12, std=0.05)
+    full = mg.op_linear(True, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
+    for rows in ([7], [39, 7], list(range(7, 20)), list(range(40))[::-1]):
+        part = mg.op_linear(True, to_dev_bf16(X[rows]), to_dev_bf16(W)).cpu().numpy()
+        np.testing.assert_array_equal(part.view(np.uint32), full[rows].view(np.uint32))
+
+
+@pytest.mark.parametrize("n,N,K", [(1, 64, 4096), (5, 48, 688), (16, 128, 4096), (33, 64, 14336), (64, 6144, 4096),
+                                   (100, 80, 1032), (256, 64, 512)])
+def test_fast_gemm_within_tolerance(n, N, K):
+    X = synth.random_bf16((n, K), seed=n + 3)
+    W = synth.random_bf16((N, K), seed=N + 5, std=0.02)
+    Y = mg.op_linear(False, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy().astype(np.float64)
+    ref = mgo.f32_from_bf16(X).astype(np.float64) @ mgo.f32_from_bf16(W).astype(np.float64).T
+    bound = K * 2.0 ** -23 * (np.abs(mgo.f32_from_bf16(X)).astype(np.float64) @
+                              np.abs(mgo.f32_from_bf16(W)).astype(np.float64).T) + 1e-30
+    assert np.all(np.abs(Y - ref) <= bound)
+
+
+@pytest.mark.parametrize("n,N,K", [(3, 48, 688), (64, 256, 4096), (130, 64, 1032)])
+def test_fast_gemm_small_integers_exact(n, N, K):
+    X = synth.small_int_bf16((n, K), seed=21)
+    W = synth.small_int_bf16((N, K), seed=22)
+    Y = mg.op_linear(False, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
+    ref = mgo.f32_from_bf16(X).astype(np.int64) @ mgo.f32_from_bf16(W).astype(np.int64).T
+    np.testing.assert_array_equal(Y, ref.astype(np.float32))
+    Yc = mg.op_linear(True, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
+    np.testing.assert_array_equal(Yc, ref.astype(np.float32))
+
+
+@pytest.mark.parametrize("d,eps", [(256, 1e-5), (4096, 1e-5), (3584, 1e-6), (5120, 1e-6), (688, 1e-5)])
+def test_rmsnorm_bitexact(d, eps):
+    x = synth.random_bf16((9, d), seed=d)
+    g = synth.random_bf16((d,), seed=d + 1)
+    y = mg.op_rmsnorm(to_dev_bf16(x), to_dev_bf16(g), eps).cpu().numpy().view(np.uint16)
+    for r in range(9):
+        np.testing.assert_array_equal(y[r], mgo.rmsnorm(mgo.CANON, x[r], g, eps))
