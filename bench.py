@@ -1,0 +1,210 @@
+"""Benchmark of the MarginGate decode step on one MI355X.
+
+Workload: a Llama-3.1-8B-shaped decoder (32 layers, d 4096, 32/8 heads, hd 128, FFN 14336,
+vocab 128256, RoPE theta 5e5) with random-init N(0, 0.02) bf16 weights, batch 64, uniform
+random 512-token prompts (canonical prefill, not timed), greedy decode.  Every row is
+protected.  Three modes run from the same prefilled state:
+  off     the BF16 fast path only (r_verify = 0)
+  gated   MarginGate: verify rows whose top-1/top-2 margin is below tau
+  always  the verifier on every row and step (the always-on baseline, r_verify = 1)
+tau is calibrated on fast-path margins so that the trigger rate matches the paper's
+Llama-3.1-8B operating point (18.56%); the measured rate is reported.
+
+One JSON line on stdout: value = gated decode tokens/s (B * steps / time of the timed
+steps, inputs resident in HBM), plus the other modes, the verifier overhead
+(inc_mode = T_mode / T_off - 1, cut = inc_always / inc_gated), the roofline of the
+dominant kernel measured with HIP events over the timed region, and the CPU oracle
+baseline on a bounded sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2605_30218_amd import mg, synth  # noqa: E402
+from paper_2605_30218_amd.runtime import GatedDecoder, prefill_fast, prefill_rows  # noqa: E402
+
+METRIC = "decode tok/s + gated-vs-always-on verifier overhead, Llama-3.1-8B-shape bs=64"
+HBM_PEAK = 8.0e12            # B/s, MI355X
+FP32_VALU_PEAK = 78.6e12     # flop/s: 256 CU x 4 SIMD x 16 lanes x 2 (fma) x 2.4 GHz, no packed fp32
+PAPER_TRIGGER = 0.1856       # Llama-3.1-8B trigger rate at tau_100 (paper Sec. 5.3)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def run_mode(dec, mode, warmup, steps, state, kv_snap, eng, profile_kinds=()):
+    eng.kv_pool.copy_(kv_snap)
+    dec.set_state(*state)
+    dec.n_repaired.zero_()
+    for _ in range(warmup):
+        dec.step(mode)
+    torch.cuda.synchronize()
+    dec.protected_row_steps = dec.verified_row_steps = 0
+    dec.hist = []
+    dec.n_repaired.zero_()
+    prof_steps = min(steps, 64)   # event pairs are recorded around the launches of the first 64 timed steps
+    for k in profile_kinds:
+        eng.profile_begin(k, prof_steps * (4 * eng.shape.n_layers + 1))
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev[0].record()
+    for s in range(steps):
+        dec.step(mode)
+        ev[s + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([ev[s].elapsed_time(ev[s + 1]) for s in range(steps)])
+    prof = {k: eng.profile_end(k) for k in profile_kinds}
+    B = dec.B
+    return dict(ms_per_step=wall * 1e3 / steps, tok_s=B * steps / wall, p50_ms=float(np.median(per)),
+                p99_ms=float(np.percentile(per, 99)), r_verify=dec.r_verify, r_repair=dec.r_repair(),
+                verified_rows_per_step=float(np.mean(dec.hist)), prof=prof)
+
+
+def calibrate_tau(dec, eng, state, kv_snap, steps, rate):
+    eng.kv_pool.copy_(kv_snap)
+    dec.set_state(*state)
+    ms = []
+    for _ in range(steps):
+        dec.step("off")
+        ms.append(dec.margin.cpu().numpy().copy())
+    return float(np.quantile(np.concatenate(ms), rate))
+
+
+def cpu_baseline(shape, weights, eng, pt, state, rows, steps):
+    """The oracle (plain mode, as it stands) on host cores: `rows` rows x `steps` steps of the
+    same workload, started from the GPU's prefilled cache of those rows."""
+    from oracle import mgo
+    last, pos = state
+    wn = synth.weights_to_numpy(weights)
+    maxp = pt.shape[1]
+    n_pages = len(rows) * maxp
+    om = mgo.OracleModel(shape, wn, len(rows), maxp, n_pages)
+    kv = eng.kv_view()
+    src_pages = torch.as_tensor(pt[rows].reshape(-1).astype(np.int64)).cuda()
+    om.kv_view()[:] = kv[:, src_pages].cpu().numpy().view(np.uint16)
+    ptl = np.arange(n_pages, dtype=np.int32).reshape(len(rows), maxp)
+    toks, poss = last[rows].copy(), pos[rows].copy()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        lg = om.decode_step(mgo.PLAIN, toks, poss, ptl)
+        toks, poss = lg.argmax(1).astype(np.int32), poss + 1
+    dt = time.perf_counter() - t0
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return dict(value=len(rows) * steps / dt, unit="tok/s", cores=threads, kind="oracle",
+                sample=f"{len(rows)} rows x {steps} decode step(s) of the same workload (plain mode, context "
+                       f"{int(pos[rows].min())}+), {dt:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--batch", type=int, default=64)
+    ap.add_argument("--prompt", type=int, default=512)
+    ap.add_argument("--modes", default="off,gated,always")
+    ap.add_argument("--always-steps", type=int, default=0, help="timed steps of the always mode (0 = --steps)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=4)
+    ap.add_argument("--cpu-steps", type=int, default=2)
+    ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--prefill", choices=("canonical", "fast"), default="canonical",
+                    help="prompt prefill before the timed steps (not timed)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (rows are independent, so "
+              "the path scales by data parallelism over requests with no exchange; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    torch.cuda.set_device(0)
+    mg.load()
+    shape = synth.LLAMA8B
+    B, P = args.batch, args.prompt
+    always_steps = args.always_steps or args.steps
+    ctx_cap = P + args.warmup + max(args.steps, always_steps) + 16
+    maxp = -(-ctx_cap // shape.page_size)
+    pt, n_pages = synth.make_page_table([ctx_cap] * B, shape.page_size, maxp, seed=5)
+    log(f"[bench] weights {shape.name} on GPU (seed 0)")
+    weights = synth.make_weights(shape, seed=0, device="cuda")
+    eng = mg.Engine(shape, weights, B, maxp, n_pages, max_prefill=1024)
+    prompts = synth.make_prompts(B, [P] * B, shape.vocab, seed=1)
+    log(f"[bench] {args.prefill} prefill {B} x {P - 1} tokens")
+    t0 = time.perf_counter()
+    last, pos0 = (prefill_rows if args.prefill == "canonical" else prefill_fast)(eng, prompts, pt)
+    prefill_s = time.perf_counter() - t0
+    log(f"[bench] prefill {prefill_s:.1f} s")
+    kv_snap = eng.kv_pool.clone()
+    state = (last, pos0)
+    dec = GatedDecoder(eng, pt, None, tau=0.0)
+    tau = args.tau if args.tau is not None else calibrate_tau(dec, eng, state, kv_snap, 8, PAPER_TRIGGER)
+    dec.tau = tau
+    log(f"[bench] tau = {tau:.5f}")
+    modes = {}
+    for mode in args.modes.split(","):
+        steps = always_steps if mode == "always" else args.steps
+        kinds = (mg.KIND_FAST_GEMM, mg.KIND_CANON_GEMV, mg.KIND_FAST_ATTN, mg.KIND_CANON_ATTN) \
+            if mode == "gated" else ()
+        log(f"[bench] mode {mode}: {args.warmup} warmup + {steps} timed steps")
+        modes[mode] = run_mode(dec, mode, args.warmup, steps, state, kv_snap, eng, kinds)
+        log(f"[bench] mode {mode}: {modes[mode]['ms_per_step']:.3f} ms/step, {modes[mode]['tok_s']:.0f} tok/s, "
+            f"r_verify {modes[mode]['r_verify']:.4f}")
+    g = modes.get("gated") or next(iter(modes.values()))
+    prof = g.pop("prof")
+    for m in modes.values():
+        m.pop("prof", None)
+    # roofline of the dominant kernel of the gated step
+    names = {mg.KIND_FAST_GEMM: "fast_gemm", mg.KIND_CANON_GEMV: "canon_gemv", mg.KIND_FAST_ATTN: "fast_attention",
+             mg.KIND_CANON_ATTN: "canon_attention"}
+    kernels = {}
+    for k, (n, ms, b, f) in prof.items():
+        kernels[names[k]] = dict(launches=n, total_ms=ms, avg_us=1e3 * ms / max(n, 1), algo_bytes=b, algo_flops=f,
+                                 gbps=b / (ms * 1e-3) / 1e9 if ms > 0 else 0.0,
+                                 tflops=f / (ms * 1e-3) / 1e12 if ms > 0 else 0.0)
+    roofline = None
+    if kernels:
+        dom = max(kernels, key=lambda k: kernels[k]["total_ms"])
+        kd = kernels[dom]
+        sec = kd["total_ms"] * 1e-3
+        hbm = kd["algo_bytes"] / sec
+        alu = kd["algo_flops"] / sec
+        if dom == "canon_gemv" and alu / FP32_VALU_PEAK > hbm / HBM_PEAK:
+            roofline = dict(kernel=dom, bound="alu", achieved=alu / 1e12, peak=FP32_VALU_PEAK / 1e12, unit="TFLOP/s",
+                            frac=alu / FP32_VALU_PEAK, traffic=None, launches=kd["launches"])
+        else:
+            roofline = dict(kernel=dom, bound="hbm", achieved=hbm / 1e9, peak=HBM_PEAK / 1e9, unit="GB/s",
+                            frac=hbm / HBM_PEAK, traffic=None, launches=kd["launches"])
+    out = dict(metric=METRIC, value=g["tok_s"], unit="tok/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
+               ms_per_step=g["ms_per_step"], higher_is_better=True, scaling="weak", vs_baseline=None, dtype="bf16",
+               data="synthetic",
+               config=dict(workload=f"Llama-3.1-8B-shaped random-init decoder, batch {B}, uniform random {P}-token "
+                                    f"prompts, gated greedy decode (all rows protected, tau for an 18.56% trigger)",
+                           global_batch=B, seq_len=P, parallelism="single GPU"),
+               roofline=roofline, tau=tau, prefill=args.prefill, prefill_s=prefill_s, modes=modes, kernels=kernels)
+    if "off" in modes:
+        t_off = modes["off"]["ms_per_step"]
+        ov = {}
+        for m in ("gated", "always"):
+            if m in modes:
+                ov[f"inc_{m}"] = modes[m]["ms_per_step"] / t_off - 1
+        if "inc_gated" in ov and "inc_always" in ov and ov["inc_gated"] > 0:
+            ov["cut"] = ov["inc_always"] / ov["inc_gated"]
+        out["verifier_overhead"] = ov
+    if not args.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle)")
+        eng.kv_pool.copy_(kv_snap)
+        out["cpu_baseline"] = cpu_baseline(shape, weights, eng, pt, state, np.arange(args.cpu_rows), args.cpu_steps)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

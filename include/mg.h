@@ -174,10 +174,11 @@ enum {
  * events (not allocation-free; call outside timed loops). */
 mg_status mg_profile_begin(mg_ctx* ctx, int kind, int max_launches);
 /* Stop recording, synchronise the recorded events and report the number of
- * launches, their summed duration in milliseconds and the summed algorithmic
- * bytes (weights + activations + KV read, per launch, as the kernel's
- * definition of its traffic). */
-mg_status mg_profile_end(mg_ctx* ctx, int kind, int* n_launches, double* total_ms, double* algo_bytes);
+ * launches, their summed duration in milliseconds, the summed algorithmic bytes
+ * (every weight, activation, K/V and output byte the launch must move once) and
+ * the summed algorithmic flops (2 per multiply-add). */
+mg_status mg_profile_end(mg_ctx* ctx, int kind, int* n_launches, double* total_ms, double* algo_bytes,
+                         double* algo_flops);
 
 #ifdef __cplusplus
 }

@@ -119,6 +119,7 @@ struct ProfKind {
     int used = 0;
     std::vector<hipEvent_t> ev0, ev1;
     double bytes = 0.0;
+    double flops = 0.0;
 };
 
 struct mg_ctx {
@@ -141,9 +142,10 @@ namespace {
 struct ProfScope {
     ProfKind* k;
     hipStream_t s;
-    double bytes;
+    double bytes, flops;
     int idx;
-    ProfScope(mg_ctx* c, int kind, hipStream_t st, double b) : k(&c->prof[kind]), s(st), bytes(b), idx(-1) {
+    ProfScope(mg_ctx* c, int kind, hipStream_t st, double b, double f = 0.0)
+        : k(&c->prof[kind]), s(st), bytes(b), flops(f), idx(-1) {
         if (k->on && k->used < k->max) {
             idx = k->used++;
             hipEventRecord(k->ev0[idx], s);
@@ -153,6 +155,7 @@ struct ProfScope {
         if (idx >= 0) {
             hipEventRecord(k->ev1[idx], s);
             k->bytes += bytes;
+            k->flops += flops;
         }
     }
 };
@@ -184,7 +187,7 @@ mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, int swiglu, cons
     a.S = fast_gemm_splits(M, N, K, c->n_cu);
     const double bytes = 2.0 * N * K + 2.0 * M * K * (swiglu ? 2 : 1) + (double)M * N * (epi == FEPI_F32 ? 4 : 2) *
                                                                         (epi == FEPI_RESID ? 2 : 1);
-    ProfScope ps(c, MG_KIND_FAST_GEMM, s, bytes);
+    ProfScope ps(c, MG_KIND_FAST_GEMM, s, bytes, 2.0 * M * N * K);
     HIPCHK(launch_fast_gemm(a, epi, s));
     return MG_OK;
 }
@@ -210,7 +213,7 @@ mg_status canon_gemv(mg_ctx* c, const uint16_t* X, int n, const int32_t* n_dev, 
     const int rows = n_dev ? cap : n;
     const double bytes = 2.0 * N * K + 2.0 * rows * K + (double)rows * N * (epi == EPI_F32 ? 4 : 2) *
                                                         (epi == EPI_RESID ? 2 : 1);
-    ProfScope ps(c, MG_KIND_CANON_GEMV, s, bytes);
+    ProfScope ps(c, MG_KIND_CANON_GEMV, s, bytes, 2.0 * rows * N * K);
     HIPCHK(launch_canon_gemv(a, epi, s));
     return MG_OK;
 }
@@ -527,11 +530,14 @@ mg_status mg_profile_begin(mg_ctx* c, int kind, int max_launches) {
     k.max = max_launches;
     k.used = 0;
     k.bytes = 0.0;
+    k.flops = 0.0;
     return MG_OK;
 }
 
-mg_status mg_profile_end(mg_ctx* c, int kind, int* n_launches, double* total_ms, double* algo_bytes) {
-    if (!c || kind < 0 || kind >= MG_KIND_COUNT || !n_launches || !total_ms || !algo_bytes) return MG_ERR_ARG;
+mg_status mg_profile_end(mg_ctx* c, int kind, int* n_launches, double* total_ms, double* algo_bytes,
+                         double* algo_flops) {
+    if (!c || kind < 0 || kind >= MG_KIND_COUNT || !n_launches || !total_ms || !algo_bytes || !algo_flops)
+        return MG_ERR_ARG;
     ProfKind& k = c->prof[kind];
     k.on = false;
     double tot = 0.0;
@@ -544,6 +550,7 @@ mg_status mg_profile_end(mg_ctx* c, int kind, int* n_launches, double* total_ms,
     *n_launches = k.used;
     *total_ms = tot;
     *algo_bytes = k.bytes;
+    *algo_flops = k.flops;
     return MG_OK;
 }
 

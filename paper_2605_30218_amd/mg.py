@@ -52,7 +52,7 @@ SIGNATURES = {
     "mg_prefill": (I, [P, I, P, P, P, P, P]),
     "mg_advance": (I, [P, I, P, P, P, P]),
     "mg_profile_begin": (I, [P, I, I]),
-    "mg_profile_end": (I, [P, I, P, P, P]),
+    "mg_profile_end": (I, [P, I, P, P, P, P]),
     "mg_op_probe_bf16": (I, [I64, P, P, P]),
     "mg_op_probe_exp": (I, [I64, P, P, P]),
     "mg_op_probe_divsqrt": (I, [I64, P, P, P, P, P]),
@@ -178,9 +178,10 @@ class Engine:
         _check("mg_profile_begin", self.lib.mg_profile_begin(self.ctx, kind, max_launches))
 
     def profile_end(self, kind):
-        n, ms, b = C.c_int(), C.c_double(), C.c_double()
-        _check("mg_profile_end", self.lib.mg_profile_end(self.ctx, kind, C.byref(n), C.byref(ms), C.byref(b)))
-        return n.value, ms.value, b.value
+        n, ms, b, f = C.c_int(), C.c_double(), C.c_double(), C.c_double()
+        _check("mg_profile_end", self.lib.mg_profile_end(self.ctx, kind, C.byref(n), C.byref(ms), C.byref(b),
+                                                         C.byref(f)))
+        return n.value, ms.value, b.value, f.value
 
 
 # ---------------------------------------------------------------- op-level calls (tests)

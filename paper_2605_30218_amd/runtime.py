@@ -112,3 +112,22 @@ def prefill_rows(engine: Engine, prompts, page_table, max_items: int = 1024):
     last = np.array([pr[-1] for pr in prompts], np.int32)
     pos0 = np.array([len(pr) - 1 for pr in prompts], np.int32)
     return last, pos0
+
+
+def prefill_fast(engine: Engine, prompts, page_table):
+    """Prompt prefill through the fast path: teacher-forced decode steps over positions
+    0..len-2, all rows still in their prompt advancing together.  Cheaper than the canonical
+    prefill; its cache depends on the batch shape like every fast-path column."""
+    dev = engine.device
+    pt = np.asarray(page_table, np.int32)
+    lens = np.array([len(p) for p in prompts])
+    logits = torch.empty((len(prompts), engine.shape.vocab), dtype=torch.float32, device=dev)
+    for t in range(int(lens.max()) - 1):
+        act = np.nonzero(lens - 1 > t)[0]
+        tok = torch.as_tensor(np.array([prompts[r][t] for r in act], np.int32)).to(dev)
+        pos = torch.full((act.size,), t, dtype=torch.int32, device=dev)
+        ptr = torch.as_tensor(np.ascontiguousarray(pt[act])).to(dev)
+        engine.decode_step(int(act.size), tok, pos, ptr, logits)
+    torch.cuda.synchronize()
+    last = np.array([pr[-1] for pr in prompts], np.int32)
+    return last, (lens - 1).astype(np.int32)
