@@ -119,6 +119,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=4)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run the plain copy kernel on MIB MiB five times (HBM counter scaling) and exit")
     ap.add_argument("--prefill", choices=("canonical", "fast"), default="canonical",
                     help="prompt prefill before the timed steps (not timed)")
     args = ap.parse_args()
@@ -128,6 +130,15 @@ def main():
         sys.exit(2)
     torch.cuda.set_device(0)
     mg.load()
+    if args.copy_calibration:
+        nb = args.copy_calibration << 20
+        src = torch.ones(nb // 4, dtype=torch.int32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            mg.op_copy(src, dst)
+        torch.cuda.synchronize()
+        print(json.dumps(dict(copy_bytes=nb, launches=5)))
+        return
     shape = synth.LLAMA8B
     B, P = args.batch, args.prompt
     always_steps = args.always_steps or args.steps

@@ -17,6 +17,11 @@
 extern "C" {
 #endif
 
+/* dst[0..n_bytes) = src[0..n_bytes) with a plain 16-byte-per-lane copy kernel that
+ * reads and writes every byte once: the reference for scaling HBM byte counters.
+ * n_bytes % 16 == 0; src and dst 16-byte aligned [device]. */
+mg_status mg_op_copy(int64_t n_bytes, const void* src, void* dst, void* stream);
+
 /* out[i] = bf16 round-to-nearest-even of in[i] (NaN -> quiet NaN), the device
  * conversion used at every bf16 rounding point.  in fp32 [n], out uint16 [n]. */
 mg_status mg_op_probe_bf16(int64_t n, const float* in, uint16_t* out, void* stream);

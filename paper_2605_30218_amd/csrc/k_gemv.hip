@@ -6,13 +6,18 @@
 //   groups of 8 consecutive K elements; group g belongs to lane g mod 64; each
 //   lane fma-accumulates its groups in increasing g (element order inside the
 //   group) starting from +0; the 64 lane sums are combined by the xor butterfly
-//   over offsets 32, 16, 8, 4, 2, 1.
+//   over offsets 32, 16, 8, 4, 2, 1 (all J*R butterflies of a wave are run
+//   together with the same pairings, see butterfly_sum_multi).
 // A wave owns J features; a block of 4 waves owns 4J features and a tile of R
-// rows.  The K dimension is walked in chunks of 512 elements (one group per
-// lane): the block stages the chunk of its R rows in LDS as fp32, every wave
-// streams one 16-byte weight group per feature and lane (1 KiB coalesced per
-// feature) and applies it to all R rows.  No split-K, no atomics: a row's
-// arithmetic is the same whatever R, J, the tile or the row count.
+// rows.  K is walked in chunks of 512 elements (one group per lane).  While the
+// fma work of chunk c runs, the weights of chunk c+1 are in flight (register
+// double buffer: one 16-byte group per feature and lane, 1 KiB coalesced per
+// feature) and the rows' activations of chunk c+1 are staged into the other half
+// of a double-buffered fp32 LDS tile.  One barrier per chunk; no split-K, no
+// atomics: a row's arithmetic is the same whatever R, J, the tile or the count.
+// Block order: the row tiles of one feature block get consecutive slots on the
+// same XCD (blocks are dealt to the 8 XCDs round-robin), so they share its L2
+// copy of the weights.
 #include "mg_device.h"
 #include "mg_kernels.h"
 
@@ -20,19 +25,61 @@ namespace mg {
 
 constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
 
+template <int R>
+struct GemvShape {
+    static constexpr int XLD = R * 64 / 256;  // staging loads (16 bytes) per thread per chunk
+};
+
+template <int R>
+__device__ __forceinline__ void gemv_load_x(const GemvArgs& a, int r0, int nr, int kc, uint4 (&xr)[GemvShape<R>::XLD]) {
+#pragma unroll
+    for (int it = 0; it < GemvShape<R>::XLD; ++it) {
+        const int t = threadIdx.x + 256 * it;
+        const int rr = t >> 6, gl = t & 63;
+        const int k = kc + gl * 8;
+        xr[it] = (rr < nr && k < a.K) ? *reinterpret_cast<const uint4*>(a.X + (size_t)(r0 + rr) * a.K + k)
+                                      : make_uint4(0, 0, 0, 0);
+    }
+}
+
+template <int R>
+__device__ __forceinline__ void gemv_store_x(float4 (*xs)[2][64], const uint4 (&xr)[GemvShape<R>::XLD]) {
+#pragma unroll
+    for (int it = 0; it < GemvShape<R>::XLD; ++it) {
+        const int t = threadIdx.x + 256 * it;
+        const int rr = t >> 6, gl = t & 63;
+        const uint4 v = xr[it];
+        xs[rr][0][gl] = make_float4(bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y));
+        xs[rr][1][gl] = make_float4(bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w));
+    }
+}
+
+template <int J>
+__device__ __forceinline__ void gemv_load_w(const uint16_t* const (&wrow)[J], const bool (&valid)[J], int g, int G,
+                                            uint4 (&w)[J]) {
+#pragma unroll
+    for (int jj = 0; jj < J; ++jj)
+        w[jj] = (valid[jj] && g < G) ? *reinterpret_cast<const uint4*>(wrow[jj] + (size_t)g * 8) : make_uint4(0, 0, 0, 0);
+}
+
 template <int J, int R, int EPI>
-__global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a) {
+__global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, int n_rt) {
+    const int b = blockIdx.x;
+    const int xcd = b & 7, slot = b >> 3;
+    const int fb = (slot / n_rt) * 8 + xcd;
+    const int rt = slot % n_rt;
+    if (fb >= n_fb) return;
     RowCount rc{a.n_dev, a.n_host, a.cap};
     const int n = rc.get();
-    const int r0 = blockIdx.x * R;
+    const int r0 = rt * R;
     if (r0 >= n) return;
     const int nr = min(R, n - r0);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int jw = (blockIdx.y * 4 + wave) * J;
+    const int jw = (fb * 4 + wave) * J;
     const int K = a.K, G = K >> 3;
 
-    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[rr][half][lane].c
-    __shared__ float4 xs[R][2][64];
+    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[buf][rr][half][lane].c
+    __shared__ float4 xs[2][R][2][64];
 
     const uint16_t* wrow[J];
     bool valid[J];
@@ -51,31 +98,32 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a) {
 #pragma unroll
         for (int rr = 0; rr < R; ++rr) acc[jj][rr] = 0.0f;
 
-    for (int kc = 0; kc < K; kc += KCH) {
-        __syncthreads();
-        for (int t = threadIdx.x; t < R * 64; t += 256) {
-            const int rr = t >> 6, gl = t & 63;
-            const int k = kc + gl * 8;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (rr < nr && k < K) v = *reinterpret_cast<const uint4*>(a.X + (size_t)(r0 + rr) * K + k);
-            xs[rr][0][gl] = make_float4(bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y));
-            xs[rr][1][gl] = make_float4(bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w));
+    const int nch = (K + KCH - 1) / KCH;
+    uint4 wcur[J], wnext[J];
+    uint4 xr[GemvShape<R>::XLD];
+    gemv_load_w<J>(wrow, valid, lane, G, wcur);
+    gemv_load_x<R>(a, r0, nr, 0, xr);
+    gemv_store_x<R>(xs[0], xr);
+    __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+        const bool more = c + 1 < nch;
+        if (more) {
+            gemv_load_w<J>(wrow, valid, (c + 1) * 64 + lane, G, wnext);
+            gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, xr);
         }
-        __syncthreads();
-        const int g = (kc >> 3) + lane;
-        if (g < G) {
+        if (c * 64 + lane < G) {
             float w[J][8];
 #pragma unroll
             for (int jj = 0; jj < J; ++jj) {
-                uint4 v = make_uint4(0, 0, 0, 0);
-                if (valid[jj]) v = *reinterpret_cast<const uint4*>(wrow[jj] + (size_t)g * 8);
+                const uint4 v = wcur[jj];
                 w[jj][0] = bf_lo(v.x); w[jj][1] = bf_hi(v.x); w[jj][2] = bf_lo(v.y); w[jj][3] = bf_hi(v.y);
                 w[jj][4] = bf_lo(v.z); w[jj][5] = bf_hi(v.z); w[jj][6] = bf_lo(v.w); w[jj][7] = bf_hi(v.w);
             }
+            float4(*xb)[2][64] = xs[c & 1];
 #pragma unroll
             for (int rr = 0; rr < R; ++rr) {
                 if (rr >= nr) break;
-                const float4 x0 = xs[rr][0][lane], x1 = xs[rr][1][lane];
+                const float4 x0 = xb[rr][0][lane], x1 = xb[rr][1][lane];
 #pragma unroll
                 for (int jj = 0; jj < J; ++jj) {
                     float s = acc[jj][rr];
@@ -91,39 +139,53 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a) {
                 }
             }
         }
+        if (more) gemv_store_x<R>(xs[(c + 1) & 1], xr);
+        __syncthreads();
+        if (more) {
+#pragma unroll
+            for (int jj = 0; jj < J; ++jj) wcur[jj] = wnext[jj];
+        }
     }
 
-    // butterfly, then lane (jj*R + rr) % 64 writes result (jj, rr); every lane holds it
+    // all J*R butterflies at once; value jj*R + rr ends in the lanes multi_index names
+    float flat[J * R];
 #pragma unroll
-    for (int jj = 0; jj < J; ++jj) {
+    for (int jj = 0; jj < J; ++jj)
 #pragma unroll
-        for (int rr = 0; rr < R; ++rr) {
-            const float v = butterfly_sum(acc[jj][rr]);
-            if (lane != ((jj * R + rr) & 63) || rr >= nr || !valid[jj]) continue;
-            const int j = jw + jj, row = r0 + rr;
-            if (EPI == EPI_F32) {
-                reinterpret_cast<float*>(a.Y)[(size_t)row * a.N + j] = v;
-            } else if (EPI == EPI_BF16) {
-                int jl = j, seg = 0;
-                while (seg < 2 && jl >= a.Nseg[seg]) { jl -= a.Nseg[seg]; ++seg; }
-                const float y = a.bias[seg] ? v + bf2f(a.bias[seg][jl]) : v;
-                reinterpret_cast<uint16_t*>(a.Y)[(size_t)row * a.N + j] = (uint16_t)f2bf(y);
-            } else {  // residual: x = bf16(x + bf16(y))
-                uint16_t* xr = reinterpret_cast<uint16_t*>(a.Y) + (size_t)row * a.N + j;
-                const float y = bf2f(f2bf(v));
-                *xr = (uint16_t)f2bf(bf2f(*xr) + y);
-            }
-        }
+        for (int rr = 0; rr < R; ++rr) flat[jj * R + rr] = acc[jj][rr];
+    const float v = butterfly_sum_multi<J * R>(flat, lane);
+    bool writer;
+    const int idx = multi_index<J * R>(lane, &writer);
+    const int jj = idx / R, rr = idx % R;
+    bool ok = writer && rr < nr;
+#pragma unroll
+    for (int k = 0; k < J; ++k)
+        if (k == jj) ok = ok && valid[k];
+    if (!ok) return;
+    const int j = jw + jj, row = r0 + rr;
+    if (EPI == EPI_F32) {
+        reinterpret_cast<float*>(a.Y)[(size_t)row * a.N + j] = v;
+    } else if (EPI == EPI_BF16) {
+        int jl = j, seg = 0;
+        while (seg < 2 && jl >= a.Nseg[seg]) { jl -= a.Nseg[seg]; ++seg; }
+        const float y = a.bias[seg] ? v + bf2f(a.bias[seg][jl]) : v;
+        reinterpret_cast<uint16_t*>(a.Y)[(size_t)row * a.N + j] = (uint16_t)f2bf(y);
+    } else {  // residual: x = bf16(x + bf16(y))
+        uint16_t* xr2 = reinterpret_cast<uint16_t*>(a.Y) + (size_t)row * a.N + j;
+        const float y = bf2f(f2bf(v));
+        *xr2 = (uint16_t)f2bf(bf2f(*xr2) + y);
     }
 }
 
 template <int J, int R>
 static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s) {
-    dim3 grid((rows + R - 1) / R, (a.N + 4 * J - 1) / (4 * J));
+    const int n_fb = (a.N + 4 * J - 1) / (4 * J);
+    const int n_rt = (rows + R - 1) / R;
+    const dim3 grid(8 * ((n_fb + 7) / 8) * n_rt);
     switch (epi) {
-        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16>), grid, dim3(256), 0, s, a); break;
-        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID>), grid, dim3(256), 0, s, a); break;
-        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32>), grid, dim3(256), 0, s, a); break;
+        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16>), grid, dim3(256), 0, s, a, n_fb, n_rt); break;
+        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID>), grid, dim3(256), 0, s, a, n_fb, n_rt); break;
+        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32>), grid, dim3(256), 0, s, a, n_fb, n_rt); break;
     }
     return hipGetLastError();
 }
@@ -131,8 +193,9 @@ static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s)
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
-    if (rows <= 8) return launch_jr<4, 8>(a, epi, rows, s);
-    return launch_jr<4, 16>(a, epi, rows, s);
+    const bool wide = a.N >= 8192;
+    if (rows > 8) return wide ? launch_jr<4, 16>(a, epi, rows, s) : launch_jr<2, 16>(a, epi, rows, s);
+    return wide ? launch_jr<4, 8>(a, epi, rows, s) : launch_jr<2, 8>(a, epi, rows, s);
 }
 
 }  // namespace mg

@@ -359,6 +359,19 @@ __global__ void probe_divsqrt_kernel(int64_t n, const float* a, const float* b, 
     }
 }
 
+// plain 16-byte copy: reads and writes n16 * 16 bytes once (counter calibration)
+__global__ __launch_bounds__(256) void copy16_kernel(int64_t n16, const uint4* __restrict__ src, uint4* __restrict__ dst) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
+        dst[i] = src[i];
+}
+
+hipError_t launch_copy16(int64_t n16, const void* src, void* dst, hipStream_t s) {
+    if (n16 <= 0) return hipSuccess;
+    hipLaunchKernelGGL(copy16_kernel, dim3(8192), dim3(256), 0, s, n16, static_cast<const uint4*>(src),
+                       static_cast<uint4*>(dst));
+    return hipGetLastError();
+}
+
 static int probe_grid(int64_t n) { return (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096); }
 
 hipError_t launch_probe_bf16(int64_t n, const float* in, uint16_t* out, hipStream_t s) {

@@ -54,11 +54,6 @@ void fast_projs(const mg_model_cfg* c, ProjShape out[5]) {
     out[4] = {c->vocab, d};
 }
 
-int fast_chunk_for(int max_pos) {
-    // fast attention: shorter chunks when contexts are short, so the grid fills the chip
-    (void)max_pos;
-    return 256;
-}
 
 Plan make_plan(const mg_model_cfg* c, int n_cu) {
     Plan p{};
@@ -84,14 +79,13 @@ Plan make_plan(const mg_model_cfg* c, int n_cu) {
     p.attn_part = o; o += up((ap_canon > ap_fast ? ap_canon : ap_fast) * sizeof(float));
     ProjShape ps[5];
     fast_projs(c, ps);
-    // split-K partials: S * M * N floats; S depends on M only through the chunk
-    // size, so the largest need is at M = min(64, max_batch) or at max_batch
+    // split-K partial tiles of the QKV, O, gate/up and down projections: S * M * N
+    // floats for every batch size the context accepts (the LM head is not split)
     size_t gp = 0;
-    const int Ms[2] = {c->max_batch < 64 ? c->max_batch : 64, c->max_batch};
-    for (int mi = 0; mi < 2; ++mi)
-        for (int k = 0; k < 5; ++k) {
-            const int S = fast_gemm_splits(Ms[mi], ps[k].N, ps[k].K, n_cu);
-            const size_t need = S > 1 ? (size_t)S * Ms[mi] * ps[k].N : 0;
+    for (int M = 1; M <= c->max_batch; ++M)
+        for (int k : {0, 1, 2, 3}) {
+            const int S = fast_gemm_splits(M, ps[k].N, ps[k].K, n_cu);
+            const size_t need = (size_t)S * M * ps[k].N;
             if (need > gp) gp = need;
         }
     p.gemm_part = o; o += up((gp ? gp : 1) * sizeof(float));
@@ -166,8 +160,11 @@ struct ProfScope {
         if (e_ != hipSuccess) return MG_ERR_HIP;    \
     } while (0)
 
+// One fast projection.  FEPI_PART writes S split partial tiles (returned in *S_out)
+// for the consuming kernel to sum; the other epilogues run unsplit.
 mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, int swiglu, const uint16_t* const* W,
-                    const uint16_t* const* bias, const int* Nseg, int nseg, void* Y, int epi, hipStream_t s) {
+                    const uint16_t* const* bias, const int* Nseg, int nseg, void* Y, int epi, hipStream_t s,
+                    int* S_out = nullptr) {
     FastGemmArgs a{};
     a.X = X;
     a.M = M;
@@ -183,10 +180,10 @@ mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, int swiglu, cons
     a.N = N;
     a.Y = Y;
     a.part = c->at<float>(c->plan.gemm_part);
-    a.tickets = c->at<int32_t>(c->plan.tickets);
-    a.S = fast_gemm_splits(M, N, K, c->n_cu);
-    const double bytes = 2.0 * N * K + 2.0 * M * K * (swiglu ? 2 : 1) + (double)M * N * (epi == FEPI_F32 ? 4 : 2) *
-                                                                        (epi == FEPI_RESID ? 2 : 1);
+    a.S = epi == FEPI_PART ? fast_gemm_splits(M, N, K, c->n_cu) : 1;
+    if (S_out) *S_out = a.S;
+    const double out_bytes = epi == FEPI_PART ? 4.0 * a.S * M * N : (double)M * N * (epi == FEPI_F32 ? 4 : 2);
+    const double bytes = 2.0 * N * K + 2.0 * M * K * (swiglu ? 2 : 1) + out_bytes;
     ProfScope ps(c, MG_KIND_FAST_GEMM, s, bytes, 2.0 * M * N * K);
     HIPCHK(launch_fast_gemm(a, epi, s));
     return MG_OK;
@@ -404,18 +401,23 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
     uint16_t* qkv = c->at<uint16_t>(c->plan.qkv);
     uint16_t* qrot = c->at<uint16_t>(c->plan.qrot);
     uint16_t* att = c->at<uint16_t>(c->plan.att);
-    uint16_t* gu = c->at<uint16_t>(c->plan.gu);
-    const int chunk = fast_chunk_for(c->plan.max_pos);
-    HIPCHK(launch_embed(it, c->W(0), d, x, s));
+    uint16_t* act = c->at<uint16_t>(c->plan.act);
+    const int chunk = fast_attention_split();
+    float* part = c->at<float>(c->plan.gemm_part);
+    // layer 0 input: embedding gather fused with the first RMSNorm
+    HIPCHK(launch_resid_norm(B, nullptr, 0, c->W(0), tokens, d, c->LW(0, 0), g.rms_eps, x, h, s));
     for (int l = 0; l < g.n_layers; ++l) {
-        HIPCHK(launch_rmsnorm(x, c->LW(l, 0), B, nullptr, B, d, g.rms_eps, h, s));
+        int S = 1;
         {
             const uint16_t* W[3] = {c->LW(l, 1), c->LW(l, 2), c->LW(l, 3)};
-            const uint16_t* Bs[3] = {c->LW(l, 4), c->LW(l, 5), c->LW(l, 6)};
             const int Ns[3] = {Nq, Nk, Nk};
-            MGCHK(fast_gemm(c, h, B, d, 0, W, g.qkv_bias ? Bs : nullptr, Ns, 3, qkv, FEPI_BF16, s));
+            MGCHK(fast_gemm(c, h, B, d, 0, W, nullptr, Ns, 3, nullptr, FEPI_PART, s, &S));
         }
-        HIPCHK(launch_rope_kv(it, m, l, qkv, c->at<float>(c->plan.rope), qrot, c->kv_pool, nullptr, s));
+        {
+            const uint16_t* Bs[3] = {c->LW(l, 4), c->LW(l, 5), c->LW(l, 6)};
+            HIPCHK(launch_rope_kv_part(B, part, S, g.qkv_bias ? Bs : nullptr, positions, page_table, m, l,
+                                       c->at<float>(c->plan.rope), qrot, c->kv_pool, s));
+        }
         {
             AttnArgs a{};
             a.it = it;
@@ -434,21 +436,23 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
         {
             const uint16_t* W[1] = {c->LW(l, 7)};
             const int Ns[1] = {d};
-            MGCHK(fast_gemm(c, att, B, Nq, 0, W, nullptr, Ns, 1, x, FEPI_RESID, s));
+            MGCHK(fast_gemm(c, att, B, Nq, 0, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
         }
-        HIPCHK(launch_rmsnorm(x, c->LW(l, 8), B, nullptr, B, d, g.rms_eps, h, s));
+        HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, c->LW(l, 8), g.rms_eps, x, h, s));
         {
             const uint16_t* W[2] = {c->LW(l, 9), c->LW(l, 10)};
             const int Ns[2] = {F, F};
-            MGCHK(fast_gemm(c, h, B, d, 0, W, nullptr, Ns, 2, gu, FEPI_BF16, s));
+            MGCHK(fast_gemm(c, h, B, d, 0, W, nullptr, Ns, 2, nullptr, FEPI_PART, s, &S));
         }
+        HIPCHK(launch_swiglu_part(B, part, S, F, act, s));
         {
             const uint16_t* W[1] = {c->LW(l, 11)};
             const int Ns[1] = {d};
-            MGCHK(fast_gemm(c, gu, B, F, 1, W, nullptr, Ns, 1, x, FEPI_RESID, s));
+            MGCHK(fast_gemm(c, act, B, F, 0, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
         }
+        const uint16_t* next_gamma = l + 1 < g.n_layers ? c->LW(l + 1, 0) : c->W(1 + WPL * g.n_layers);
+        HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, next_gamma, g.rms_eps, x, h, s));
     }
-    HIPCHK(launch_rmsnorm(x, c->W(1 + WPL * g.n_layers), B, nullptr, B, d, g.rms_eps, h, s));
     const uint16_t* W[1] = {c->W(2 + WPL * g.n_layers)};
     const int Ns[1] = {g.vocab};
     MGCHK(fast_gemm(c, h, B, d, 0, W, nullptr, Ns, 1, logits, FEPI_F32, s));
@@ -556,6 +560,11 @@ mg_status mg_profile_end(mg_ctx* c, int kind, int* n_launches, double* total_ms,
 
 // ---------------------------------------------------------------- op-level entry points (tests)
 
+mg_status mg_op_copy(int64_t n_bytes, const void* src, void* dst, void* stream) {
+    if (n_bytes < 0 || n_bytes % 16 || (n_bytes && (!src || !dst))) return MG_ERR_ARG;
+    return launch_copy16(n_bytes / 16, src, dst, static_cast<hipStream_t>(stream)) == hipSuccess ? MG_OK : MG_ERR_HIP;
+}
+
 mg_status mg_op_probe_bf16(int64_t n, const float* in, uint16_t* out, void* stream) {
     if (n < 0 || (n && (!in || !out))) return MG_ERR_ARG;
     return launch_probe_bf16(n, in, out, static_cast<hipStream_t>(stream)) == hipSuccess ? MG_OK : MG_ERR_HIP;
@@ -574,7 +583,7 @@ mg_status mg_op_probe_divsqrt(int64_t n, const float* a, const float* b, float* 
 size_t mg_op_linear_workspace_bytes(int n, int N, int K) {
     if (n <= 0 || N <= 0 || K <= 0) return 0;
     const int S = fast_gemm_splits(n, N, K, device_cu_count());
-    return up((size_t)S * n * N * sizeof(float)) + up((size_t)((N + 63) / 64) * sizeof(int32_t));
+    return up((size_t)S * n * N * sizeof(float));
 }
 
 mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const uint16_t* W, const uint16_t* bias,
@@ -596,6 +605,7 @@ mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const 
     }
     const size_t need = mg_op_linear_workspace_bytes(n, N, K);
     if (!workspace || workspace_bytes < need) return MG_ERR_WORKSPACE;
+    if (bias) return MG_ERR_ARG;
     FastGemmArgs a{};
     a.X = X;
     a.M = n;
@@ -606,10 +616,9 @@ mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const 
     a.Y = Y;
     a.S = fast_gemm_splits(n, N, K, device_cu_count());
     a.part = static_cast<float*>(workspace);
-    a.tickets = reinterpret_cast<int32_t*>(static_cast<unsigned char*>(workspace) + up((size_t)a.S * n * N * 4));
-    if (bias) return MG_ERR_ARG;
-    if (hipMemsetAsync(a.tickets, 0, (size_t)((N + 63) / 64) * sizeof(int32_t), s) != hipSuccess) return MG_ERR_HIP;
-    return launch_fast_gemm(a, FEPI_F32, s) == hipSuccess ? MG_OK : MG_ERR_HIP;
+    if (a.S == 1) return launch_fast_gemm(a, FEPI_F32, s) == hipSuccess ? MG_OK : MG_ERR_HIP;
+    if (launch_fast_gemm(a, FEPI_PART, s) != hipSuccess) return MG_ERR_HIP;
+    return launch_sum_partials(a.part, a.S, (int64_t)n * N, Y, s) == hipSuccess ? MG_OK : MG_ERR_HIP;
 }
 
 mg_status mg_op_rmsnorm(int n, int d, const uint16_t* x, const uint16_t* gamma, float eps, uint16_t* y, void* stream) {

@@ -64,6 +64,44 @@ __device__ __forceinline__ float butterfly_sum(float v) {
     return v;
 }
 
+// The same xor butterfly for NV = 2^k values at once.  At offset o a lane keeps the
+// level sum of one value of each pair and gets its partner's copy of that value, so
+// every sum is formed from exactly the operands the single-value butterfly adds at
+// that lane (own value + partner at l xor o); after k levels each lane holds one
+// value, and the remaining offsets run as the plain butterfly.  Value index
+// v = sum_j bit(lane, 5 - j) << j ends up in every lane whose bits 5..6-k spell v.
+template <int NV>
+__device__ __forceinline__ float butterfly_sum_multi(float (&v)[NV], int lane) {
+    static_assert(NV >= 1 && NV <= 64 && (NV & (NV - 1)) == 0, "power of two up to 64");
+    int o = 32;
+#pragma unroll
+    for (int cnt = NV; cnt > 1; cnt >>= 1) {
+        const bool hi = (lane & o) != 0;
+#pragma unroll
+        for (int i = 0; i < cnt / 2; ++i) {
+            const float a = v[2 * i], b = v[2 * i + 1];
+            const float recv = __shfl_xor(hi ? a : b, o, MG_WAVE);
+            v[i] = hi ? b + recv : a + recv;
+        }
+        o >>= 1;
+    }
+    float r = v[0];
+    for (; o >= 1; o >>= 1) r = r + __shfl_xor(r, o, MG_WAVE);
+    return r;
+}
+
+// index of the value butterfly_sum_multi<NV> leaves in `lane`, and whether this lane
+// is the lowest of the lanes holding it
+template <int NV>
+__device__ __forceinline__ int multi_index(int lane, bool* writer) {
+    int k = 0;
+    while ((1 << k) < NV) ++k;
+    int v = 0;
+    for (int j = 0; j < k; ++j) v |= ((lane >> (5 - j)) & 1) << j;
+    *writer = (lane & ((1 << (6 - k)) - 1)) == 0;
+    return v;
+}
+
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, MG_WAVE));

@@ -53,22 +53,35 @@ struct GemvArgs {
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
 
 // ---------------------------------------------------------------- fast MFMA GEMM
-enum { FEPI_BF16 = 0, FEPI_RESID = 1, FEPI_F32 = 2 };
+enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2 };
 struct FastGemmArgs {
     const uint16_t* X;         // [M][K] bf16; with swiglu_x: [M][2K] = [gate | up]
     int M, K;
     int swiglu_x;              // 1: X row = silu(gate) * up, computed on load
     const uint16_t* W[3];
-    const uint16_t* bias[3];
+    const uint16_t* bias[3];   // FEPI_BF16 only
     int Nseg[3];
     int N;
-    void* Y;
-    float* part;               // split-K partials [S][M][N] fp32 (workspace)
-    int32_t* tickets;          // [N/64] zero-initialised counters (workspace)
-    int S;                     // split-K factor
+    void* Y;                   // FEPI_BF16: bf16 [M][N]; FEPI_F32: fp32 [M][N]
+    float* part;               // FEPI_PART: fp32 partial tiles [S][M][N]
+    int S;                     // split-K factor (1 unless FEPI_PART)
 };
 hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s);
+hipError_t launch_sum_partials(const float* part, int S, int64_t n, float* out, hipStream_t s);
 int fast_gemm_splits(int M, int N, int K, int n_cu);
+
+// fast-path consumers of split partial tiles
+// x[r] = bf16(x[r] + bf16(sum_s part[s][r])) (skipped when part == NULL; with embed != NULL,
+// x[r] = embed[token of r] instead), then h[r] = bf16((x * rms^-1) * gamma)
+hipError_t launch_resid_norm(int B, const float* part, int S, const uint16_t* embed, const int32_t* tokens, int d,
+                             const uint16_t* gamma, float eps, uint16_t* x, uint16_t* h, hipStream_t s);
+// act[r] = bf16(silu(bf16(sum gate partials)) * bf16(sum up partials)); part rows [gate F | up F]
+hipError_t launch_swiglu_part(int B, const float* part, int S, int F, uint16_t* act, hipStream_t s);
+// qkv[r] = bf16(sum_s part[s][r] + bias), then RoPE of q and k, q' -> qrot, K' and V into
+// the paged cache at the row's position
+hipError_t launch_rope_kv_part(int B, const float* part, int S, const uint16_t* const* bias, const int32_t* positions,
+                               const int32_t* page_table, const ModelDims& m, int layer, const float* rope_cs,
+                               uint16_t* qrot, uint16_t* kv_pool, hipStream_t s);
 
 // ---------------------------------------------------------------- small kernels
 hipError_t launch_embed(const Items& it, const uint16_t* embed, int d, uint16_t* x, hipStream_t s);
@@ -96,6 +109,7 @@ struct AttnArgs {
     uint16_t* out;             // [n][Hq*hd]
 };
 hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s);
+int fast_attention_split();  // positions per split of the fast attention
 
 // ---------------------------------------------------------------- gate / repair / misc
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1,
@@ -108,6 +122,7 @@ hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_
 hipError_t launch_advance(int B, const int32_t* emitted, int32_t* tokens, int32_t* positions, hipStream_t s);
 
 // element-wise numerics probes used by the tests
+hipError_t launch_copy16(int64_t n16, const void* src, void* dst, hipStream_t s);
 hipError_t launch_probe_bf16(int64_t n, const float* in, uint16_t* out, hipStream_t s);
 hipError_t launch_probe_exp(int64_t n, const float* in, float* out, hipStream_t s);
 hipError_t launch_probe_divsqrt(int64_t n, const float* a, const float* b, float* q, float* r, hipStream_t s);

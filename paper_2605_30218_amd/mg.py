@@ -53,6 +53,7 @@ SIGNATURES = {
     "mg_advance": (I, [P, I, P, P, P, P]),
     "mg_profile_begin": (I, [P, I, I]),
     "mg_profile_end": (I, [P, I, P, P, P, P]),
+    "mg_op_copy": (I, [I64, P, P, P]),
     "mg_op_probe_bf16": (I, [I64, P, P, P]),
     "mg_op_probe_exp": (I, [I64, P, P, P]),
     "mg_op_probe_divsqrt": (I, [I64, P, P, P, P, P]),
@@ -185,6 +186,11 @@ class Engine:
 
 
 # ---------------------------------------------------------------- op-level calls (tests)
+
+def op_copy(src, dst):
+    _check("mg_op_copy", load().mg_op_copy(src.numel() * src.element_size(), src.data_ptr(), dst.data_ptr(),
+                                           _stream()))
+
 
 def op_probe_bf16(x):
     out = torch.empty(x.shape, dtype=torch.int16, device=x.device)

@@ -71,7 +71,8 @@ def test_canonical_gemv_row_result_independent_of_row_count_and_place():
 
 
 @pytest.mark.parametrize("n,N,K", [(1, 64, 4096), (5, 48, 688), (16, 128, 4096), (33, 64, 14336), (64, 6144, 4096),
-                                   (100, 80, 1032), (256, 64, 512)])
+                                   (100, 80, 1032), (256, 64, 512), (64, 28672, 4096), (64, 4096, 14336),
+                                   (64, 128256, 4096), (1, 4096, 4096), (128, 6144, 5120)])
 def test_fast_gemm_within_tolerance(n, N, K):
     X = synth.random_bf16((n, K), seed=n + 3)
     W = synth.random_bf16((N, K), seed=N + 5, std=0.02)
