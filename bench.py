@@ -134,10 +134,14 @@ def main():
         nb = args.copy_calibration << 20
         src = torch.ones(nb // 4, dtype=torch.int32, device="cuda")
         dst = torch.empty_like(src)
-        for _ in range(5):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        ev[0].record()
+        for i in range(5):
             mg.op_copy(src, dst)
+            ev[i + 1].record()
         torch.cuda.synchronize()
-        print(json.dumps(dict(copy_bytes=nb, launches=5)))
+        ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(5)]
+        print(json.dumps(dict(copy_bytes=nb, launches=5, ms=ms, gbps_read_plus_write=2 * nb / (min(ms) * 1e-3) / 1e9)))
         return
     shape = synth.LLAMA8B
     B, P = args.batch, args.prompt

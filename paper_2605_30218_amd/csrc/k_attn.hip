@@ -67,11 +67,22 @@ __global__ __launch_bounds__(256) void attn_chunk_kernel(AttnArgs a) {
         const int jb = j0 + sc * ATT_SUB;
         const int nn = min(ATT_SUB, j0 + nj - jb);
         __syncthreads();
-        for (int e = t; e < nn * u4; e += 256) {
-            const int pp = e / u4, uu = e % u4;
-            const uint4 v = reinterpret_cast<const uint4*>(src_row(jb + pp, 0))[uu];
-            uint32_t* dst = ks + pp * KW + uu * 4;
-            dst[0] = v.x; dst[1] = v.y; dst[2] = v.z; dst[3] = v.w;
+        {   // all staging loads of the sub-chunk in flight before the LDS stores
+            constexpr int NLD = ATT_SUB * ATT_MAXHD / 8 / 256;
+            uint4 v[NLD];
+#pragma unroll
+            for (int k = 0; k < NLD; ++k) {
+                const int e = t + 256 * k;
+                v[k] = e < nn * u4 ? reinterpret_cast<const uint4*>(src_row(jb + e / u4, 0))[e % u4] : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < NLD; ++k) {
+                const int e = t + 256 * k;
+                if (e < nn * u4) {
+                    uint32_t* dst = ks + (e / u4) * KW + (e % u4) * 4;
+                    dst[0] = v[k].x; dst[1] = v[k].y; dst[2] = v[k].z; dst[3] = v[k].w;
+                }
+            }
         }
         __syncthreads();
 #pragma unroll
@@ -125,9 +136,19 @@ __global__ __launch_bounds__(256) void attn_chunk_kernel(AttnArgs a) {
         const int jb = j0 + sc * ATT_SUB;
         const int nn = min(ATT_SUB, j0 + nj - jb);
         __syncthreads();
-        for (int e = t; e < nn * u4; e += 256) {
-            const int pp = e / u4, uu = e % u4;
-            reinterpret_cast<uint4*>(vsh + pp * hd)[uu] = reinterpret_cast<const uint4*>(src_row(jb + pp, 1))[uu];
+        {
+            constexpr int NLD = ATT_SUB * ATT_MAXHD / 8 / 256;
+            uint4 v[NLD];
+#pragma unroll
+            for (int k = 0; k < NLD; ++k) {
+                const int e = t + 256 * k;
+                v[k] = e < nn * u4 ? reinterpret_cast<const uint4*>(src_row(jb + e / u4, 1))[e % u4] : make_uint4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int k = 0; k < NLD; ++k) {
+                const int e = t + 256 * k;
+                if (e < nn * u4) reinterpret_cast<uint4*>(vsh + (e / u4) * hd)[e % u4] = v[k];
+            }
         }
         __syncthreads();
 #pragma unroll

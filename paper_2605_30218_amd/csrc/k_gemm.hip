@@ -6,7 +6,7 @@
 // B-operand registers: lane (j, q) loads W[n+j][k+8q .. k+8q+7] (16 bytes), so a
 // 32-wide k step of 16 features reads 16 rows x 64 contiguous bytes.  The block
 // walks its K range in chunks of KC; while the MFMAs of chunk c run, the weights
-// of chunk c+1 are already in flight (register double buffer) and the activations
+// of chunks c+1 and c+2 are already in flight (three register buffers) and the activations
 // of chunk c+1 are staged into the other half of a double-buffered LDS tile (rows
 // padded by 16 bytes so the A-operand lanes of a k group hit distinct banks).
 // One barrier per chunk.  The K range may be split over blocks (split-K): each
@@ -86,20 +86,30 @@ __device__ __forceinline__ void store_x(unsigned char* buf, const uint4 (&xr)[Ge
     }
 }
 
+#ifndef MG_GEMM_KPERM
+#define MG_GEMM_KPERM 0
+#endif
+// k offset, inside a chunk, of the 8 values lane group q supplies at MFMA k-step st.
+// MG_GEMM_KPERM = 1 permutes the chunk so a lane's NST groups are contiguous (each
+// weight row read as 4 lanes x 16*NST contiguous bytes per chunk instead of 64 bytes
+// per k-step); measured slower than the natural order on MI355X, so off by default.
+template <int NST>
+__device__ __forceinline__ int kofs(int st, int q) { return MG_GEMM_KPERM ? q * 8 * NST + st * 8 : st * 32 + q * 8; }
+
 template <int MT, int FT>
 __device__ __forceinline__ void load_w(const uint16_t* const (&wrow)[FT], const bool (&wok)[FT], int kc, int K, int q,
                                        uint4 (&wr)[GemmShape<MT>::NST][FT]) {
     using S = GemmShape<MT>;
 #pragma unroll
     for (int st = 0; st < S::NST; ++st) {
-        const int k = kc + st * 32 + q * 8;
+        const int k = kc + kofs<S::NST>(st, q);
 #pragma unroll
         for (int f = 0; f < FT; ++f)
             wr[st][f] = (wok[f] && k < K) ? *reinterpret_cast<const uint4*>(wrow[f] + k) : make_uint4(0, 0, 0, 0);
     }
 }
 
-template <int MT, int FT, int EPI, bool SWI>
+template <int MT, int FT, int EPI, bool SWI, int PF>
 __global__ __launch_bounds__(256) void fast_gemm_kernel(FastGemmArgs a) {
     using S = GemmShape<MT>;
     __shared__ __attribute__((aligned(16))) unsigned char xs[2][S::ROWS * S::STRIDE];
@@ -132,40 +142,80 @@ __global__ __launch_bounds__(256) void fast_gemm_kernel(FastGemmArgs a) {
 #pragma unroll
         for (int f = 0; f < FT; ++f) acc[mt][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    uint4 wcur[S::NST][FT], wnext[S::NST][FT];
-    uint4 xr[S::XLD];
-    if (c0 < c1) {
-        load_w<MT, FT>(wrow, wok, c0 * S::KC, K, q, wcur);
-        load_x<MT, SWI>(a, c0 * S::KC, xr);
-        store_x<MT>(xs[c0 & 1], xr);  // chunk c always lives in buffer c & 1
-    }
-    __syncthreads();
-    for (int c = c0; c < c1; ++c) {
-        const bool more = c + 1 < c1;
-        if (more) {
-            load_w<MT, FT>(wrow, wok, (c + 1) * S::KC, K, q, wnext);
-            load_x<MT, SWI>(a, (c + 1) * S::KC, xr);
+    if constexpr (PF == 1) {
+        // weights prefetched one chunk ahead (register double buffer)
+        uint4 wcur[S::NST][FT], wnext[S::NST][FT];
+        uint4 xr[S::XLD];
+        if (c0 < c1) {
+            load_w<MT, FT>(wrow, wok, c0 * S::KC, K, q, wcur);
+            load_x<MT, SWI>(a, c0 * S::KC, xr);
+            store_x<MT>(xs[c0 & 1], xr);
         }
-        const unsigned char* buf = xs[c & 1];
+        __syncthreads();
+        for (int c = c0; c < c1; ++c) {
+            const bool more = c + 1 < c1;
+            if (more) {
+                load_w<MT, FT>(wrow, wok, (c + 1) * S::KC, K, q, wnext);
+                load_x<MT, SWI>(a, (c + 1) * S::KC, xr);
+            }
+            const unsigned char* buf = xs[c & 1];
 #pragma unroll
-        for (int st = 0; st < S::NST; ++st) {
+            for (int st = 0; st < S::NST; ++st) {
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt) {
-                const uint4 av = *reinterpret_cast<const uint4*>(buf + (16 * mt + jl) * S::STRIDE + (st * 32 + q * 8) * 2);
-                const bf16x8_t A = __builtin_bit_cast(bf16x8_t, av);
+                for (int mt = 0; mt < MT; ++mt) {
+                    const uint4 av = *reinterpret_cast<const uint4*>(buf + (16 * mt + jl) * S::STRIDE + kofs<S::NST>(st, q) * 2);
+                    const bf16x8_t A = __builtin_bit_cast(bf16x8_t, av);
 #pragma unroll
-                for (int f = 0; f < FT; ++f)
-                    acc[mt][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8_t, wcur[st][f]),
-                                                                          acc[mt][f], 0, 0, 0);
+                    for (int f = 0; f < FT; ++f)
+                        acc[mt][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            A, __builtin_bit_cast(bf16x8_t, wcur[st][f]), acc[mt][f], 0, 0, 0);
+                }
+            }
+            if (more) store_x<MT>(xs[(c + 1) & 1], xr);
+            __syncthreads();
+            if (more) {
+#pragma unroll
+                for (int st = 0; st < S::NST; ++st)
+#pragma unroll
+                    for (int f = 0; f < FT; ++f) wcur[st][f] = wnext[st][f];
             }
         }
-        if (more) store_x<MT>(xs[(c + 1) & 1], xr);
+    } else {
+        // weights are prefetched two chunks ahead into three rotating register buffers;
+        // the chunk loop is unrolled by three so every buffer index is a constant
+        uint4 wb0[S::NST][FT], wb1[S::NST][FT], wb2[S::NST][FT];
+        uint4 xr[S::XLD];
+        if (c0 < c1) {
+            load_w<MT, FT>(wrow, wok, c0 * S::KC, K, q, wb0);
+            if (c0 + 1 < c1) load_w<MT, FT>(wrow, wok, (c0 + 1) * S::KC, K, q, wb1);
+            load_x<MT, SWI>(a, c0 * S::KC, xr);
+            store_x<MT>(xs[c0 & 1], xr);  // chunk c always lives in buffer c & 1
+        }
         __syncthreads();
-        if (more) {
-#pragma unroll
-            for (int st = 0; st < S::NST; ++st)
-#pragma unroll
-                for (int f = 0; f < FT; ++f) wcur[st][f] = wnext[st][f];
+        auto step = [&](int c, uint4 (&cur)[S::NST][FT], uint4 (&far)[S::NST][FT]) {
+            if (c + 2 < c1) load_w<MT, FT>(wrow, wok, (c + 2) * S::KC, K, q, far);
+            const bool more = c + 1 < c1;
+            if (more) load_x<MT, SWI>(a, (c + 1) * S::KC, xr);
+            const unsigned char* buf = xs[c & 1];
+    #pragma unroll
+            for (int st = 0; st < S::NST; ++st) {
+    #pragma unroll
+                for (int mt = 0; mt < MT; ++mt) {
+                    const uint4 av = *reinterpret_cast<const uint4*>(buf + (16 * mt + jl) * S::STRIDE + kofs<S::NST>(st, q) * 2);
+                    const bf16x8_t A = __builtin_bit_cast(bf16x8_t, av);
+    #pragma unroll
+                    for (int f = 0; f < FT; ++f)
+                        acc[mt][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8_t, cur[st][f]),
+                                                                              acc[mt][f], 0, 0, 0);
+                }
+            }
+            if (more) store_x<MT>(xs[(c + 1) & 1], xr);
+            __syncthreads();
+        };
+        for (int c = c0; c < c1; c += 3) {
+            step(c, wb0, wb2);
+            if (c + 1 < c1) step(c + 1, wb1, wb0);
+            if (c + 2 < c1) step(c + 2, wb2, wb1);
         }
     }
 
@@ -208,7 +258,10 @@ static int mt_for(int M) {
 static int g_n_cu = 256;
 int fast_gemm_ft(int M, int N) {
     (void)M;
-    return N / 128 >= 2 * g_n_cu ? 2 : 1;
+#ifndef MG_GEMM_FT2_MIN_N
+#define MG_GEMM_FT2_MIN_N 8192
+#endif
+    return N >= MG_GEMM_FT2_MIN_N ? 2 : 1;
 }
 
 int fast_gemm_splits(int M, int N, int K, int n_cu) {
@@ -231,12 +284,15 @@ int fast_gemm_splits(int M, int N, int K, int n_cu) {
     return S < 1 ? 1 : S;
 }
 
+#ifndef MG_GEMM_PF
+#define MG_GEMM_PF 1
+#endif
 template <int MT, int FT, int EPI>
 static void launch_epi(const FastGemmArgs& a, dim3 g, hipStream_t s) {
     if (a.swiglu_x)
-        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, true>), g, dim3(256), 0, s, a);
+        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, true, MG_GEMM_PF>), g, dim3(256), 0, s, a);
     else
-        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, false>), g, dim3(256), 0, s, a);
+        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, false, MG_GEMM_PF>), g, dim3(256), 0, s, a);
 }
 
 template <int MT, int FT>

@@ -12,9 +12,11 @@
 // rows.  K is walked in chunks of 512 elements (one group per lane).  While the
 // fma work of chunk c runs, the weights of chunk c+1 are in flight (register
 // double buffer: one 16-byte group per feature and lane, 1 KiB coalesced per
-// feature) and the rows' activations of chunk c+1 are staged into the other half
-// of a double-buffered fp32 LDS tile.  One barrier per chunk; no split-K, no
-// atomics: a row's arithmetic is the same whatever R, J, the tile or the count.
+// feature) and the rows' activations of chunk c+1 are loaded into registers, then
+// staged into the fp32 LDS tile between two barriers (one buffer keeps the LDS
+// footprint at R * 2 KiB, so more blocks fit per CU; measured faster than double
+// buffering).  No split-K, no atomics: a row's arithmetic is the same whatever R,
+// J, the tile or the count.
 // Block order: the row tiles of one feature block get consecutive slots on the
 // same XCD (blocks are dealt to the 8 XCDs round-robin), so they share its L2
 // copy of the weights.
@@ -24,6 +26,16 @@
 namespace mg {
 
 constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
+
+#ifndef MG_GEMV_LDS_BUFS
+#define MG_GEMV_LDS_BUFS 1
+#endif
+#ifndef MG_GEMV_J_WIDE
+#define MG_GEMV_J_WIDE 2
+#endif
+#ifndef MG_GEMV_J_NARROW
+#define MG_GEMV_J_NARROW 2
+#endif
 
 template <int R>
 struct GemvShape {
@@ -78,8 +90,10 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, i
     const int jw = (fb * 4 + wave) * J;
     const int K = a.K, G = K >> 3;
 
-    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[buf][rr][half][lane].c
-    __shared__ float4 xs[2][R][2][64];
+    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[buf][rr][half][lane].c;
+    // one buffer (two barriers per chunk) or two (one barrier per chunk)
+    constexpr int NB = MG_GEMV_LDS_BUFS;
+    __shared__ float4 xs[NB][R][2][64];
 
     const uint16_t* wrow[J];
     bool valid[J];
@@ -119,27 +133,35 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, i
                 w[jj][0] = bf_lo(v.x); w[jj][1] = bf_hi(v.x); w[jj][2] = bf_lo(v.y); w[jj][3] = bf_hi(v.y);
                 w[jj][4] = bf_lo(v.z); w[jj][5] = bf_hi(v.z); w[jj][6] = bf_lo(v.w); w[jj][7] = bf_hi(v.w);
             }
-            float4(*xb)[2][64] = xs[c & 1];
+            float4(*xb)[2][64] = xs[NB == 1 ? 0 : (c & 1)];
+            // rows past nr are skipped by a uniform branch; the loop stays fully unrolled
+            // so every accumulator index is a compile-time constant (no scratch)
 #pragma unroll
             for (int rr = 0; rr < R; ++rr) {
-                if (rr >= nr) break;
-                const float4 x0 = xb[rr][0][lane], x1 = xb[rr][1][lane];
+                if (rr < nr) {
+                    const float4 x0 = xb[rr][0][lane], x1 = xb[rr][1][lane];
 #pragma unroll
-                for (int jj = 0; jj < J; ++jj) {
-                    float s = acc[jj][rr];
-                    s = __builtin_fmaf(x0.x, w[jj][0], s);
-                    s = __builtin_fmaf(x0.y, w[jj][1], s);
-                    s = __builtin_fmaf(x0.z, w[jj][2], s);
-                    s = __builtin_fmaf(x0.w, w[jj][3], s);
-                    s = __builtin_fmaf(x1.x, w[jj][4], s);
-                    s = __builtin_fmaf(x1.y, w[jj][5], s);
-                    s = __builtin_fmaf(x1.z, w[jj][6], s);
-                    s = __builtin_fmaf(x1.w, w[jj][7], s);
-                    acc[jj][rr] = s;
+                    for (int jj = 0; jj < J; ++jj) {
+                        float s = acc[jj][rr];
+                        s = __builtin_fmaf(x0.x, w[jj][0], s);
+                        s = __builtin_fmaf(x0.y, w[jj][1], s);
+                        s = __builtin_fmaf(x0.z, w[jj][2], s);
+                        s = __builtin_fmaf(x0.w, w[jj][3], s);
+                        s = __builtin_fmaf(x1.x, w[jj][4], s);
+                        s = __builtin_fmaf(x1.y, w[jj][5], s);
+                        s = __builtin_fmaf(x1.z, w[jj][6], s);
+                        s = __builtin_fmaf(x1.w, w[jj][7], s);
+                        acc[jj][rr] = s;
+                    }
                 }
             }
         }
-        if (more) gemv_store_x<R>(xs[(c + 1) & 1], xr);
+        if (NB == 1) {
+            __syncthreads();
+            if (more) gemv_store_x<R>(xs[0], xr);
+        } else if (more) {
+            gemv_store_x<R>(xs[(c + 1) & 1], xr);
+        }
         __syncthreads();
         if (more) {
 #pragma unroll
@@ -194,8 +216,9 @@ hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
     const bool wide = a.N >= 8192;
-    if (rows > 8) return wide ? launch_jr<4, 16>(a, epi, rows, s) : launch_jr<2, 16>(a, epi, rows, s);
-    return wide ? launch_jr<4, 8>(a, epi, rows, s) : launch_jr<2, 8>(a, epi, rows, s);
+    constexpr int JW = MG_GEMV_J_WIDE, JN = MG_GEMV_J_NARROW;
+    if (rows > 8) return wide ? launch_jr<JW, 16>(a, epi, rows, s) : launch_jr<JN, 16>(a, epi, rows, s);
+    return wide ? launch_jr<JW, 8>(a, epi, rows, s) : launch_jr<JN, 8>(a, epi, rows, s);
 }
 
 }  // namespace mg

@@ -27,6 +27,8 @@ hipError_t launch_embed(const Items& it, const uint16_t* embed, int d, uint16_t*
 // One wave per row.  ss = CDOT(x, x) (lane l owns groups l, l+64, ...; fma in
 // element order; xor butterfly), m = ss / d, r = 1 / sqrt(m + eps),
 // y_i = bf16((x_i * r) * gamma_i).  Used by both paths (it is batch-invariant).
+constexpr int RMS_MAXG = 16;  // groups of 8 per lane: d <= 8192
+
 __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict__ x, const uint16_t* __restrict__ g,
                                                       RowCount rc, int d, float eps, uint16_t* __restrict__ y) {
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -34,27 +36,41 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
     if (row >= rc.get()) return;
     const uint4* xr = reinterpret_cast<const uint4*>(x + (size_t)row * d);
     const int G = d >> 3;
-    float a = 0.0f;
-    for (int gi = lane; gi < G; gi += 64) {
-        const uint4 v = xr[gi];
-        const float e[8] = {bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y),
-                            bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w)};
+    // the lane's groups lane, lane+64, ... are loaded together and kept in registers
+    uint4 xv[RMS_MAXG];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) a = __builtin_fmaf(e[k], e[k], a);
+    for (int k = 0; k < RMS_MAXG; ++k) {
+        const int gi = lane + 64 * k;
+        xv[k] = gi < G ? xr[gi] : make_uint4(0, 0, 0, 0);
+    }
+    float a = 0.0f;
+#pragma unroll
+    for (int k = 0; k < RMS_MAXG; ++k) {
+        if (lane + 64 * k < G) {
+            const uint4 v = xv[k];
+            const float e[8] = {bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y),
+                                bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w)};
+#pragma unroll
+            for (int i = 0; i < 8; ++i) a = __builtin_fmaf(e[i], e[i], a);
+        }
     }
     const float ss = butterfly_sum(a);
     const float m = ieee_div(ss, (float)d);
     const float r = ieee_div(1.0f, ieee_sqrt(m + eps));
     const uint4* gr = reinterpret_cast<const uint4*>(g);
     uint4* yr = reinterpret_cast<uint4*>(y + (size_t)row * d);
-    for (int gi = lane; gi < G; gi += 64) {
-        const uint4 v = xr[gi], gv = gr[gi];
-        uint4 o;
-        o.x = pack_bf2((bf_lo(v.x) * r) * bf_lo(gv.x), (bf_hi(v.x) * r) * bf_hi(gv.x));
-        o.y = pack_bf2((bf_lo(v.y) * r) * bf_lo(gv.y), (bf_hi(v.y) * r) * bf_hi(gv.y));
-        o.z = pack_bf2((bf_lo(v.z) * r) * bf_lo(gv.z), (bf_hi(v.z) * r) * bf_hi(gv.z));
-        o.w = pack_bf2((bf_lo(v.w) * r) * bf_lo(gv.w), (bf_hi(v.w) * r) * bf_hi(gv.w));
-        yr[gi] = o;
+#pragma unroll
+    for (int k = 0; k < RMS_MAXG; ++k) {
+        const int gi = lane + 64 * k;
+        if (gi < G) {
+            const uint4 v = xv[k], gv = gr[gi];
+            uint4 o;
+            o.x = pack_bf2((bf_lo(v.x) * r) * bf_lo(gv.x), (bf_hi(v.x) * r) * bf_hi(gv.x));
+            o.y = pack_bf2((bf_lo(v.y) * r) * bf_lo(gv.y), (bf_hi(v.y) * r) * bf_hi(gv.y));
+            o.z = pack_bf2((bf_lo(v.z) * r) * bf_lo(gv.z), (bf_hi(v.z) * r) * bf_hi(gv.z));
+            o.w = pack_bf2((bf_lo(v.w) * r) * bf_lo(gv.w), (bf_hi(v.w) * r) * bf_hi(gv.w));
+            yr[gi] = o;
+        }
     }
 }
 
@@ -62,6 +78,7 @@ hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, int n_host, 
                           float eps, uint16_t* y, hipStream_t s) {
     const int rows = n_dev ? cap : n_host;
     if (rows <= 0) return hipSuccess;
+    if (d % 8 || d / 8 > 64 * RMS_MAXG) return hipErrorInvalidValue;
     RowCount rc{n_dev, n_host, cap};
     hipLaunchKernelGGL(rmsnorm_kernel, dim3((rows + 3) / 4), dim3(256), 0, s, x, gamma, rc, d, eps, y);
     return hipGetLastError();
@@ -164,6 +181,7 @@ struct Top2 {
     int i1;
     int nan;
 };
+constexpr int TOP2_MAX_SLICES = 128;
 
 __device__ __forceinline__ Top2 top2_merge(const Top2& a, const Top2& b) {
     if (a.i1 < 0) return Top2{b.v1, b.v2, b.i1, b.nan | a.nan};
@@ -195,81 +213,105 @@ __device__ __forceinline__ Top2 top2_shfl(const Top2& s, int o) {
     return t;
 }
 
-// One block per row: 256 threads scan the row with 16-byte loads, merge by wave
-// shuffles then across waves.  With `gate` set, the last block to finish also
-// writes the ordered list of gated rows and their count.
-__global__ __launch_bounds__(256) void top2_kernel(int B, int V, const float* __restrict__ logits,
-                                                   const uint8_t* __restrict__ prot, float tau, int32_t* top1,
-                                                   float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated,
-                                                   int32_t* ticket, const int32_t* n_dev) {
-    const int b = blockIdx.x;
+// Stage 1: block (s, b) scans slice s of row b (16-byte loads), merges its lanes by
+// wave shuffles and its waves through LDS, and stores the slice's state.
+__global__ __launch_bounds__(256) void top2_slice_kernel(int B, int V, int slice, const float* __restrict__ logits,
+                                                         Top2* __restrict__ part, int nsl, const int32_t* n_dev) {
+    const int s = blockIdx.x, b = blockIdx.y;
     const int nrows = n_dev ? min(max(*n_dev, 0), B) : B;
-    __shared__ Top2 ws[4];
-    __shared__ int last;
-    __shared__ uint8_t flags[1024];
-    if (b < nrows) {
-        const float* row = logits + (size_t)b * V;
-        Top2 s{-__builtin_inff(), -__builtin_inff(), -1, 0};
-        const int t = threadIdx.x;
-        if ((V & 3) == 0) {
-            const float4* r4 = reinterpret_cast<const float4*>(row);
-            for (int q = t; q < V / 4; q += 256) {
-                const float4 v = r4[q];
-                top2_push(s, v.x, 4 * q);
-                top2_push(s, v.y, 4 * q + 1);
-                top2_push(s, v.z, 4 * q + 2);
-                top2_push(s, v.w, 4 * q + 3);
-            }
-        } else {
-            for (int q = t; q < V; q += 256) top2_push(s, row[q], q);
+    if (b >= nrows) return;
+    const float* row = logits + (size_t)b * V;
+    const int j0 = s * slice, j1 = min(j0 + slice, V);
+    Top2 st{-__builtin_inff(), -__builtin_inff(), -1, 0};
+    const int t = threadIdx.x;
+    if ((V & 3) == 0) {  // slice is a multiple of 4, so are j0 and j1
+        const float4* r4 = reinterpret_cast<const float4*>(row);
+        for (int q = j0 / 4 + t; q < j1 / 4; q += 256) {
+            const float4 v = r4[q];
+            top2_push(st, v.x, 4 * q);
+            top2_push(st, v.y, 4 * q + 1);
+            top2_push(st, v.z, 4 * q + 2);
+            top2_push(st, v.w, 4 * q + 3);
         }
+    } else {
+        for (int q = j0 + t; q < j1; q += 256) top2_push(st, row[q], q);
+    }
 #pragma unroll
-        for (int o = 32; o >= 1; o >>= 1) s = top2_merge(s, top2_shfl(s, o));
-        if ((t & 63) == 0) ws[t >> 6] = s;
-        __syncthreads();
-        if (t == 0) {
-            Top2 f = top2_merge(top2_merge(ws[0], ws[1]), top2_merge(ws[2], ws[3]));
-            const int i1 = f.i1 < 0 ? 0 : f.i1;
-            const float g = f.nan ? __builtin_nanf("") : f.v1 - f.v2;
+    for (int o = 32; o >= 1; o >>= 1) st = top2_merge(st, top2_shfl(st, o));
+    __shared__ Top2 ws[4];
+    if ((t & 63) == 0) ws[t >> 6] = st;
+    __syncthreads();
+    if (t == 0) part[(size_t)b * nsl + s] = top2_merge(top2_merge(ws[0], ws[1]), top2_merge(ws[2], ws[3]));
+}
+
+// Stage 2: one block of 1024 threads.  Row b's nsl slice states sit in nsl/2
+// consecutive threads (2 states each, nsl a power of two, B * nsl <= 2048), merged
+// by xor shuffles inside that lane group; then top1 / margin / gate, and the gated
+// rows compacted in increasing order with per-wave ballots.
+__global__ __launch_bounds__(1024) void top2_final_kernel(int B, const Top2* __restrict__ part, int nsl,
+                                                          const uint8_t* __restrict__ prot, float tau, int32_t* top1,
+                                                          float* margin, uint8_t* gate, int32_t* gated_rows,
+                                                          int32_t* n_gated, const int32_t* n_dev) {
+    const int nrows = n_dev ? min(max(*n_dev, 0), B) : B;
+    const int t = threadIdx.x;
+    const int tpr = nsl / 2;            // threads per row (power of two, <= 64)
+    const int b = t / tpr;
+    const bool live = b < nrows;
+    Top2 st{-__builtin_inff(), -__builtin_inff(), -1, 0};
+    if (live) st = top2_merge(part[(size_t)b * nsl + 2 * (t % tpr)], part[(size_t)b * nsl + 2 * (t % tpr) + 1]);
+    for (int o = 1; o < tpr; o <<= 1) st = top2_merge(st, top2_shfl(st, o));
+    __shared__ uint8_t fire_s[256];
+    __shared__ int wave_cnt[4];
+    if (t % tpr == 0 && b < B) {
+        int fire = 0;
+        if (live) {
+            const int i1 = st.i1 < 0 ? 0 : st.i1;
+            const float g = st.nan ? __builtin_nanf("") : st.v1 - st.v2;
             top1[b] = i1;
             if (margin) margin[b] = g;
             if (gate) {
                 const int p = prot ? (prot[b] != 0) : 1;
-                const int fire = p && !(g >= tau);
+                fire = p && !(g >= tau);
                 gate[b] = (uint8_t)fire;
-                if (gated_rows) ticket[1 + b] = fire;
             }
         }
+        fire_s[b] = (uint8_t)fire;
     }
-    if (!gate || !gated_rows) return;
-    // ordered compaction by the last block to finish; ticket[0] counts finished
-    // blocks, ticket[1 + b] holds row b's decision
+    if (!gated_rows) return;
+    __syncthreads();  // fire_s complete
+    // rows 0..255 -> waves 0..3 of 64 rows: ballot, then prefix over the waves
+    const int w = t >> 6, l = t & 63;
+    const int f = (t < nrows) ? fire_s[t] : 0;  // t < 256 whenever t < nrows
+    const unsigned long long bal = __ballot(f);
+    if (w < 4 && l == 0) wave_cnt[w] = __popcll(bal);
     __syncthreads();
-    if (threadIdx.x == 0) {
-        __threadfence();
-        last = (atomicAdd(ticket, 1) == (int)gridDim.x - 1);
-    }
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
-    for (int q = threadIdx.x; q < nrows; q += blockDim.x)
-        flags[q] = (uint8_t)__hip_atomic_load(ticket + 1 + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        int n = 0;
-        for (int q = 0; q < nrows; ++q)
-            if (flags[q]) gated_rows[n++] = q;
-        *n_gated = n;
-        __hip_atomic_store(ticket, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (w < 4) {
+        int base = 0;
+        for (int k = 0; k < w; ++k) base += wave_cnt[k];
+        if (f) gated_rows[base + __popcll(bal & ((1ull << l) - 1ull))] = t;
+        if (t == 0) *n_gated = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
     }
 }
 
+int top2_slices(int B, int V) {
+    int nsl = 2;
+    while (nsl * 2 <= TOP2_MAX_SLICES && (nsl * 2) * (B > 0 ? B : 1) <= 2048 && (V + nsl * 2 - 1) / (nsl * 2) >= 1024)
+        nsl *= 2;
+    return nsl;
+}
+
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1, float* margin,
-                       uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* ticket, const int32_t* n_dev,
+                       uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, void* part_ws, const int32_t* n_dev,
                        hipStream_t s) {
     if (B <= 0) return hipSuccess;
-    hipLaunchKernelGGL(top2_kernel, dim3(B), dim3(256), 0, s, B, V, logits, prot, tau, top1, margin, gate, gated_rows,
-                       n_gated, ticket, n_dev);
+    if (B > 256) return hipErrorInvalidValue;
+    const int nsl = top2_slices(B, V);
+    int slice = (V + nsl - 1) / nsl;
+    slice = (slice + 3) & ~3;
+    Top2* part = static_cast<Top2*>(part_ws);
+    hipLaunchKernelGGL(top2_slice_kernel, dim3(nsl, B), dim3(256), 0, s, B, V, slice, logits, part, nsl, n_dev);
+    hipLaunchKernelGGL(top2_final_kernel, dim3(1), dim3(1024), 0, s, B, part, nsl, prot, tau, top1, margin, gate,
+                       gated_rows, n_gated, n_dev);
     return hipGetLastError();
 }
 
@@ -361,13 +403,22 @@ __global__ void probe_divsqrt_kernel(int64_t n, const float* a, const float* b, 
 
 // plain 16-byte copy: reads and writes n16 * 16 bytes once (counter calibration)
 __global__ __launch_bounds__(256) void copy16_kernel(int64_t n16, const uint4* __restrict__ src, uint4* __restrict__ dst) {
-    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n16; i += (int64_t)gridDim.x * blockDim.x)
-        dst[i] = src[i];
+    // four independent 16-byte loads in flight per thread before the stores
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    for (; i + 3 * stride < n16; i += 4 * stride) {
+        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride], d = src[i + 3 * stride];
+        dst[i] = a;
+        dst[i + stride] = b;
+        dst[i + 2 * stride] = c;
+        dst[i + 3 * stride] = d;
+    }
+    for (; i < n16; i += stride) dst[i] = src[i];
 }
 
 hipError_t launch_copy16(int64_t n16, const void* src, void* dst, hipStream_t s) {
     if (n16 <= 0) return hipSuccess;
-    hipLaunchKernelGGL(copy16_kernel, dim3(8192), dim3(256), 0, s, n16, static_cast<const uint4*>(src),
+    hipLaunchKernelGGL(copy16_kernel, dim3(2048), dim3(256), 0, s, n16, static_cast<const uint4*>(src),
                        static_cast<uint4*>(dst));
     return hipGetLastError();
 }

@@ -24,7 +24,7 @@ constexpr size_t ALIGN = 256;
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 struct Plan {
-    size_t rope, x, h, qkv, qrot, att, gu, act, attn_part, gemm_part, tickets, gate_ticket, vlog, total;
+    size_t rope, x, h, qkv, qrot, att, gu, act, attn_part, gemm_part, top2_ws, vlog, total;
     int rows_cap, max_pos, chunks_canon, chunks_fast, attn_rows_fast, gemm_part_floats;
 };
 
@@ -89,10 +89,7 @@ Plan make_plan(const mg_model_cfg* c, int n_cu) {
             if (need > gp) gp = need;
         }
     p.gemm_part = o; o += up((gp ? gp : 1) * sizeof(float));
-    int maxN = 0;
-    for (int k = 0; k < 5; ++k) maxN = ps[k].N > maxN ? ps[k].N : maxN;
-    p.tickets = o; o += up((size_t)((maxN + 63) / 64) * sizeof(int32_t));
-    p.gate_ticket = o; o += up((size_t)(1 + c->max_batch) * sizeof(int32_t));
+    p.top2_ws = o; o += up(TOP2_WS_BYTES);
     p.vlog = o; o += up((size_t)c->max_batch * c->vocab * sizeof(float));
     p.total = o;
     return p;
@@ -366,8 +363,6 @@ mg_status mg_create(const mg_model_cfg* cfg, const void* const* weights, void* k
         }
     }
     if (hipMemcpy(c->at<float>(plan.rope), cs.data(), cs.size() * sizeof(float), hipMemcpyHostToDevice) != hipSuccess ||
-        hipMemset(c->ws + plan.tickets, 0, plan.gate_ticket + (size_t)(1 + cfg->max_batch) * 4 - plan.tickets) !=
-            hipSuccess ||
         hipDeviceSynchronize() != hipSuccess) {
         delete c;
         return MG_ERR_HIP;
@@ -468,7 +463,7 @@ mg_status mg_margin_gate(mg_ctx* c, int B, const float* logits, const uint8_t* p
     hipStream_t s = static_cast<hipStream_t>(stream);
     ProfScope ps(c, MG_KIND_GATE, s, (double)B * c->cfg.vocab * 4.0);
     HIPCHK(launch_top2(B, c->cfg.vocab, logits, protected_mask, tau, top1, margin, gate, gated_rows, n_gated,
-                       c->at<int32_t>(c->plan.gate_ticket), nullptr, s));
+                       c->ws + c->plan.top2_ws, nullptr, s));
     return MG_OK;
 }
 
@@ -484,8 +479,8 @@ mg_status mg_verify_rows(mg_ctx* c, int n, const int32_t* rows, const int32_t* n
     Items it{rows, n == -1 ? n_dev : nullptr, cap, tokens, positions, page_table, 0};
     float* lg = v_logits ? v_logits : c->at<float>(c->plan.vlog);
     MGCHK(canon_forward(c, it, v_kvcol, lg, s));
-    HIPCHK(launch_top2(cap, c->cfg.vocab, lg, nullptr, 0.0f, v_tok, nullptr, nullptr, nullptr, nullptr, nullptr,
-                       it.n_dev, s));
+    HIPCHK(launch_top2(cap, c->cfg.vocab, lg, nullptr, 0.0f, v_tok, nullptr, nullptr, nullptr, nullptr,
+                       c->ws + c->plan.top2_ws, it.n_dev, s));
     return MG_OK;
 }
 

@@ -112,8 +112,11 @@ hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s);
 int fast_attention_split();  // positions per split of the fast attention
 
 // ---------------------------------------------------------------- gate / repair / misc
+// top-1 / top-2 of B <= 256 logit rows in two launches (vocabulary slices, then a
+// per-row merge and the ordered compaction); part_ws holds TOP2_WS_BYTES
+constexpr size_t TOP2_WS_BYTES = 256 * 128 * 16;
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1,
-                       float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* ticket,
+                       float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, void* part_ws,
                        const int32_t* n_dev, hipStream_t s);
 hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_t* rows, const int32_t* positions,
                          const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
