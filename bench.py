@@ -28,20 +28,29 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2605_30218_amd import mg, synth  # noqa: E402
+from paper_2605_30218_amd import mg, profsum, synth  # noqa: E402
 from paper_2605_30218_amd.runtime import GatedDecoder, prefill_fast, prefill_rows  # noqa: E402
 
 METRIC = "decode tok/s + gated-vs-always-on verifier overhead, Llama-3.1-8B-shape bs=64"
 HBM_PEAK = 8.0e12            # B/s, MI355X
 FP32_VALU_PEAK = 78.6e12     # flop/s: 256 CU x 4 SIMD x 16 lanes x 2 (fma) x 2.4 GHz, no packed fp32
-PAPER_TRIGGER = 0.1856       # Llama-3.1-8B trigger rate at tau_100 (paper Sec. 5.3)
+PAPER_TRIGGER = 0.1856       # Llama-3.1-8B trigger rate at tau_100 (paper Sec. 4.3)
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "{kernel}_traffic_llama8b_bs64.txt")
+
+
+def attn_bytes(shape, rows, ctx):
+    """Algorithmic HBM bytes of one layer's decode attention: K and V of `ctx` positions
+    per row and KV head, the rotated query in and the attention output out."""
+    kv = ctx * shape.n_kv_heads * shape.head_dim * 2 * 2
+    qo = 2 * shape.n_q_heads * shape.head_dim * 2
+    return rows * (kv + qo)
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def run_mode(dec, mode, warmup, steps, state, kv_snap, eng, profile_kinds=()):
+def run_mode(dec, mode, warmup, steps, state, kv_snap, eng, profile_kinds=(), profile_steps=32):
     eng.kv_pool.copy_(kv_snap)
     dec.set_state(*state)
     dec.n_repaired.zero_()
@@ -51,9 +60,13 @@ def run_mode(dec, mode, warmup, steps, state, kv_snap, eng, profile_kinds=()):
     dec.protected_row_steps = dec.verified_row_steps = 0
     dec.hist = []
     dec.n_repaired.zero_()
-    prof_steps = min(steps, 64)   # event pairs are recorded around the launches of the first 64 timed steps
+    prof_steps = min(steps, profile_steps)
+    ctx0 = int(dec.positions.max().item()) + 1     # positions attended at the first timed step
+    L = eng.shape.n_layers
+    per_step = {mg.KIND_FAST_GEMM: 4 * L + 1, mg.KIND_CANON_GEMV: 4 * L + 1, mg.KIND_FAST_ATTN: L,
+                mg.KIND_CANON_ATTN: L}
     for k in profile_kinds:
-        eng.profile_begin(k, prof_steps * (4 * eng.shape.n_layers + 1))
+        eng.profile_begin(k, prof_steps * per_step[k])
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -66,6 +79,16 @@ def run_mode(dec, mode, warmup, steps, state, kv_snap, eng, profile_kinds=()):
     per = np.array([ev[s].elapsed_time(ev[s + 1]) for s in range(steps)])
     prof = {k: eng.profile_end(k) for k in profile_kinds}
     B = dec.B
+    # attention bytes are not known to the library (positions live on the device); every row
+    # of this workload has the same position, so they follow from the step index.  A kind
+    # records the launches of its first prof_steps steps that ran it (the verifier runs only
+    # on steps with gated rows).
+    for k, rows in ((mg.KIND_FAST_ATTN, [B] * steps), (mg.KIND_CANON_ATTN, dec.hist)):
+        if k in prof:
+            n, ms, b, f = prof[k]
+            ran = [(s, r) for s, r in enumerate(rows) if r][:n // L]
+            b = sum(L * attn_bytes(eng.shape, r, ctx0 + s) for s, r in ran)
+            prof[k] = (n, ms, float(b), f)
     return dict(ms_per_step=wall * 1e3 / steps, tok_s=B * steps / wall, p50_ms=float(np.median(per)),
                 p99_ms=float(np.percentile(per, 99)), r_verify=dec.r_verify, r_repair=dec.r_repair(),
                 verified_rows_per_step=float(np.mean(dec.hist)), prof=prof)
@@ -119,6 +142,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=4)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--profile-steps", type=int, default=32,
+                    help="timed gated steps (from the first) whose kernel launches are bracketed by HIP events")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run the plain copy kernel on MIB MiB five times (HBM counter scaling) and exit")
     ap.add_argument("--prefill", choices=("canonical", "fast"), default="canonical",
@@ -168,9 +193,9 @@ def main():
     for mode in args.modes.split(","):
         steps = always_steps if mode == "always" else args.steps
         kinds = (mg.KIND_FAST_GEMM, mg.KIND_CANON_GEMV, mg.KIND_FAST_ATTN, mg.KIND_CANON_ATTN) \
-            if mode == "gated" else ()
+            if mode == "gated" and args.profile_steps > 0 else ()
         log(f"[bench] mode {mode}: {args.warmup} warmup + {steps} timed steps")
-        modes[mode] = run_mode(dec, mode, args.warmup, steps, state, kv_snap, eng, kinds)
+        modes[mode] = run_mode(dec, mode, args.warmup, steps, state, kv_snap, eng, kinds, args.profile_steps)
         log(f"[bench] mode {mode}: {modes[mode]['ms_per_step']:.3f} ms/step, {modes[mode]['tok_s']:.0f} tok/s, "
             f"r_verify {modes[mode]['r_verify']:.4f}")
     g = modes.get("gated") or next(iter(modes.values()))
@@ -192,12 +217,21 @@ def main():
         sec = kd["total_ms"] * 1e-3
         hbm = kd["algo_bytes"] / sec
         alu = kd["algo_flops"] / sec
+        # HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary, if it was
+        # taken on the kernel's current source
+        traffic = None
+        if dom in profsum.SOURCES:
+            t = profsum.read_traffic(TRAFFIC_SUMMARY.format(kernel=dom))
+            if t and t[1] == profsum.source_sha(dom):
+                traffic = t[0]
+        common = dict(kernel=dom, traffic=traffic, traffic_unit="bytes/launch", launches=kd["launches"],
+                      algo_bytes_per_launch=kd["algo_bytes"] / max(kd["launches"], 1), avg_us=kd["avg_us"])
         if dom == "canon_gemv" and alu / FP32_VALU_PEAK > hbm / HBM_PEAK:
-            roofline = dict(kernel=dom, bound="alu", achieved=alu / 1e12, peak=FP32_VALU_PEAK / 1e12, unit="TFLOP/s",
-                            frac=alu / FP32_VALU_PEAK, traffic=None, launches=kd["launches"])
+            roofline = dict(bound="alu", achieved=alu / 1e12, peak=FP32_VALU_PEAK / 1e12, unit="TFLOP/s",
+                            frac=alu / FP32_VALU_PEAK, **common)
         else:
-            roofline = dict(kernel=dom, bound="hbm", achieved=hbm / 1e9, peak=HBM_PEAK / 1e9, unit="GB/s",
-                            frac=hbm / HBM_PEAK, traffic=None, launches=kd["launches"])
+            roofline = dict(bound="hbm", achieved=hbm / 1e9, peak=HBM_PEAK / 1e9, unit="GB/s",
+                            frac=hbm / HBM_PEAK, **common)
     out = dict(metric=METRIC, value=g["tok_s"], unit="tok/s", n_gpus=1, steps=args.steps, warmup=args.warmup,
                ms_per_step=g["ms_per_step"], higher_is_better=True, scaling="weak", vs_baseline=None, dtype="bf16",
                data="synthetic",

@@ -89,9 +89,9 @@ mg_status mg_create(const mg_model_cfg* cfg, const void* const* weights, void* k
                     void* workspace, size_t workspace_bytes, mg_ctx** out);
 mg_status mg_destroy(mg_ctx* ctx);
 
-/* (1) The BF16 fast path: one batched decoder forward (paper Sec. 4.1, "the
- * default BF16 batched forward"; Sec. 4.2, it "tentatively appends the current
- * token and K/V column").  For each row b < B: consumes tokens[b] at position
+/* (1) The BF16 fast path: the ordinary batched decoder forward whose logits the
+ * gate inspects (paper Sec. 3.1, margin trigger), which also writes the current
+ * token's K/V column into the cache as a tentative entry (Sec. 3.2).  For each row b < B: consumes tokens[b] at position
  * positions[b], writes that position's K (after RoPE) and V into the paged
  * cache in every layer, attends over positions 0..positions[b], and writes
  * fp32 logits[b][V].  Its reduction plan depends on B (it may differ in the last
@@ -101,23 +101,23 @@ mg_status mg_destroy(mg_ctx* ctx);
 mg_status mg_decode_step(mg_ctx* ctx, int B, const int32_t* tokens, const int32_t* positions,
                          const int32_t* page_table, float* logits, void* stream);
 
-/* (2) The margin gate (Sec. 4.1): per row, top1[b] = argmax (lowest index on
+/* (2) The margin gate (Sec. 3.1): per row, top1[b] = argmax (lowest index on
  * ties), margin[b] = l_(1) - l_(2) where l_(2) is the second largest value of
  * the row (0 when the maximum is duplicated; NaN when the row holds a NaN),
  * gate[b] = protected[b] && !(margin[b] >= tau), i.e. the strict trigger
  * g < tau with NaN firing.  gated_rows receives the gated row indices in
  * increasing order and *n_gated their count (device scalar), so the verifier can
- * be launched on exactly those rows (the repair request of Sec. 4.2).
+ * be launched on exactly those rows (the repair request of Sec. 3.2).
  * logits [device fp32 B*V]; protected_mask [device uint8 B] or NULL (= all rows
- * protected, Sec. 4.3's per-request policy); top1, gated_rows [device int32 B];
+ * protected, Sec. 3.3's per-request policy); top1, gated_rows [device int32 B];
  * margin [device fp32 B]; gate [device uint8 B]; n_gated [device int32 1].
  * Bit-exact: comparisons only, no rounding. */
 mg_status mg_margin_gate(mg_ctx* ctx, int B, const float* logits, const uint8_t* protected_mask, float tau,
                          int32_t* top1, float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated,
                          void* stream);
 
-/* (3) The deterministic verifier (Sec. 4.2, "Deterministic verifier contract"):
- * recomputes the current transition of rows rows[0..n) of the step batch with
+/* (3) The deterministic verifier (Sec. 3.2, deterministic verifier contract):
+ * runs the current step again for rows rows[0..n) of the step batch with
  * the canonical reduction order (fixed per-lane groups + xor butterfly for dot
  * products, chunks of 256 positions for attention, own EXP), which depends on
  * neither n, nor the row's place in the list, nor the batch.  The row attends
@@ -132,7 +132,7 @@ mg_status mg_verify_rows(mg_ctx* ctx, int n, const int32_t* rows, const int32_t*
                          const int32_t* positions, const int32_t* page_table, float* v_logits, int32_t* v_tok,
                          uint16_t* v_kvcol, void* stream);
 
-/* (4) Commit and single-column repair (Sec. 4.2): for list entry i with row
+/* (4) Commit and single-column repair (Sec. 3.2): for list entry i with row
  * r = rows[i]: emitted[r] = v_tok[i]; if v_tok[i] != top1[r] the verifier's
  * column v_kvcol[i] overwrites the cache at position positions[r] in every
  * layer and *n_repaired is incremented (device int32, accumulates over calls).
@@ -171,9 +171,10 @@ enum {
 
 /* Start recording a HIP event pair around every launch of kernel class `kind`
  * (on the stream it is launched on), up to max_launches launches.  Creates the
- * events (not allocation-free; call outside timed loops). */
+ * events (not allocation-free; call outside timed loops).  The events are
+ * timing-only: recording them performs no system-scope fence. */
 mg_status mg_profile_begin(mg_ctx* ctx, int kind, int max_launches);
-/* Stop recording, synchronise the recorded events and report the number of
+/* Stop recording, synchronise the device and report the number of
  * launches, their summed duration in milliseconds, the summed algorithmic bytes
  * (every weight, activation, K/V and output byte the launch must move once) and
  * the summed algorithmic flops (2 per multiply-add). */

@@ -8,17 +8,18 @@
  * What is computed, and where the paper fixes it:
  *  - The decoder is a Llama/Qwen-style dense transformer run one row at a time
  *    (rows never interact, so this oracle is batch-invariant by construction).
- *    Storage is bf16 and every reduction accumulates in fp32; the paper's fast
- *    path is "the default BF16 batched forward" (Sec. 4.1, Margin trigger).
+ *    Storage is bf16 and every reduction accumulates in fp32; the fast path is
+ *    the ordinary batched BF16 forward whose logits feed the gate (Sec. 3.1,
+ *    margin trigger).
  *  - The margin is g = l_(1) - l_(2) over the fp32 logits of the current step,
- *    and the verifier fires iff g < tau, strictly (Sec. 4.1).
- *  - The verifier recomputes the current transition and returns a token plus the
- *    K/V column of the current position (Sec. 4.2, Deterministic verifier
+ *    and the verifier fires iff g < tau, strictly (Sec. 3.1).
+ *  - The verifier runs the current step again for the row and returns a token plus the
+ *    K/V column of the current position (Sec. 3.2, Deterministic verifier
  *    contract).  It reads the committed cache for earlier positions and its own
  *    freshly computed column for the current one.
  *  - Commit: fast commit and verified commit keep the tentative column; when the
  *    verifier token differs, the verifier token is emitted and only the current
- *    column is overwritten, in every layer (Sec. 4.2, Single-Column Repair).
+ *    column is overwritten, in every layer (Sec. 3.2, Single-Column Repair).
  *
  * Readings where the paper is silent (each is listed with its reason in the
  * design notes of the repository):

@@ -8,10 +8,10 @@
  * number it produces is recomputed here from the definitions.
  *
  * Paper anchors (section / equation names of arXiv 2605.30218):
- *   Sec. 4.1 "Margin trigger"       g = l_(1) - l_(2); verify iff g < tau
- *   Sec. 4.2 "Single-Column Repair" fast commit / verified commit / repair
- *   Sec. 4.2 "Deterministic verifier contract"
- *   Sec. 4.3 "Verifier Accounting"  r_verify, r_repair
+ *   Sec. 3.1 "Margin trigger"       g = l_(1) - l_(2); verify iff g < tau
+ *   Sec. 3.2 "Single-Column Repair" fast commit / verified commit / repair
+ *   Sec. 3.2 "Deterministic verifier contract"
+ *   Sec. 3.3 "Verifier Accounting"  r_verify, r_repair
  *   Sec. 2.4 (Obs. 3) N(Delta) = |{j : l_j >= l_(1) - Delta}|
  *
  * Two arithmetic modes share one decoder:

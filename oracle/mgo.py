@@ -6,8 +6,8 @@ GPU package: shapes arrive as any object with the model-shape attributes, weight
 and state as numpy arrays.
 
 The gated loop below follows the MarginGate decode step of arXiv 2605.30218:
-Sec. 4.1 (margin trigger g < tau), Sec. 4.2 (fast commit / verified commit /
-single-column repair) and Sec. 4.3 (r_verify, r_repair accounting).
+Sec. 3.1 (margin trigger g < tau), Sec. 3.2 (fast commit / verified commit /
+single-column repair) and Sec. 3.3 (r_verify, r_repair accounting).
 """
 from __future__ import annotations
 
@@ -257,7 +257,7 @@ class OracleModel:
     # -------------------------------------------------------------- the gated loop
 
     def gated_step(self, fast_mode, tokens, positions, page_table, protected, tau, verify="gated"):
-        """One MarginGate step (Sec. 4.1-4.3).  verify in {"off", "gated", "always"}.
+        """One MarginGate step (Sec. 3.1-3.3).  verify in {"off", "gated", "always"}.
         Returns (emitted, record) where record holds logits, top1, margin, gate, rows, v_tok, n_repaired."""
         logits = self.decode_step(fast_mode, tokens, positions, page_table)
         top1, margin, gate, rows = self.margin_gate(logits, protected, tau)

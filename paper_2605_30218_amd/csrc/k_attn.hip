@@ -1,17 +1,16 @@
-// k_attn.hip -- paged GQA decode attention, fast and canonical.
+// k_attn.hip -- paged GQA decode attention, canonical (verifier, prefill) and fast.
 //
-// One block per (item, KV head, chunk of positions).  The block serves the G
-// query heads that share the KV head, so each K/V page row is read from HBM
-// once per item.  K and V of the chunk are staged in LDS 64 positions at a time
-// (K rows padded to an odd word stride: a lane per position reads conflict-free).
-//   score      s_j = (sum_d q_d k_jd, sequential fma over d) * fp32(1/sqrt(hd))
-//   chunk      m = max_j s_j, e_j = exp(s_j - m), l = sum_j e_j,
-//              a[d] = sum_j e_j v_jd (sequential fma over j)
+// Both serve the G query heads that share a KV head from one block or wave, so each
+// K/V page row is read from HBM once per item, and both split the context into
+// chunks whose partial (m, l, a) a combine kernel merges:
+//   score      s_j = (q . k_j) * fp32(1/sqrt(hd))
+//   chunk      m = max_j s_j, e_j = exp(s_j - m), l = sum_j e_j, a[d] = sum_j e_j v_jd
 //   combine    over chunks in ascending order: M = max m_c, w_c = exp(m_c - M),
-//              L = sum w_c l_c, O[d] = sum w_c a_c[d] (sequential fma), out = bf16(O / L)
-// Canonical (the verifier): chunks of 256 positions, so the chunk count depends
-// only on the context length; the verifier's EXP; l summed sequentially in
-// position order.  Fast: any chunk size, hardware exp, tree sum for l.
+//              L = sum w_c l_c, O[d] = sum w_c a_c[d], out = bf16(O / L)
+// Canonical (the verifier): chunks of 256 positions, so the chunk count depends only
+// on the context length; every sum is sequential in a fixed order (d for the scores,
+// position for l and a, chunk for L and O), with fma where the definition has a
+// product; the verifier's EXP.  Fast: 128-position splits, MFMA scores, exp2.
 // The current position p comes from the item's own column when one is given
 // (the verifier never reads the tentative column of the cache).
 #include "mg_device.h"
@@ -21,88 +20,123 @@ namespace mg {
 
 constexpr int ATT_MAXG = 8;     // query heads per KV head
 constexpr int ATT_MAXHD = 128;
-constexpr int ATT_MAXC = 256;   // positions per chunk
-constexpr int ATT_SUB = 64;     // positions staged at a time
+constexpr int ATT_MAXC = 256;   // positions per canonical chunk
 
 __device__ __forceinline__ float attn_scale(int hd) { return hd == 128 ? 0x1.6a09e6p-4f : 0x1.0p-3f; }
 
-template <bool CANON>
-__global__ __launch_bounds__(256) void attn_chunk_kernel(AttnArgs a) {
+// Canonical attention: one block of 256 threads per (item, KV head, chunk of 256
+// positions).  Thread j loads the K row of position j into registers and the block's
+// V rows are staged into LDS; every K and V load of the chunk is issued at once, so
+// the block waits for memory once.  The sequential chains below read LDS in unrolled
+// batches, so their loads are in flight together.
+//   scores  thread j: s_j for each query head of the group, sequential fma over d, * scale
+//   chunk   wave w: heads w, w + 4: m = max_j s_j, e_j = EXP(s_j - m) in place
+//   l       thread h < G: sequential sum of e_j in position order
+//   values  thread t: d pair (2 dp, 2 dp + 1) of the heads hg, hg + 256 / (hd/2), ...:
+//           a[d] = sequential fma over j of e_j v_jd
+template <int HD>
+__global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
+    constexpr int U4 = HD / 8;                // 16-byte pieces per K/V row
+    constexpr int NLD = ATT_MAXC * U4 / 256;  // V pieces per thread
+    constexpr int HP = HD / 2;                // d pairs (words per V row)
+    constexpr int HPT = 256 / HP;             // head groups over the block's threads
+    constexpr int NPG = ATT_MAXC / 16;        // pages per chunk
+    constexpr int UB = 8;                     // positions per batch of LDS reads
+    static_assert(NLD * 256 == ATT_MAXC * U4, "pieces must divide evenly");
+
+    __shared__ __attribute__((aligned(16))) uint32_t vs[ATT_MAXC * HP];
+    __shared__ __attribute__((aligned(16))) float qs[ATT_MAXG * HD];
+    __shared__ __attribute__((aligned(16))) float ps[ATT_MAXG * ATT_MAXC];
+    __shared__ float red[ATT_MAXG][2];
+    __shared__ const uint16_t* pgk[NPG];
+
     const int i = blockIdx.z;
     if (i >= items_n(a.it)) return;
     const int kh = blockIdx.y, c = blockIdx.x;
     const int r = items_row(a.it, i), p = items_pos(a.it, i);
-    const int C = a.chunk;
-    const int j0 = c * C;
+    const int j0 = c * ATT_MAXC;
     if (j0 > p) return;
-    const int nj = min(C, p + 1 - j0);
+    const int nj = min(ATT_MAXC, p + 1 - j0);
     const ModelDims& m = a.m;
-    const int hd = m.hd, G = m.Hq / m.Hkv, Nk = m.Hkv * hd;
-    const int KW = hd / 2 + 1;  // 32-bit words per staged K row (odd)
-
-    __shared__ float qs[ATT_MAXG * ATT_MAXHD];
-    __shared__ uint32_t ks[ATT_SUB * (ATT_MAXHD / 2 + 1)];
-    __shared__ float ps[ATT_MAXG * ATT_MAXC];
-    __shared__ __attribute__((aligned(16))) uint16_t vsh[ATT_SUB * ATT_MAXHD];
-    __shared__ float red[ATT_MAXG][2];
-
+    const int G = m.Hq / m.Hkv, Nk = m.Hkv * HD;
     const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
-    const uint16_t* qrow = a.qrot + (size_t)i * m.Hq * hd + (size_t)kh * G * hd;
-    for (int e = t; e < G * hd; e += 256) qs[e] = bf2f(qrow[e]);
-    const float scale = attn_scale(hd);
-    const int32_t* ptab = a.it.page_table + (size_t)r * m.max_pages_per_row;
-    const uint16_t* own = a.own_col ? a.own_col + ((size_t)i * m.L + a.layer) * 2 * Nk + (size_t)kh * hd : nullptr;
+    const size_t kv_stride = (size_t)m.Hkv * m.page_size * HD;  // K -> V of the same page
 
-    auto src_row = [&](int jpos, int kv) -> const uint16_t* {
-        if (own && jpos == p) return own + (size_t)kv * Nk;
-        const int page = ptab[jpos / m.page_size], slot = jpos % m.page_size;
-        return a.kv_pool + ((((size_t)a.layer * m.n_pages + page) * 2 + kv) * m.Hkv + kh) * (size_t)m.page_size * hd +
-               (size_t)slot * hd;
+    // K base of each page of the chunk (page_size is 16)
+    if (t < NPG) {
+        const int jp = j0 + 16 * t;
+        pgk[t] = jp <= p ? a.kv_pool + ((((size_t)a.layer * m.n_pages + a.it.page_table[(size_t)r * m.max_pages_per_row +
+                                                                                           jp / 16]) * 2) * m.Hkv + kh) *
+                                           (size_t)m.page_size * HD
+                         : nullptr;
+    }
+    const uint16_t* qrow = a.qrot + (size_t)i * m.Hq * HD + (size_t)kh * G * HD;
+    for (int e = t; e < G * HD; e += 256) qs[e] = bf2f(qrow[e]);
+    const uint16_t* own = a.own_col ? a.own_col + ((size_t)i * m.L + a.layer) * 2 * Nk + (size_t)kh * HD : nullptr;
+    __syncthreads();
+
+    auto row_ptr = [&](int jj) -> const uint16_t* {  // K row of chunk position jj < nj
+        if (own && j0 + jj == p) return own;
+        return pgk[jj >> 4] + (size_t)(jj & 15) * HD;
     };
-
-    const int nsub = (nj + ATT_SUB - 1) / ATT_SUB;
-    const int u4 = hd / 8;  // 16-byte pieces per row
-    // ---- scores
-    for (int sc = 0; sc < nsub; ++sc) {
-        const int jb = j0 + sc * ATT_SUB;
-        const int nn = min(ATT_SUB, j0 + nj - jb);
-        __syncthreads();
-        {   // all staging loads of the sub-chunk in flight before the LDS stores
-            constexpr int NLD = ATT_SUB * ATT_MAXHD / 8 / 256;
-            uint4 v[NLD];
+    uint4 kr[U4], vr[NLD];
+    if (t < nj) {
+        const uint4* kp = reinterpret_cast<const uint4*>(row_ptr(t));
 #pragma unroll
-            for (int k = 0; k < NLD; ++k) {
-                const int e = t + 256 * k;
-                v[k] = e < nn * u4 ? reinterpret_cast<const uint4*>(src_row(jb + e / u4, 0))[e % u4] : make_uint4(0, 0, 0, 0);
-            }
+        for (int k = 0; k < U4; ++k) kr[k] = kp[k];
+    }
 #pragma unroll
-            for (int k = 0; k < NLD; ++k) {
-                const int e = t + 256 * k;
-                if (e < nn * u4) {
-                    uint32_t* dst = ks + (e / u4) * KW + (e % u4) * 4;
-                    dst[0] = v[k].x; dst[1] = v[k].y; dst[2] = v[k].z; dst[3] = v[k].w;
-                }
-            }
-        }
-        __syncthreads();
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-            const int h = wave + 4 * hh;
-            if (h < G && lane < nn) {
-                const uint32_t* kr = ks + lane * KW;
-                const float* qh = qs + h * hd;
-                float s = 0.0f;
-                for (int w2 = 0; w2 < hd / 2; ++w2) {
-                    const uint32_t kw = kr[w2];
-                    s = __builtin_fmaf(qh[2 * w2], bf_lo(kw), s);
-                    s = __builtin_fmaf(qh[2 * w2 + 1], bf_hi(kw), s);
-                }
-                ps[h * ATT_MAXC + sc * ATT_SUB + lane] = s * scale;
-            }
+    for (int k = 0; k < NLD; ++k) {
+        const int e = t + 256 * k;
+        const int jj = e / U4, pc = e % U4;
+        vr[k] = make_uint4(0, 0, 0, 0);
+        if (jj < nj) {
+            const uint16_t* kp = row_ptr(jj);
+            const uint16_t* vp = (own && j0 + jj == p) ? own + Nk : kp + kv_stride;
+            vr[k] = *reinterpret_cast<const uint4*>(vp + pc * 8);
         }
     }
+#pragma unroll
+    for (int k = 0; k < NLD; ++k) {
+        const int e = t + 256 * k;
+        *reinterpret_cast<uint4*>(vs + (e / U4) * HP + (e % U4) * 4) = vr[k];
+    }
+
+    // ---- scores: position t, all heads of the group at once (K in registers)
+    const float scale = attn_scale(HD);
+    if (t < nj) {
+        float sc[ATT_MAXG];
+#pragma unroll
+        for (int h = 0; h < ATT_MAXG; ++h) sc[h] = 0.0f;
+#pragma unroll
+        for (int k = 0; k < U4; ++k) {
+            const float kf[8] = {bf_lo(kr[k].x), bf_hi(kr[k].x), bf_lo(kr[k].y), bf_hi(kr[k].y),
+                                 bf_lo(kr[k].z), bf_hi(kr[k].z), bf_lo(kr[k].w), bf_hi(kr[k].w)};
+#pragma unroll
+            for (int h = 0; h < ATT_MAXG; ++h) {
+                if (h < G) {
+                    const float4 q0 = *reinterpret_cast<const float4*>(qs + h * HD + 8 * k);
+                    const float4 q1 = *reinterpret_cast<const float4*>(qs + h * HD + 8 * k + 4);
+                    float s = sc[h];
+                    s = __builtin_fmaf(q0.x, kf[0], s);
+                    s = __builtin_fmaf(q0.y, kf[1], s);
+                    s = __builtin_fmaf(q0.z, kf[2], s);
+                    s = __builtin_fmaf(q0.w, kf[3], s);
+                    s = __builtin_fmaf(q1.x, kf[4], s);
+                    s = __builtin_fmaf(q1.y, kf[5], s);
+                    s = __builtin_fmaf(q1.z, kf[6], s);
+                    s = __builtin_fmaf(q1.w, kf[7], s);
+                    sc[h] = s;
+                }
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < ATT_MAXG; ++h)
+            if (h < G) ps[h * ATT_MAXC + t] = sc[h] * scale;
+    }
     __syncthreads();
-    // ---- chunk max, exponentials (and the fast sum)
+
+    // ---- chunk max and exponentials
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
         const int h = wave + 4 * hh;
@@ -110,77 +144,79 @@ __global__ __launch_bounds__(256) void attn_chunk_kernel(AttnArgs a) {
             float mx = -__builtin_inff();
             for (int j = lane; j < nj; j += 64) mx = fmaxf(mx, ps[h * ATT_MAXC + j]);
             mx = wave_max(mx);
-            float ls = 0.0f;
-            for (int j = lane; j < nj; j += 64) {
-                const float d = ps[h * ATT_MAXC + j] - mx;
-                const float e = CANON ? canon_exp(d) : __expf(d);
-                ps[h * ATT_MAXC + j] = e;
-                ls += e;
-            }
-            if (!CANON) ls = wave_sum_fast(ls);
-            if (lane == 0) {
-                red[h][0] = mx;
-                red[h][1] = ls;
-            }
+            for (int j = lane; j < nj; j += 64) ps[h * ATT_MAXC + j] = canon_exp(ps[h * ATT_MAXC + j] - mx);
+            if (lane == 0) red[h][0] = mx;
         }
     }
     __syncthreads();
-    if (CANON && t < G) {  // l = sum of e_j in position order
+
+    // ---- l (sequential in position order) and the weighted values
+    const int nb = nj / UB * UB;  // positions handled in whole batches
+    if (t < G) {
+        const float* ph = ps + t * ATT_MAXC;
         float l = 0.0f;
-        for (int j = 0; j < nj; ++j) l = l + ps[t * ATT_MAXC + j];
+        for (int j = 0; j < nb; j += UB) {
+            const float4 e0 = *reinterpret_cast<const float4*>(ph + j);
+            const float4 e1 = *reinterpret_cast<const float4*>(ph + j + 4);
+            l = l + e0.x; l = l + e0.y; l = l + e0.z; l = l + e0.w;
+            l = l + e1.x; l = l + e1.y; l = l + e1.z; l = l + e1.w;
+        }
+        for (int j = nb; j < nj; ++j) l = l + ph[j];
         red[t][1] = l;
     }
-    // ---- weighted values
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int sc = 0; sc < nsub; ++sc) {
-        const int jb = j0 + sc * ATT_SUB;
-        const int nn = min(ATT_SUB, j0 + nj - jb);
-        __syncthreads();
-        {
-            constexpr int NLD = ATT_SUB * ATT_MAXHD / 8 / 256;
-            uint4 v[NLD];
+    const int dp = t % HP, hg = t / HP;
+    constexpr int NH = (ATT_MAXG + HPT - 1) / HPT;  // heads per thread
+    float acc[NH][2];
 #pragma unroll
-            for (int k = 0; k < NLD; ++k) {
-                const int e = t + 256 * k;
-                v[k] = e < nn * u4 ? reinterpret_cast<const uint4*>(src_row(jb + e / u4, 1))[e % u4] : make_uint4(0, 0, 0, 0);
-            }
+    for (int u = 0; u < NH; ++u) acc[u][0] = acc[u][1] = 0.0f;
+    for (int j = 0; j < nb; j += UB) {
+        uint32_t vw[UB];
 #pragma unroll
-            for (int k = 0; k < NLD; ++k) {
-                const int e = t + 256 * k;
-                if (e < nn * u4) reinterpret_cast<uint4*>(vsh + (e / u4) * hd)[e % u4] = v[k];
+        for (int b = 0; b < UB; ++b) vw[b] = vs[(j + b) * HP + dp];
+#pragma unroll
+        for (int u = 0; u < NH; ++u) {
+            const int h = hg + HPT * u;
+            if (h < G) {
+                const float4 e0 = *reinterpret_cast<const float4*>(ps + h * ATT_MAXC + j);
+                const float4 e1 = *reinterpret_cast<const float4*>(ps + h * ATT_MAXC + j + 4);
+                const float e[UB] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+#pragma unroll
+                for (int b = 0; b < UB; ++b) {
+                    acc[u][0] = __builtin_fmaf(e[b], bf_lo(vw[b]), acc[u][0]);
+                    acc[u][1] = __builtin_fmaf(e[b], bf_hi(vw[b]), acc[u][1]);
+                }
             }
         }
-        __syncthreads();
+    }
+    for (int j = nb; j < nj; ++j) {
+        const uint32_t vw = vs[j * HP + dp];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int o = t + 256 * k;
-            if (o < G * hd) {
-                const int h = o / hd, d = o % hd;
-                const float* ph = ps + h * ATT_MAXC + sc * ATT_SUB;
-                float s = acc[k];
-                for (int pp = 0; pp < nn; ++pp) s = __builtin_fmaf(ph[pp], bf2f(vsh[pp * hd + d]), s);
-                acc[k] = s;
+        for (int u = 0; u < NH; ++u) {
+            const int h = hg + HPT * u;
+            if (h < G) {
+                const float e = ps[h * ATT_MAXC + j];
+                acc[u][0] = __builtin_fmaf(e, bf_lo(vw), acc[u][0]);
+                acc[u][1] = __builtin_fmaf(e, bf_hi(vw), acc[u][1]);
             }
         }
     }
     __syncthreads();
-    const int stride = hd + 2;
+    constexpr int stride = HD + 2;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int o = t + 256 * k;
-        if (o < G * hd) {
-            const int h = o / hd, d = o % hd;
+    for (int u = 0; u < NH; ++u) {
+        const int h = hg + HPT * u;
+        if (h < G) {
             float* dst = a.part + (((size_t)i * m.Hq + kh * G + h) * a.max_chunks + c) * stride;
-            if (d == 0) {
+            if (dp == 0) {
                 dst[0] = red[h][0];
                 dst[1] = red[h][1];
             }
-            dst[2 + d] = acc[k];
+            dst[2 + 2 * dp] = acc[u][0];
+            dst[3 + 2 * dp] = acc[u][1];
         }
     }
 }
 
-template <bool CANON>
 __global__ void attn_combine_kernel(AttnArgs a) {
     const int i = blockIdx.y;
     if (i >= items_n(a.it)) return;
@@ -196,7 +232,7 @@ __global__ void attn_combine_kernel(AttnArgs a) {
     float L = 0.0f, O = 0.0f;
     for (int c = 0; c < S; ++c) {
         const float mc = base[(size_t)c * stride];
-        const float w = CANON ? canon_exp(mc - M) : __expf(mc - M);
+        const float w = canon_exp(mc - M);
         L = __builtin_fmaf(w, base[(size_t)c * stride + 1], L);
         O = __builtin_fmaf(w, base[(size_t)c * stride + 2 + d], O);
     }
@@ -389,8 +425,12 @@ hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     dim3 g1(a.max_chunks, a.m.Hkv, n), g2(a.m.Hq, n);
     if (canon) {
-        hipLaunchKernelGGL(attn_chunk_kernel<true>, g1, dim3(256), 0, s, a);
-        hipLaunchKernelGGL(attn_combine_kernel<true>, g2, dim3(a.m.hd), 0, s, a);
+        if (a.chunk != ATT_MAXC) return hipErrorInvalidValue;
+        if (a.m.hd == 128)
+            hipLaunchKernelGGL(attn_canon_kernel<128>, g1, dim3(256), 0, s, a);
+        else
+            hipLaunchKernelGGL(attn_canon_kernel<64>, g1, dim3(256), 0, s, a);
+        hipLaunchKernelGGL(attn_combine_kernel, g2, dim3(a.m.hd), 0, s, a);
     } else {
         if (a.m.hd == 128)
             hipLaunchKernelGGL(attn_fast_kernel<128>, g1, dim3(64), 0, s, a);

@@ -23,9 +23,15 @@ namespace mg {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
+#ifndef MG_GEMM_KC_SMALL
+#define MG_GEMM_KC_SMALL 128
+#endif
+// K per chunk for a tile of MT 16-row tiles (host and device must agree)
+__host__ __device__ constexpr int gemm_kc(int MT) { return MT <= 4 ? MG_GEMM_KC_SMALL : MT <= 8 ? 128 : 64; }
+
 template <int MT>
 struct GemmShape {
-    static constexpr int KC = MT <= 8 ? 128 : 64;  // K per chunk
+    static constexpr int KC = gemm_kc(MT);  // K per chunk
     static constexpr int ROWS = 16 * MT;
     static constexpr int STRIDE = KC * 2 + 16;    // LDS bytes per staged row
     static constexpr int NST = KC / 32;           // MFMA k-steps per chunk
@@ -266,7 +272,7 @@ int fast_gemm_ft(int M, int N) {
 
 int fast_gemm_splits(int M, int N, int K, int n_cu) {
     g_n_cu = n_cu;
-    const int KC = mt_for(M) <= 8 ? 128 : 64;
+    const int KC = gemm_kc(mt_for(M));
     const int nchunks = (K + KC - 1) / KC;
     const int FB = 64 * fast_gemm_ft(M, N);
     const int nb = (N + FB - 1) / FB;

@@ -521,7 +521,10 @@ mg_status mg_profile_begin(mg_ctx* c, int kind, int max_launches) {
     ProfKind& k = c->prof[kind];
     while ((int)k.ev0.size() < max_launches) {
         hipEvent_t a, b;
-        if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) return MG_ERR_HIP;
+        // timing-only events: no system-scope fence (cache writeback and invalidate) per record
+        if (hipEventCreateWithFlags(&a, hipEventDisableSystemFence) != hipSuccess ||
+            hipEventCreateWithFlags(&b, hipEventDisableSystemFence) != hipSuccess)
+            return MG_ERR_HIP;
         k.ev0.push_back(a);
         k.ev1.push_back(b);
     }
@@ -539,6 +542,7 @@ mg_status mg_profile_end(mg_ctx* c, int kind, int* n_launches, double* total_ms,
         return MG_ERR_ARG;
     ProfKind& k = c->prof[kind];
     k.on = false;
+    if (hipDeviceSynchronize() != hipSuccess) return MG_ERR_HIP;
     double tot = 0.0;
     for (int i = 0; i < k.used; ++i) {
         if (hipEventSynchronize(k.ev1[i]) != hipSuccess) return MG_ERR_HIP;

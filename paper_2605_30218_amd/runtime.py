@@ -1,10 +1,10 @@
-"""Host-side sequencing of the MarginGate decode loop over libmg (arXiv 2605.30218, Sec. 4).
+"""Host-side sequencing of the MarginGate decode loop over libmg (arXiv 2605.30218, Sec. 3).
 
 Per step: the fast batched forward (tentative K/V append), the margin gate, one
 device-to-host read of the gated-row count, the verifier on exactly those rows, and
 the commit / single-column repair.  Modes: "off" (fast path only, r_verify = 0),
 "gated" (MarginGate), "always" (the verifier on every protected row, r_verify = 1:
-the always-on baseline of Sec. 4.3).  All arithmetic runs in libmg; this module only
+the always-on baseline of Sec. 3.3).  All arithmetic runs in libmg; this module only
 orders calls and keeps counters.
 """
 from __future__ import annotations

@@ -3,7 +3,7 @@
 This module holds none of the method's arithmetic.  It is the one piece of code that
 both the GPU path (through its tests and benchmark) and the CPU oracle consume, so the
 two sides read the same bytes.  The real models and datasets of arXiv 2605.30218
-(Sec. 5.1: Llama-3.x, Qwen2.5, MATH500, GSM8K, ...) are not available; these inputs
+(Sec. 4.1: Llama-3.x, Qwen2.5, MATH500, GSM8K, ...) are not available; these inputs
 stand in for them with the same shapes: weights N(0, 0.02) rounded to bf16, RMSNorm
 gains 1, untied embedding and LM head, uniform random prompt token ids.
 """

@@ -7,7 +7,7 @@ vocab 4096, page 16): GPU through the C ABI against the CPU oracle on the same i
   verifier batch invariance                        bit-identical for 1..256 rows, any placement
   gated loop, state-forced                         every gate, verifier token and repaired column exact
   gated loop, free-running                         token for token with the oracle (near-ties adjudicated)
-Paper: arXiv 2605.30218 Sec. 4.1-4.3."""
+Paper: arXiv 2605.30218 Sec. 3.1-3.3."""
 import numpy as np
 import pytest
 import torch
@@ -253,7 +253,7 @@ def test_free_running_matches_oracle_token_for_token(pair, prompts):
 
 
 def test_protected_row_alone_vs_in_batch(pair, prompts):
-    """Sequence determinism (Sec. 5.1): row 0 decoded at bs=1 and inside bs=4 emits the same
+    """Sequence determinism (Sec. 4.1): row 0 decoded at bs=1 and inside bs=4 emits the same
     tokens when every low-margin step is verified (tau = 0.5)."""
     steps = 20
     seqs = []

@@ -3,8 +3,8 @@
 Each test checks one oracle function against something other than itself: closed forms,
 exact small-integer arithmetic, brute force, library routines in float64, hand-derived
 fixtures (tests/golden/), invariants of the definitions.  Paper anchors: arXiv 2605.30218
-Sec. 4.1 (margin g = l_(1) - l_(2), trigger g < tau), Sec. 2.4 / Obs. 3 (N(Delta) > 1 iff
-g < Delta), Sec. 4.2 (fast commit, verified commit, single-column repair), Sec. 4.3
+Sec. 3.1 (margin g = l_(1) - l_(2), trigger g < tau), Sec. 2.4 / Obs. 3 (N(Delta) > 1 iff
+g < Delta), Sec. 3.2 (fast commit, verified commit, single-column repair), Sec. 3.3
 (r_verify, r_repair).
 """
 import json
@@ -485,7 +485,7 @@ def test_verifier_scratch_column_equals_cache_path():
 
 
 def test_repair_overwrites_only_the_current_column():
-    """Sec. 4.2: a verified commit keeps the tentative column; a repair copies the verifier's
+    """Sec. 3.2: a verified commit keeps the tentative column; a repair copies the verifier's
     column at the current position in every layer and nothing else."""
     om, w, pt = _tiny_model(max_batch=3, ctx=48)
     rng = np.random.default_rng(0)
