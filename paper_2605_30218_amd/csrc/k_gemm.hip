@@ -5,16 +5,19 @@
 // owns 16*FT of them for all rows.  Weights go straight from HBM into MFMA
 // B-operand registers: lane (j, q) loads W[n+j][k+8q .. k+8q+7] (16 bytes), so a
 // 32-wide k step of 16 features reads 16 rows x 64 contiguous bytes.  The block
-// walks its K range in chunks of KC; while the MFMAs of chunk c run, the weights
-// of chunks c+1 and c+2 are already in flight (three register buffers) and the activations
-// of chunk c+1 are staged into the other half of a double-buffered LDS tile (rows
-// padded by 16 bytes so the A-operand lanes of a k group hit distinct banks).
-// One barrier per chunk.  The K range may be split over blocks (split-K): each
-// split writes its fp32 partial tile and the kernel that consumes the projection
-// (RoPE and K/V append, or residual add + RMSNorm) sums the splits in split order,
-// so blocks never wait for each other and no cache-flushing fence is needed.  The
-// summation order depends on M (tile and chunk choice) and on the split count:
-// this path may be batch-variant.
+// walks its K range in chunks of KC.  Chunk c+1 is requested while the MFMAs of
+// chunk c run: its activations first, then its weights, into the other register
+// buffer of a ping-pong pair (the loop is unrolled by two, so no buffer is copied).
+// Loads complete in order, so staging the activations of chunk c+1 into the other
+// half of the double-buffered LDS tile waits only for those, and the weights of
+// chunk c+1 stay in flight across the barrier.  Every load is unconditional (rows
+// past N read row 0, k past K reads the row's last group; the activations there
+// are zero and the results are discarded).  The K range may be split over blocks
+// (split-K): each split writes its fp32 partial tile and the kernel that consumes
+// the projection (RoPE and K/V append, SwiGLU, or residual add + RMSNorm) sums the
+// splits in split order, so blocks never wait for each other.  The summation order
+// depends on M (tile and chunk choice) and on the split count: this path may be
+// batch-variant.
 #include "mg_device.h"
 #include "mg_kernels.h"
 
@@ -54,68 +57,64 @@ __device__ __forceinline__ void fast_epilogue(const FastGemmArgs& a, int split, 
     }
 }
 
-__device__ __forceinline__ float silu_fast(float g) { return g / (1.0f + __expf(-g)); }
-
-template <int MT, bool SWI>
+// activations of chunk kc: rows past M read row M-1; groups past K read the row's
+// last group and are zeroed when staged (so the wait for the data happens at the store)
+template <int MT>
 __device__ __forceinline__ void load_x(const FastGemmArgs& a, int kc, uint4 (&xr)[GemmShape<MT>::XLD]) {
     using S = GemmShape<MT>;
 #pragma unroll
     for (int it = 0; it < S::XLD; ++it) {
         const int t = threadIdx.x + 256 * it;
-        const int row = t / S::GPR, g = t % S::GPR;
-        const int k = kc + g * 8;
-        uint4 v = make_uint4(0, 0, 0, 0);
-        if (row < a.M && k < a.K) {
-            if (!SWI) {
-                v = *reinterpret_cast<const uint4*>(a.X + (size_t)row * a.K + k);
-            } else {
-                const uint4 gv = *reinterpret_cast<const uint4*>(a.X + (size_t)row * 2 * a.K + k);
-                const uint4 uv = *reinterpret_cast<const uint4*>(a.X + (size_t)row * 2 * a.K + a.K + k);
-                v.x = pack_bf2(silu_fast(bf_lo(gv.x)) * bf_lo(uv.x), silu_fast(bf_hi(gv.x)) * bf_hi(uv.x));
-                v.y = pack_bf2(silu_fast(bf_lo(gv.y)) * bf_lo(uv.y), silu_fast(bf_hi(gv.y)) * bf_hi(uv.y));
-                v.z = pack_bf2(silu_fast(bf_lo(gv.z)) * bf_lo(uv.z), silu_fast(bf_hi(gv.z)) * bf_hi(uv.z));
-                v.w = pack_bf2(silu_fast(bf_lo(gv.w)) * bf_lo(uv.w), silu_fast(bf_hi(gv.w)) * bf_hi(uv.w));
-            }
-        }
-        xr[it] = v;
+        const int row = min(t / S::GPR, a.M - 1), k = kc + (t % S::GPR) * 8;
+        xr[it] = *reinterpret_cast<const uint4*>(a.X + (size_t)row * a.K + min(k, a.K - 8));
     }
 }
 
 template <int MT>
-__device__ __forceinline__ void store_x(unsigned char* buf, const uint4 (&xr)[GemmShape<MT>::XLD]) {
+__device__ __forceinline__ void store_x(unsigned char* buf, int kc, int K, const uint4 (&xr)[GemmShape<MT>::XLD]) {
     using S = GemmShape<MT>;
 #pragma unroll
     for (int it = 0; it < S::XLD; ++it) {
         const int t = threadIdx.x + 256 * it;
         const int row = t / S::GPR, g = t % S::GPR;
-        *reinterpret_cast<uint4*>(buf + row * S::STRIDE + g * 16) = xr[it];
+        const uint32_t keep = 0u - (uint32_t)(kc + g * 8 < K);
+        const uint4 v = make_uint4(xr[it].x & keep, xr[it].y & keep, xr[it].z & keep, xr[it].w & keep);
+        *reinterpret_cast<uint4*>(buf + row * S::STRIDE + g * 16) = v;
     }
 }
 
-#ifndef MG_GEMM_KPERM
-#define MG_GEMM_KPERM 0
-#endif
-// k offset, inside a chunk, of the 8 values lane group q supplies at MFMA k-step st.
-// MG_GEMM_KPERM = 1 permutes the chunk so a lane's NST groups are contiguous (each
-// weight row read as 4 lanes x 16*NST contiguous bytes per chunk instead of 64 bytes
-// per k-step); measured slower than the natural order on MI355X, so off by default.
-template <int NST>
-__device__ __forceinline__ int kofs(int st, int q) { return MG_GEMM_KPERM ? q * 8 * NST + st * 8 : st * 32 + q * 8; }
-
+// weights of chunk kc: lane group q supplies k = kc + 32 st + 8 q .. +7 at k-step st
 template <int MT, int FT>
-__device__ __forceinline__ void load_w(const uint16_t* const (&wrow)[FT], const bool (&wok)[FT], int kc, int K, int q,
+__device__ __forceinline__ void load_w(const uint16_t* const (&wrow)[FT], int kc, int K, int q,
                                        uint4 (&wr)[GemmShape<MT>::NST][FT]) {
     using S = GemmShape<MT>;
 #pragma unroll
     for (int st = 0; st < S::NST; ++st) {
-        const int k = kc + kofs<S::NST>(st, q);
+        const int k = min(kc + st * 32 + q * 8, K - 8);
 #pragma unroll
-        for (int f = 0; f < FT; ++f)
-            wr[st][f] = (wok[f] && k < K) ? *reinterpret_cast<const uint4*>(wrow[f] + k) : make_uint4(0, 0, 0, 0);
+        for (int f = 0; f < FT; ++f) wr[st][f] = *reinterpret_cast<const uint4*>(wrow[f] + k);
     }
 }
 
-template <int MT, int FT, int EPI, bool SWI, int PF>
+template <int MT, int FT>
+__device__ __forceinline__ void mfma_chunk(const unsigned char* buf, int jl, int q, const uint4 (&w)[GemmShape<MT>::NST][FT],
+                                           f32x4_t (&acc)[MT][FT]) {
+    using S = GemmShape<MT>;
+#pragma unroll
+    for (int st = 0; st < S::NST; ++st) {
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const uint4 av = *reinterpret_cast<const uint4*>(buf + (16 * mt + jl) * S::STRIDE + (st * 32 + q * 8) * 2);
+            const bf16x8_t A = __builtin_bit_cast(bf16x8_t, av);
+#pragma unroll
+            for (int f = 0; f < FT; ++f)
+                acc[mt][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8_t, w[st][f]), acc[mt][f],
+                                                                      0, 0, 0);
+        }
+    }
+}
+
+template <int MT, int FT, int EPI>
 __global__ __launch_bounds__(256) void fast_gemm_kernel(FastGemmArgs a) {
     using S = GemmShape<MT>;
     __shared__ __attribute__((aligned(16))) unsigned char xs[2][S::ROWS * S::STRIDE];
@@ -148,81 +147,38 @@ __global__ __launch_bounds__(256) void fast_gemm_kernel(FastGemmArgs a) {
 #pragma unroll
         for (int f = 0; f < FT; ++f) acc[mt][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    if constexpr (PF == 1) {
-        // weights prefetched one chunk ahead (register double buffer)
-        uint4 wcur[S::NST][FT], wnext[S::NST][FT];
-        uint4 xr[S::XLD];
-        if (c0 < c1) {
-            load_w<MT, FT>(wrow, wok, c0 * S::KC, K, q, wcur);
-            load_x<MT, SWI>(a, c0 * S::KC, xr);
-            store_x<MT>(xs[c0 & 1], xr);
-        }
+    uint4 wA[S::NST][FT], wB[S::NST][FT];
+    uint4 xr[S::XLD];
+    if (c0 < c1) {
+        load_x<MT>(a, c0 * S::KC, xr);
+        load_w<MT, FT>(wrow, c0 * S::KC, K, q, wA);
+        store_x<MT>(xs[c0 & 1], c0 * S::KC, K, xr);
+    }
+    __syncthreads();
+    // one chunk with a successor: request chunk c+1 (activations, then weights into
+    // `nxt`), run chunk c from `cur`, stage the activations of c+1, barrier.  The
+    // requests are unconditional inside the loop, so the compiler's wait for `cur`
+    // leaves the requests of c+1 in flight.
+    auto step = [&](int c, uint4 (&cur)[S::NST][FT], uint4 (&nxt)[S::NST][FT]) {
+        load_x<MT>(a, (c + 1) * S::KC, xr);
+        load_w<MT, FT>(wrow, (c + 1) * S::KC, K, q, nxt);
+        // keep every request of chunk c+1 ahead of the MFMAs of chunk c
+        __builtin_amdgcn_sched_barrier(0);
+        mfma_chunk<MT, FT>(xs[c & 1], jl, q, cur, acc);
+        store_x<MT>(xs[(c + 1) & 1], (c + 1) * S::KC, K, xr);
         __syncthreads();
-        for (int c = c0; c < c1; ++c) {
-            const bool more = c + 1 < c1;
-            if (more) {
-                load_w<MT, FT>(wrow, wok, (c + 1) * S::KC, K, q, wnext);
-                load_x<MT, SWI>(a, (c + 1) * S::KC, xr);
-            }
-            const unsigned char* buf = xs[c & 1];
-#pragma unroll
-            for (int st = 0; st < S::NST; ++st) {
-#pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const uint4 av = *reinterpret_cast<const uint4*>(buf + (16 * mt + jl) * S::STRIDE + kofs<S::NST>(st, q) * 2);
-                    const bf16x8_t A = __builtin_bit_cast(bf16x8_t, av);
-#pragma unroll
-                    for (int f = 0; f < FT; ++f)
-                        acc[mt][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            A, __builtin_bit_cast(bf16x8_t, wcur[st][f]), acc[mt][f], 0, 0, 0);
-                }
-            }
-            if (more) store_x<MT>(xs[(c + 1) & 1], xr);
-            __syncthreads();
-            if (more) {
-#pragma unroll
-                for (int st = 0; st < S::NST; ++st)
-#pragma unroll
-                    for (int f = 0; f < FT; ++f) wcur[st][f] = wnext[st][f];
-            }
-        }
-    } else {
-        // weights are prefetched two chunks ahead into three rotating register buffers;
-        // the chunk loop is unrolled by three so every buffer index is a constant
-        uint4 wb0[S::NST][FT], wb1[S::NST][FT], wb2[S::NST][FT];
-        uint4 xr[S::XLD];
-        if (c0 < c1) {
-            load_w<MT, FT>(wrow, wok, c0 * S::KC, K, q, wb0);
-            if (c0 + 1 < c1) load_w<MT, FT>(wrow, wok, (c0 + 1) * S::KC, K, q, wb1);
-            load_x<MT, SWI>(a, c0 * S::KC, xr);
-            store_x<MT>(xs[c0 & 1], xr);  // chunk c always lives in buffer c & 1
-        }
-        __syncthreads();
-        auto step = [&](int c, uint4 (&cur)[S::NST][FT], uint4 (&far)[S::NST][FT]) {
-            if (c + 2 < c1) load_w<MT, FT>(wrow, wok, (c + 2) * S::KC, K, q, far);
-            const bool more = c + 1 < c1;
-            if (more) load_x<MT, SWI>(a, (c + 1) * S::KC, xr);
-            const unsigned char* buf = xs[c & 1];
-    #pragma unroll
-            for (int st = 0; st < S::NST; ++st) {
-    #pragma unroll
-                for (int mt = 0; mt < MT; ++mt) {
-                    const uint4 av = *reinterpret_cast<const uint4*>(buf + (16 * mt + jl) * S::STRIDE + kofs<S::NST>(st, q) * 2);
-                    const bf16x8_t A = __builtin_bit_cast(bf16x8_t, av);
-    #pragma unroll
-                    for (int f = 0; f < FT; ++f)
-                        acc[mt][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, __builtin_bit_cast(bf16x8_t, cur[st][f]),
-                                                                              acc[mt][f], 0, 0, 0);
-                }
-            }
-            if (more) store_x<MT>(xs[(c + 1) & 1], xr);
-            __syncthreads();
-        };
-        for (int c = c0; c < c1; c += 3) {
-            step(c, wb0, wb2);
-            if (c + 1 < c1) step(c + 1, wb1, wb0);
-            if (c + 2 < c1) step(c + 2, wb2, wb1);
-        }
+    };
+    int c = c0;
+    for (; c + 2 < c1; c += 2) {
+        step(c, wA, wB);
+        step(c + 1, wB, wA);
+    }
+    // the last one or two chunks
+    if (c + 1 < c1) {
+        step(c, wA, wB);
+        mfma_chunk<MT, FT>(xs[(c + 1) & 1], jl, q, wB, acc);
+    } else if (c < c1) {
+        mfma_chunk<MT, FT>(xs[c & 1], jl, q, wA, acc);
     }
 
     // D[i][j] of a 16x16 tile sits in lane j + 16*(i/4), element i%4
@@ -290,15 +246,9 @@ int fast_gemm_splits(int M, int N, int K, int n_cu) {
     return S < 1 ? 1 : S;
 }
 
-#ifndef MG_GEMM_PF
-#define MG_GEMM_PF 1
-#endif
 template <int MT, int FT, int EPI>
 static void launch_epi(const FastGemmArgs& a, dim3 g, hipStream_t s) {
-    if (a.swiglu_x)
-        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, true, MG_GEMM_PF>), g, dim3(256), 0, s, a);
-    else
-        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, false, MG_GEMM_PF>), g, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI>), g, dim3(256), 0, s, a);
 }
 
 template <int MT, int FT>
@@ -321,6 +271,7 @@ static void launch_mt(const FastGemmArgs& a, int epi, int ft, hipStream_t s) {
 
 hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s) {
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
+    if (a.K < 8 || a.K % 8 || a.N % 16) return hipErrorInvalidValue;
     if (epi != FEPI_PART && a.S != 1) return hipErrorInvalidValue;  // only partial tiles may be split
     const int ft = fast_gemm_ft(a.M, a.N);
     switch (mt_for(a.M)) {

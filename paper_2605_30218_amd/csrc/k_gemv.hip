@@ -12,11 +12,11 @@
 // rows.  K is walked in chunks of 512 elements (one group per lane).  While the
 // fma work of chunk c runs, the weights of chunk c+1 are in flight (register
 // double buffer: one 16-byte group per feature and lane, 1 KiB coalesced per
-// feature) and the rows' activations of chunk c+1 are loaded into registers, then
-// staged into the fp32 LDS tile between two barriers (one buffer keeps the LDS
-// footprint at R * 2 KiB, so more blocks fit per CU; measured faster than double
-// buffering).  No split-K, no atomics: a row's arithmetic is the same whatever R,
-// J, the tile or the count.
+// feature, in a ping-pong register pair) and the rows' activations of chunk c+1 are
+// loaded into registers, then staged into the fp32 LDS tile between two barriers
+// (one buffer keeps the LDS footprint at R * 2 KiB, so more blocks fit per CU).  No
+// split-K, no atomics: a row's arithmetic is the same whatever R, J, the tile or the
+// count.
 // Block order: the row tiles of one feature block get consecutive slots on the
 // same XCD (blocks are dealt to the 8 XCDs round-robin), so they share its L2
 // copy of the weights.
@@ -27,9 +27,6 @@ namespace mg {
 
 constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
 
-#ifndef MG_GEMV_LDS_BUFS
-#define MG_GEMV_LDS_BUFS 1
-#endif
 #ifndef MG_GEMV_J_WIDE
 #define MG_GEMV_J_WIDE 2
 #endif
@@ -42,15 +39,16 @@ struct GemvShape {
     static constexpr int XLD = R * 64 / 256;  // staging loads (16 bytes) per thread per chunk
 };
 
+// activations of chunk kc for rows r0 .. r0+R-1: rows past nr read row nr-1 and k past
+// K reads the last group (those values are never used: rows past nr are skipped and
+// lanes past the last group do no arithmetic), so every load is unconditional
 template <int R>
 __device__ __forceinline__ void gemv_load_x(const GemvArgs& a, int r0, int nr, int kc, uint4 (&xr)[GemvShape<R>::XLD]) {
 #pragma unroll
     for (int it = 0; it < GemvShape<R>::XLD; ++it) {
         const int t = threadIdx.x + 256 * it;
-        const int rr = t >> 6, gl = t & 63;
-        const int k = kc + gl * 8;
-        xr[it] = (rr < nr && k < a.K) ? *reinterpret_cast<const uint4*>(a.X + (size_t)(r0 + rr) * a.K + k)
-                                      : make_uint4(0, 0, 0, 0);
+        const int rr = min(t >> 6, nr - 1), k = min(kc + (t & 63) * 8, a.K - 8);
+        xr[it] = *reinterpret_cast<const uint4*>(a.X + (size_t)(r0 + rr) * a.K + k);
     }
 }
 
@@ -66,12 +64,46 @@ __device__ __forceinline__ void gemv_store_x(float4 (*xs)[2][64], const uint4 (&
     }
 }
 
+// weights of group g (clamped to the last group) of the J feature rows
 template <int J>
-__device__ __forceinline__ void gemv_load_w(const uint16_t* const (&wrow)[J], const bool (&valid)[J], int g, int G,
-                                            uint4 (&w)[J]) {
+__device__ __forceinline__ void gemv_load_w(const uint16_t* const (&wrow)[J], int g, int G, uint4 (&w)[J]) {
+    const int gc = min(g, G - 1);
 #pragma unroll
-    for (int jj = 0; jj < J; ++jj)
-        w[jj] = (valid[jj] && g < G) ? *reinterpret_cast<const uint4*>(wrow[jj] + (size_t)g * 8) : make_uint4(0, 0, 0, 0);
+    for (int jj = 0; jj < J; ++jj) w[jj] = *reinterpret_cast<const uint4*>(wrow[jj] + (size_t)gc * 8);
+}
+
+// this lane's group of one chunk for every live row: sequential fma in element order
+template <int J, int R>
+__device__ __forceinline__ void gemv_fma_chunk(const float4 (*xb)[2][64], int lane, int nr, const uint4 (&wv)[J],
+                                               float (&acc)[J][R]) {
+    float w[J][8];
+#pragma unroll
+    for (int jj = 0; jj < J; ++jj) {
+        const uint4 v = wv[jj];
+        w[jj][0] = bf_lo(v.x); w[jj][1] = bf_hi(v.x); w[jj][2] = bf_lo(v.y); w[jj][3] = bf_hi(v.y);
+        w[jj][4] = bf_lo(v.z); w[jj][5] = bf_hi(v.z); w[jj][6] = bf_lo(v.w); w[jj][7] = bf_hi(v.w);
+    }
+    // rows past nr are skipped by a uniform branch; the loop stays fully unrolled so
+    // every accumulator index is a compile-time constant (no scratch)
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr) {
+        if (rr < nr) {
+            const float4 x0 = xb[rr][0][lane], x1 = xb[rr][1][lane];
+#pragma unroll
+            for (int jj = 0; jj < J; ++jj) {
+                float s = acc[jj][rr];
+                s = __builtin_fmaf(x0.x, w[jj][0], s);
+                s = __builtin_fmaf(x0.y, w[jj][1], s);
+                s = __builtin_fmaf(x0.z, w[jj][2], s);
+                s = __builtin_fmaf(x0.w, w[jj][3], s);
+                s = __builtin_fmaf(x1.x, w[jj][4], s);
+                s = __builtin_fmaf(x1.y, w[jj][5], s);
+                s = __builtin_fmaf(x1.z, w[jj][6], s);
+                s = __builtin_fmaf(x1.w, w[jj][7], s);
+                acc[jj][rr] = s;
+            }
+        }
+    }
 }
 
 template <int J, int R, int EPI>
@@ -90,10 +122,8 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, i
     const int jw = (fb * 4 + wave) * J;
     const int K = a.K, G = K >> 3;
 
-    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[buf][rr][half][lane].c;
-    // one buffer (two barriers per chunk) or two (one barrier per chunk)
-    constexpr int NB = MG_GEMV_LDS_BUFS;
-    __shared__ float4 xs[NB][R][2][64];
+    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[rr][half][lane].c
+    __shared__ float4 xs[R][2][64];
 
     const uint16_t* wrow[J];
     bool valid[J];
@@ -113,60 +143,35 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, i
         for (int rr = 0; rr < R; ++rr) acc[jj][rr] = 0.0f;
 
     const int nch = (K + KCH - 1) / KCH;
-    uint4 wcur[J], wnext[J];
+    uint4 wA[J], wB[J];
     uint4 xr[GemvShape<R>::XLD];
-    gemv_load_w<J>(wrow, valid, lane, G, wcur);
     gemv_load_x<R>(a, r0, nr, 0, xr);
-    gemv_store_x<R>(xs[0], xr);
+    gemv_load_w<J>(wrow, lane, G, wA);
+    gemv_store_x<R>(xs, xr);
     __syncthreads();
-    for (int c = 0; c < nch; ++c) {
-        const bool more = c + 1 < nch;
-        if (more) {
-            gemv_load_w<J>(wrow, valid, (c + 1) * 64 + lane, G, wnext);
-            gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, xr);
-        }
-        if (c * 64 + lane < G) {
-            float w[J][8];
-#pragma unroll
-            for (int jj = 0; jj < J; ++jj) {
-                const uint4 v = wcur[jj];
-                w[jj][0] = bf_lo(v.x); w[jj][1] = bf_hi(v.x); w[jj][2] = bf_lo(v.y); w[jj][3] = bf_hi(v.y);
-                w[jj][4] = bf_lo(v.z); w[jj][5] = bf_hi(v.z); w[jj][6] = bf_lo(v.w); w[jj][7] = bf_hi(v.w);
-            }
-            float4(*xb)[2][64] = xs[NB == 1 ? 0 : (c & 1)];
-            // rows past nr are skipped by a uniform branch; the loop stays fully unrolled
-            // so every accumulator index is a compile-time constant (no scratch)
-#pragma unroll
-            for (int rr = 0; rr < R; ++rr) {
-                if (rr < nr) {
-                    const float4 x0 = xb[rr][0][lane], x1 = xb[rr][1][lane];
-#pragma unroll
-                    for (int jj = 0; jj < J; ++jj) {
-                        float s = acc[jj][rr];
-                        s = __builtin_fmaf(x0.x, w[jj][0], s);
-                        s = __builtin_fmaf(x0.y, w[jj][1], s);
-                        s = __builtin_fmaf(x0.z, w[jj][2], s);
-                        s = __builtin_fmaf(x0.w, w[jj][3], s);
-                        s = __builtin_fmaf(x1.x, w[jj][4], s);
-                        s = __builtin_fmaf(x1.y, w[jj][5], s);
-                        s = __builtin_fmaf(x1.z, w[jj][6], s);
-                        s = __builtin_fmaf(x1.w, w[jj][7], s);
-                        acc[jj][rr] = s;
-                    }
-                }
-            }
-        }
-        if (NB == 1) {
-            __syncthreads();
-            if (more) gemv_store_x<R>(xs[0], xr);
-        } else if (more) {
-            gemv_store_x<R>(xs[(c + 1) & 1], xr);
-        }
+    // one chunk with a successor: request chunk c+1 (activations first, then weights
+    // into `nxt`), run chunk c, then restage the LDS tile between two barriers.  Loads
+    // complete in order, so the restaging waits for the activations only and the
+    // weights of chunk c+1 stay in flight.
+    auto step = [&](int c, const uint4 (&cur)[J], uint4 (&nxt)[J]) {
+        gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, xr);
+        gemv_load_w<J>(wrow, (c + 1) * 64 + lane, G, nxt);
+        __builtin_amdgcn_sched_barrier(0);
+        if (c * 64 + lane < G) gemv_fma_chunk<J, R>(xs, lane, nr, cur, acc);
         __syncthreads();
-        if (more) {
-#pragma unroll
-            for (int jj = 0; jj < J; ++jj) wcur[jj] = wnext[jj];
-        }
+        gemv_store_x<R>(xs, xr);
+        __syncthreads();
+    };
+    int c = 0;
+    for (; c + 2 < nch; c += 2) {
+        step(c, wA, wB);
+        step(c + 1, wB, wA);
+    }
+    if (c + 1 < nch) {
+        step(c, wA, wB);
+        if ((c + 1) * 64 + lane < G) gemv_fma_chunk<J, R>(xs, lane, nr, wB, acc);
+    } else if (c * 64 + lane < G) {
+        gemv_fma_chunk<J, R>(xs, lane, nr, wA, acc);
     }
 
     // all J*R butterflies at once; value jj*R + rr ends in the lanes multi_index names

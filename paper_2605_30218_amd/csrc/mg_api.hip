@@ -159,14 +159,13 @@ struct ProfScope {
 
 // One fast projection.  FEPI_PART writes S split partial tiles (returned in *S_out)
 // for the consuming kernel to sum; the other epilogues run unsplit.
-mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, int swiglu, const uint16_t* const* W,
+mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, const uint16_t* const* W,
                     const uint16_t* const* bias, const int* Nseg, int nseg, void* Y, int epi, hipStream_t s,
                     int* S_out = nullptr) {
     FastGemmArgs a{};
     a.X = X;
     a.M = M;
     a.K = K;
-    a.swiglu_x = swiglu;
     int N = 0;
     for (int k = 0; k < 3; ++k) {
         a.W[k] = k < nseg ? W[k] : nullptr;
@@ -180,7 +179,7 @@ mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, int swiglu, cons
     a.S = epi == FEPI_PART ? fast_gemm_splits(M, N, K, c->n_cu) : 1;
     if (S_out) *S_out = a.S;
     const double out_bytes = epi == FEPI_PART ? 4.0 * a.S * M * N : (double)M * N * (epi == FEPI_F32 ? 4 : 2);
-    const double bytes = 2.0 * N * K + 2.0 * M * K * (swiglu ? 2 : 1) + out_bytes;
+    const double bytes = 2.0 * N * K + 2.0 * M * K + out_bytes;
     ProfScope ps(c, MG_KIND_FAST_GEMM, s, bytes, 2.0 * M * N * K);
     HIPCHK(launch_fast_gemm(a, epi, s));
     return MG_OK;
@@ -406,7 +405,7 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
         {
             const uint16_t* W[3] = {c->LW(l, 1), c->LW(l, 2), c->LW(l, 3)};
             const int Ns[3] = {Nq, Nk, Nk};
-            MGCHK(fast_gemm(c, h, B, d, 0, W, nullptr, Ns, 3, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 3, nullptr, FEPI_PART, s, &S));
         }
         {
             const uint16_t* Bs[3] = {c->LW(l, 4), c->LW(l, 5), c->LW(l, 6)};
@@ -431,26 +430,26 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
         {
             const uint16_t* W[1] = {c->LW(l, 7)};
             const int Ns[1] = {d};
-            MGCHK(fast_gemm(c, att, B, Nq, 0, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, att, B, Nq, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
         }
         HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, c->LW(l, 8), g.rms_eps, x, h, s));
         {
             const uint16_t* W[2] = {c->LW(l, 9), c->LW(l, 10)};
             const int Ns[2] = {F, F};
-            MGCHK(fast_gemm(c, h, B, d, 0, W, nullptr, Ns, 2, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 2, nullptr, FEPI_PART, s, &S));
         }
         HIPCHK(launch_swiglu_part(B, part, S, F, act, s));
         {
             const uint16_t* W[1] = {c->LW(l, 11)};
             const int Ns[1] = {d};
-            MGCHK(fast_gemm(c, act, B, F, 0, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, act, B, F, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
         }
         const uint16_t* next_gamma = l + 1 < g.n_layers ? c->LW(l + 1, 0) : c->W(1 + WPL * g.n_layers);
         HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, next_gamma, g.rms_eps, x, h, s));
     }
     const uint16_t* W[1] = {c->W(2 + WPL * g.n_layers)};
     const int Ns[1] = {g.vocab};
-    MGCHK(fast_gemm(c, h, B, d, 0, W, nullptr, Ns, 1, logits, FEPI_F32, s));
+    MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 1, logits, FEPI_F32, s));
     return MG_OK;
 }
 

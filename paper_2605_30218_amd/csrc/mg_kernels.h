@@ -55,9 +55,8 @@ hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
 // ---------------------------------------------------------------- fast MFMA GEMM
 enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2 };
 struct FastGemmArgs {
-    const uint16_t* X;         // [M][K] bf16; with swiglu_x: [M][2K] = [gate | up]
+    const uint16_t* X;         // [M][K] bf16
     int M, K;
-    int swiglu_x;              // 1: X row = silu(gate) * up, computed on load
     const uint16_t* W[3];
     const uint16_t* bias[3];   // FEPI_BF16 only
     int Nseg[3];
