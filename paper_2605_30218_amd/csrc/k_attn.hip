@@ -227,14 +227,38 @@ __global__ void attn_combine_kernel(AttnArgs a) {
     const int S = (p + 1 + a.chunk - 1) / a.chunk;
     const int stride = hd + 2;
     const float* base = a.part + ((size_t)i * a.m.Hq + h) * a.max_chunks * stride;
-    float M = base[0];
-    for (int c = 1; c < S; ++c) M = fmaxf(M, base[(size_t)c * stride]);
-    float L = 0.0f, O = 0.0f;
-    for (int c = 0; c < S; ++c) {
-        const float mc = base[(size_t)c * stride];
-        const float w = canon_exp(mc - M);
-        L = __builtin_fmaf(w, base[(size_t)c * stride + 1], L);
-        O = __builtin_fmaf(w, base[(size_t)c * stride + 2 + d], O);
+    // the chunk partials are read in batches of CB (all loads of a batch in flight together)
+    constexpr int CB = 8;
+    float M = -__builtin_inff(), L = 0.0f, O = 0.0f;
+    if (S <= CB) {
+        float mc[CB], lc[CB], ac[CB];
+#pragma unroll
+        for (int c = 0; c < CB; ++c) {
+            const int cc = min(c, S - 1);
+            mc[c] = base[(size_t)cc * stride];
+            lc[c] = base[(size_t)cc * stride + 1];
+            ac[c] = base[(size_t)cc * stride + 2 + d];
+        }
+        M = mc[0];
+#pragma unroll
+        for (int c = 1; c < CB; ++c)
+            if (c < S) M = fmaxf(M, mc[c]);
+#pragma unroll
+        for (int c = 0; c < CB; ++c) {
+            if (c < S) {
+                const float w = canon_exp(mc[c] - M);
+                L = __builtin_fmaf(w, lc[c], L);
+                O = __builtin_fmaf(w, ac[c], O);
+            }
+        }
+    } else {
+        M = base[0];
+        for (int c = 1; c < S; ++c) M = fmaxf(M, base[(size_t)c * stride]);
+        for (int c = 0; c < S; ++c) {
+            const float w = canon_exp(base[(size_t)c * stride] - M);
+            L = __builtin_fmaf(w, base[(size_t)c * stride + 1], L);
+            O = __builtin_fmaf(w, base[(size_t)c * stride + 2 + d], O);
+        }
     }
     a.out[(size_t)i * a.m.Hq * hd + (size_t)h * hd + d] = (uint16_t)f2bf(ieee_div(O, L));
 }

@@ -47,6 +47,14 @@ __global__ __launch_bounds__(RN_THREADS) void resid_norm_kernel(int M, const flo
     const int d4 = d / 4;
     uint2* xr = reinterpret_cast<uint2*>(x + (size_t)r * d);
     const uint2* src = embed ? reinterpret_cast<const uint2*>(embed + (size_t)tokens[r] * d) : xr;
+    // gamma is requested first, so the block waits for memory once
+    const uint2* g2 = reinterpret_cast<const uint2*>(gamma);
+    uint2 gv[RN_MAXQ];
+#pragma unroll
+    for (int k = 0; k < RN_MAXQ; ++k) {
+        const int q = threadIdx.x + RN_THREADS * k;
+        gv[k] = q < d4 ? g2[q] : make_uint2(0, 0);
+    }
     float4 xv[RN_MAXQ];
     float ss = 0.0f;
 #pragma unroll
@@ -74,13 +82,12 @@ __global__ __launch_bounds__(RN_THREADS) void resid_norm_kernel(int M, const flo
 #pragma unroll
     for (int w = 0; w < RN_THREADS / 64; ++w) tot += red[w];
     const float rs = ieee_div(1.0f, ieee_sqrt(ieee_div(tot, (float)d) + eps));
-    const uint2* g2 = reinterpret_cast<const uint2*>(gamma);
     uint2* hr = reinterpret_cast<uint2*>(h + (size_t)r * d);
 #pragma unroll
     for (int k = 0; k < RN_MAXQ; ++k) {
         const int q = threadIdx.x + RN_THREADS * k;
         if (q >= d4) break;
-        const uint2 g = g2[q];
+        const uint2 g = gv[k];
         const float4 o = xv[k];
         hr[q] = make_uint2(pack_bf2((o.x * rs) * bf_lo(g.x), (o.y * rs) * bf_hi(g.x)),
                            pack_bf2((o.z * rs) * bf_lo(g.y), (o.w * rs) * bf_hi(g.y)));

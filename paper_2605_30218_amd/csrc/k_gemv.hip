@@ -27,11 +27,11 @@ namespace mg {
 
 constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
 
-#ifndef MG_GEMV_J_WIDE
-#define MG_GEMV_J_WIDE 2
+#ifndef MG_GEMV_J_R8
+#define MG_GEMV_J_R8 2
 #endif
-#ifndef MG_GEMV_J_NARROW
-#define MG_GEMV_J_NARROW 2
+#ifndef MG_GEMV_J_R16
+#define MG_GEMV_J_R16 2
 #endif
 
 template <int R>
@@ -220,10 +220,8 @@ static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s)
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
-    const bool wide = a.N >= 8192;
-    constexpr int JW = MG_GEMV_J_WIDE, JN = MG_GEMV_J_NARROW;
-    if (rows > 8) return wide ? launch_jr<JW, 16>(a, epi, rows, s) : launch_jr<JN, 16>(a, epi, rows, s);
-    return wide ? launch_jr<JW, 8>(a, epi, rows, s) : launch_jr<JN, 8>(a, epi, rows, s);
+    if (rows > 8) return launch_jr<MG_GEMV_J_R16, 16>(a, epi, rows, s);
+    return launch_jr<MG_GEMV_J_R8, 8>(a, epi, rows, s);
 }
 
 }  // namespace mg

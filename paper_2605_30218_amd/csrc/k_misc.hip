@@ -37,11 +37,14 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
     const uint4* xr = reinterpret_cast<const uint4*>(x + (size_t)row * d);
     const int G = d >> 3;
     // the lane's groups lane, lane+64, ... are loaded together and kept in registers
-    uint4 xv[RMS_MAXG];
+    // gamma is requested with x, so the block waits for memory once
+    const uint4* gr = reinterpret_cast<const uint4*>(g);
+    uint4 xv[RMS_MAXG], gv[RMS_MAXG];
 #pragma unroll
     for (int k = 0; k < RMS_MAXG; ++k) {
         const int gi = lane + 64 * k;
         xv[k] = gi < G ? xr[gi] : make_uint4(0, 0, 0, 0);
+        gv[k] = gi < G ? gr[gi] : make_uint4(0, 0, 0, 0);
     }
     float a = 0.0f;
 #pragma unroll
@@ -57,18 +60,17 @@ __global__ __launch_bounds__(256) void rmsnorm_kernel(const uint16_t* __restrict
     const float ss = butterfly_sum(a);
     const float m = ieee_div(ss, (float)d);
     const float r = ieee_div(1.0f, ieee_sqrt(m + eps));
-    const uint4* gr = reinterpret_cast<const uint4*>(g);
     uint4* yr = reinterpret_cast<uint4*>(y + (size_t)row * d);
 #pragma unroll
     for (int k = 0; k < RMS_MAXG; ++k) {
         const int gi = lane + 64 * k;
         if (gi < G) {
-            const uint4 v = xv[k], gv = gr[gi];
+            const uint4 v = xv[k], w = gv[k];
             uint4 o;
-            o.x = pack_bf2((bf_lo(v.x) * r) * bf_lo(gv.x), (bf_hi(v.x) * r) * bf_hi(gv.x));
-            o.y = pack_bf2((bf_lo(v.y) * r) * bf_lo(gv.y), (bf_hi(v.y) * r) * bf_hi(gv.y));
-            o.z = pack_bf2((bf_lo(v.z) * r) * bf_lo(gv.z), (bf_hi(v.z) * r) * bf_hi(gv.z));
-            o.w = pack_bf2((bf_lo(v.w) * r) * bf_lo(gv.w), (bf_hi(v.w) * r) * bf_hi(gv.w));
+            o.x = pack_bf2((bf_lo(v.x) * r) * bf_lo(w.x), (bf_hi(v.x) * r) * bf_hi(w.x));
+            o.y = pack_bf2((bf_lo(v.y) * r) * bf_lo(w.y), (bf_hi(v.y) * r) * bf_hi(w.y));
+            o.z = pack_bf2((bf_lo(v.z) * r) * bf_lo(w.z), (bf_hi(v.z) * r) * bf_hi(w.z));
+            o.w = pack_bf2((bf_lo(v.w) * r) * bf_lo(w.w), (bf_hi(v.w) * r) * bf_hi(w.w));
             yr[gi] = o;
         }
     }
@@ -112,28 +114,61 @@ __global__ __launch_bounds__(256) void rope_kv_kernel(Items it, ModelDims m, int
         vdst = kdst + (size_t)Nk * m.page_size;
     }
     const int kv_head_stride = kv_col ? hd : hd * m.page_size;
-    const int nq_pairs = m.Hq * h2, nk_pairs = m.Hkv * h2;
-    for (int t = threadIdx.x; t < nq_pairs + nk_pairs; t += blockDim.x) {
-        const bool isq = t < nq_pairs;
-        const int tt = isq ? t : t - nq_pairs;
-        const int head = tt / h2, ii = tt % h2;
-        const uint16_t* s = isq ? src + head * hd : src + Nq + head * hd;
-        const float a = bf2f(s[ii]), b = bf2f(s[ii + h2]);
-        const float c = csp[2 * ii], sn = csp[2 * ii + 1];
-        const float ac = a * c, bs = b * sn, bc = b * c, as = a * sn;
-        const uint16_t o1 = (uint16_t)f2bf(ac - bs), o2 = (uint16_t)f2bf(bc + as);
-        if (isq) {
-            qrot[(size_t)i * Nq + head * hd + ii] = o1;
-            qrot[(size_t)i * Nq + head * hd + ii + h2] = o2;
-        } else {
-            kdst[(size_t)head * kv_head_stride + ii] = o1;
-            kdst[(size_t)head * kv_head_stride + ii + h2] = o2;
+    // task = 8 consecutive pairs (i, i + hd/2) of one q or k head, or 8 values of v;
+    // each thread's tasks are loaded together before any arithmetic
+    const int gph = h2 / 8;                       // pair groups per head
+    const int n_rot = (m.Hq + m.Hkv) * gph, n_v = Nk / 8;
+    constexpr int TPT = 4;                        // tasks per thread per round
+    for (int t0 = 0; t0 < n_rot + n_v; t0 += 256 * TPT) {
+        uint4 lo[TPT], hi[TPT];
+        float4 c4[TPT][4];
+#pragma unroll
+        for (int u = 0; u < TPT; ++u) {
+            const int t = t0 + threadIdx.x + 256 * u;
+            if (t < n_rot) {
+                const int head = t / gph, ii = (t % gph) * 8;
+                const uint16_t* sh = head < m.Hq ? src + head * hd : src + Nq + (head - m.Hq) * hd;
+                lo[u] = *reinterpret_cast<const uint4*>(sh + ii);
+                hi[u] = *reinterpret_cast<const uint4*>(sh + ii + h2);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) c4[u][q] = *reinterpret_cast<const float4*>(csp + 2 * ii + 4 * q);
+            } else if (t < n_rot + n_v) {
+                lo[u] = *reinterpret_cast<const uint4*>(src + Nq + Nk + (t - n_rot) * 8);
+            }
         }
-    }
-    const uint16_t* vs = src + Nq + Nk;
-    for (int t = threadIdx.x; t < Nk; t += blockDim.x) {
-        const int head = t / hd, dd = t % hd;
-        vdst[(size_t)head * kv_head_stride + dd] = vs[t];
+#pragma unroll
+        for (int u = 0; u < TPT; ++u) {
+            const int t = t0 + threadIdx.x + 256 * u;
+            if (t < n_rot) {
+                const int head = t / gph, ii = (t % gph) * 8;
+                const float a[8] = {bf_lo(lo[u].x), bf_hi(lo[u].x), bf_lo(lo[u].y), bf_hi(lo[u].y),
+                                    bf_lo(lo[u].z), bf_hi(lo[u].z), bf_lo(lo[u].w), bf_hi(lo[u].w)};
+                const float b[8] = {bf_lo(hi[u].x), bf_hi(hi[u].x), bf_lo(hi[u].y), bf_hi(hi[u].y),
+                                    bf_lo(hi[u].z), bf_hi(hi[u].z), bf_lo(hi[u].w), bf_hi(hi[u].w)};
+                const float cc[16] = {c4[u][0].x, c4[u][0].y, c4[u][0].z, c4[u][0].w, c4[u][1].x, c4[u][1].y,
+                                      c4[u][1].z, c4[u][1].w, c4[u][2].x, c4[u][2].y, c4[u][2].z, c4[u][2].w,
+                                      c4[u][3].x, c4[u][3].y, c4[u][3].z, c4[u][3].w};
+                uint32_t o1[8], o2[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float c = cc[2 * e], sn = cc[2 * e + 1];
+                    const float ac = a[e] * c, bs = b[e] * sn, bc = b[e] * c, as = a[e] * sn;
+                    o1[e] = f2bf(ac - bs);
+                    o2[e] = f2bf(bc + as);
+                }
+                const uint4 w1 = make_uint4(o1[0] | (o1[1] << 16), o1[2] | (o1[3] << 16), o1[4] | (o1[5] << 16),
+                                            o1[6] | (o1[7] << 16));
+                const uint4 w2 = make_uint4(o2[0] | (o2[1] << 16), o2[2] | (o2[3] << 16), o2[4] | (o2[5] << 16),
+                                            o2[6] | (o2[7] << 16));
+                uint16_t* dst = head < m.Hq ? qrot + (size_t)i * Nq + head * hd
+                                            : kdst + (size_t)(head - m.Hq) * kv_head_stride;
+                *reinterpret_cast<uint4*>(dst + ii) = w1;
+                *reinterpret_cast<uint4*>(dst + ii + h2) = w2;
+            } else if (t < n_rot + n_v) {
+                const int e = (t - n_rot) * 8, head = e / hd, dd = e % hd;
+                *reinterpret_cast<uint4*>(vdst + (size_t)head * kv_head_stride + dd) = lo[u];
+            }
+        }
     }
 }
 
