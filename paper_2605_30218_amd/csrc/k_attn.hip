@@ -1,16 +1,16 @@
-// k_attn.hip -- paged GQA decode attention, canonical (verifier, prefill) and fast.
+// k_attn.hip -- the verifier's (and the prefill's) paged GQA decode attention.
 //
-// Both serve the G query heads that share a KV head from one block or wave, so each
-// K/V page row is read from HBM once per item, and both split the context into
-// chunks whose partial (m, l, a) a combine kernel merges:
+// A block serves the G query heads that share a KV head, so each K/V page row is
+// read from HBM once per item; the context is split into chunks whose partial
+// (m, l, a) a combine kernel merges:
 //   score      s_j = (q . k_j) * fp32(1/sqrt(hd))
 //   chunk      m = max_j s_j, e_j = exp(s_j - m), l = sum_j e_j, a[d] = sum_j e_j v_jd
 //   combine    over chunks in ascending order: M = max m_c, w_c = exp(m_c - M),
 //              L = sum w_c l_c, O[d] = sum w_c a_c[d], out = bf16(O / L)
-// Canonical (the verifier): chunks of 256 positions, so the chunk count depends only
-// on the context length; every sum is sequential in a fixed order (d for the scores,
-// position for l and a, chunk for L and O), with fma where the definition has a
-// product; the verifier's EXP.  Fast: 128-position splits, MFMA scores, exp2.
+// Chunks of 256 positions, so the chunk count depends only on the context length;
+// every sum is sequential in a fixed order (d for the scores, position for l and a,
+// chunk for L and O), with fma where the definition has a product; the verifier's EXP.
+// (The fast path's attention is in k_attn_fast.hip.)
 // The current position p comes from the item's own column when one is given
 // (the verifier never reads the tentative column of the cache).
 #include "mg_device.h"
@@ -263,205 +263,16 @@ __global__ void attn_combine_kernel(AttnArgs a) {
     a.out[(size_t)i * a.m.Hq * hd + (size_t)h * hd + d] = (uint16_t)f2bf(ieee_div(O, L));
 }
 
-// ---------------------------------------------------------------------------------
-// Fast decode attention: one wave per (item, KV head, split of FAST_SPLIT positions).
-// Scores on MFMA: S[h][pos] = Q[h][:] . K[pos][:] with the G query heads as the rows
-// of a 16-row A operand (rows >= G are zero) and 16 positions of a page as the B
-// operand loaded straight from the page (lane (j, q) reads 16 bytes of position j).
-// Softmax online in the exp2 domain, P in fp32; O += P V on the vector ALU with the
-// wave split as 16 d-groups x 4 positions per 16-byte load (64/DG positions when
-// hd = 64), reduced over the position groups at the end.  Partial (m, l, O) per split
-// go to the combine kernel.
-typedef __bf16 bf16x8_at __attribute__((ext_vector_type(8)));
-typedef float f32x4_at __attribute__((ext_vector_type(4)));
-constexpr int FAST_SPLIT = 128;
-
-template <int HD>
-__global__ __launch_bounds__(64) void attn_fast_kernel(AttnArgs a) {
-    constexpr int DG = HD / 8;        // 16-byte d-groups per row
-    constexpr int PPI = 64 / DG;      // positions per V load instruction
-    constexpr int KST = HD / 32;      // MFMA k-steps over d
-    const int i = blockIdx.z;
-    if (i >= items_n(a.it)) return;
-    const int kh = blockIdx.y, sp = blockIdx.x;
-    const int r = items_row(a.it, i), p = items_pos(a.it, i);
-    const int s0 = sp * FAST_SPLIT;
-    if (s0 > p) return;
-    const int s1 = min(s0 + FAST_SPLIT, p + 1);
-    const ModelDims& m = a.m;
-    const int G = m.Hq / m.Hkv;
-    const int lane = threadIdx.x;
-    const int jl = lane & 15, qg = lane >> 4;
-    const int dg = lane % DG, po = lane / DG;
-    const float sl2 = attn_scale(HD) * 1.4426950408889634f;  // scores in log2 units
-    const int32_t* ptab = a.it.page_table + (size_t)r * m.max_pages_per_row;
-    const size_t page_stride_kv = (size_t)m.Hkv * m.page_size * HD;  // K -> V of the same page
-    auto page_k = [&](int pos) -> const uint16_t* {
-        const int page = ptab[pos / m.page_size];
-        return a.kv_pool + ((((size_t)a.layer * m.n_pages + page) * 2) * m.Hkv + kh) * (size_t)m.page_size * HD;
-    };
-
-    // Q as the A operand: lane (h = jl, qg) holds Q[h][32 st + 8 qg .. +7]
-    uint4 qa[KST];
-    {
-        const uint16_t* qrow = a.qrot + (size_t)i * m.Hq * HD + (size_t)(kh * G + jl) * HD;
-#pragma unroll
-        for (int st = 0; st < KST; ++st)
-            qa[st] = jl < G ? *reinterpret_cast<const uint4*>(qrow + st * 32 + qg * 8) : make_uint4(0, 0, 0, 0);
-    }
-    float mrow[4], lrow[4];     // per head h = 4 qg + v (lanes of group qg)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) { mrow[v] = -__builtin_inff(); lrow[v] = 0.0f; }
-    float o[ATT_MAXG][8];
-#pragma unroll
-    for (int h = 0; h < ATT_MAXG; ++h)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) o[h][e] = 0.0f;
-
-    for (int base = s0; base < s1; base += 32) {
-        const bool two = base + 16 < s1;        // second page of this step holds a valid position
-        const uint16_t* kp0 = page_k(base);
-        const uint16_t* kp1 = two ? page_k(base + 16) : kp0;
-        // scores of the two pages
-        f32x4_at sc[2];
-#pragma unroll
-        for (int pg = 0; pg < 2; ++pg) {
-            sc[pg] = f32x4_at{0.f, 0.f, 0.f, 0.f};
-            const uint16_t* kp = pg ? kp1 : kp0;
-#pragma unroll
-            for (int st = 0; st < KST; ++st) {
-                const uint4 kb = *reinterpret_cast<const uint4*>(kp + jl * HD + st * 32 + qg * 8);
-                sc[pg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_at, qa[st]),
-                                                                 __builtin_bit_cast(bf16x8_at, kb), sc[pg], 0, 0, 0);
-            }
-        }
-        // V rows of this step: lane (dg, po) loads position 4t + po (t < 32/PPI)
-        uint4 vv[32 / PPI];
-#pragma unroll
-        for (int t = 0; t < 32 / PPI; ++t) {
-            const int pl = PPI * t + po;          // 0..31 within the step
-            const int pos = base + pl;
-            const uint16_t* vp = (pl < 16 ? kp0 : kp1) + page_stride_kv;
-            vv[t] = (pos < s1) ? *reinterpret_cast<const uint4*>(vp + (pl & 15) * HD + dg * 8) : make_uint4(0, 0, 0, 0);
-        }
-        // online softmax per head row (4 qg + v): lanes jl hold positions
-        float pmax[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            float x0 = (base + jl < s1) ? sc[0][v] * sl2 : -__builtin_inff();
-            float x1 = (base + 16 + jl < s1) ? sc[1][v] * sl2 : -__builtin_inff();
-            sc[0][v] = x0;
-            sc[1][v] = x1;
-            float mx = fmaxf(x0, x1);
-#pragma unroll
-            for (int o2 = 1; o2 < 16; o2 <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o2, 64));
-            pmax[v] = mx;
-        }
-        float alpha[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const float mn = fmaxf(mrow[v], pmax[v]);
-            alpha[v] = exp2f(mrow[v] - mn);
-            mrow[v] = mn;
-            const float p0 = exp2f(sc[0][v] - mn), p1 = exp2f(sc[1][v] - mn);
-            sc[0][v] = p0;
-            sc[1][v] = p1;
-            lrow[v] = lrow[v] * alpha[v] + (p0 + p1);
-        }
-        // rescale O and accumulate P V; head h's P of position pl sits in lane (pl % 16) + 16 (h / 4)
-#pragma unroll
-        for (int h = 0; h < ATT_MAXG; ++h) {
-            if (h >= G) break;
-            const float al = __shfl(alpha[h & 3], 16 * (h >> 2), 64);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) o[h][e] *= al;
-        }
-#pragma unroll
-        for (int t = 0; t < 32 / PPI; ++t) {
-            const int pl = PPI * t + po;
-            const float v8[8] = {bf_lo(vv[t].x), bf_hi(vv[t].x), bf_lo(vv[t].y), bf_hi(vv[t].y),
-                                 bf_lo(vv[t].z), bf_hi(vv[t].z), bf_lo(vv[t].w), bf_hi(vv[t].w)};
-#pragma unroll
-            for (int h = 0; h < ATT_MAXG; ++h) {
-                if (h >= G) break;
-                const float src = (PPI * t < 16) ? sc[0][h & 3] : sc[1][h & 3];
-                const float ph = __shfl(src, (pl & 15) + 16 * (h >> 2), 64);
-#pragma unroll
-                for (int e = 0; e < 8; ++e) o[h][e] = __builtin_fmaf(ph, v8[e], o[h][e]);
-            }
-        }
-    }
-    // reduce O over the position groups po and l over the 16 position lanes
-#pragma unroll
-    for (int h = 0; h < ATT_MAXG; ++h) {
-        if (h >= G) break;
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-            for (int off = DG; off < 64; off <<= 1) o[h][e] += __shfl_xor(o[h][e], off, 64);
-    }
-#pragma unroll
-    for (int v = 0; v < 4; ++v)
-        for (int off = 1; off < 16; off <<= 1) lrow[v] += __shfl_xor(lrow[v], off, 64);
-    const int stride = HD + 2;
-#pragma unroll
-    for (int h = 0; h < ATT_MAXG; ++h) {
-        if (h >= G) break;
-        float* dst = a.part + (((size_t)i * m.Hq + kh * G + h) * a.max_chunks + sp) * stride;
-        const float mh = __shfl(mrow[h & 3], 16 * (h >> 2), 64);
-        const float lh = __shfl(lrow[h & 3], 16 * (h >> 2), 64);
-        if (lane == 0) {
-            dst[0] = mh;
-            dst[1] = lh;
-        }
-        if (po == 0) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) dst[2 + dg * 8 + e] = o[h][e];
-        }
-    }
-}
-
-// combine of the fast splits: m in log2 units
-__global__ void attn_fast_combine_kernel(AttnArgs a) {
-    const int i = blockIdx.y;
-    if (i >= items_n(a.it)) return;
-    const int h = blockIdx.x, d = threadIdx.x;
-    const int hd = a.m.hd;
-    if (d >= hd) return;
-    const int p = items_pos(a.it, i);
-    const int S = (p + 1 + FAST_SPLIT - 1) / FAST_SPLIT;
-    const int stride = hd + 2;
-    const float* base = a.part + ((size_t)i * a.m.Hq + h) * a.max_chunks * stride;
-    float M = base[0];
-    for (int c = 1; c < S; ++c) M = fmaxf(M, base[(size_t)c * stride]);
-    float L = 0.0f, O = 0.0f;
-    for (int c = 0; c < S; ++c) {
-        const float w = exp2f(base[(size_t)c * stride] - M);
-        L += w * base[(size_t)c * stride + 1];
-        O += w * base[(size_t)c * stride + 2 + d];
-    }
-    a.out[(size_t)i * a.m.Hq * hd + (size_t)h * hd + d] = (uint16_t)f2bf(O / L);
-}
-
-int fast_attention_split() { return FAST_SPLIT; }
-
 hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s) {
     const int n = a.it.n_host;
     if (n <= 0) return hipSuccess;
+    if (!canon || a.chunk != ATT_MAXC) return hipErrorInvalidValue;  // the fast path has its own kernel
     dim3 g1(a.max_chunks, a.m.Hkv, n), g2(a.m.Hq, n);
-    if (canon) {
-        if (a.chunk != ATT_MAXC) return hipErrorInvalidValue;
-        if (a.m.hd == 128)
-            hipLaunchKernelGGL(attn_canon_kernel<128>, g1, dim3(256), 0, s, a);
-        else
-            hipLaunchKernelGGL(attn_canon_kernel<64>, g1, dim3(256), 0, s, a);
-        hipLaunchKernelGGL(attn_combine_kernel, g2, dim3(a.m.hd), 0, s, a);
-    } else {
-        if (a.m.hd == 128)
-            hipLaunchKernelGGL(attn_fast_kernel<128>, g1, dim3(64), 0, s, a);
-        else
-            hipLaunchKernelGGL(attn_fast_kernel<64>, g1, dim3(64), 0, s, a);
-        hipLaunchKernelGGL(attn_fast_combine_kernel, g2, dim3(a.m.hd), 0, s, a);
-    }
+    if (a.m.hd == 128)
+        hipLaunchKernelGGL(attn_canon_kernel<128>, g1, dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(attn_canon_kernel<64>, g1, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_combine_kernel, g2, dim3(a.m.hd), 0, s, a);
     return hipGetLastError();
 }
 

@@ -1,0 +1,305 @@
+// k_attn_fast.hip -- the fast path's decode attention, fused with the split-K sum of
+// the QKV projection, the bias, RoPE and the tentative K/V append.
+//
+// One block of 4 waves per (row, KV head).
+// Prologue: sums the QKV split partials of the block's features (the G query heads of
+// the group, then k, then v) in split order, adds the bias and rounds to bf16 (the
+// projection's rounding point); rotates q and k (rotate-half RoPE from the fp32
+// cos/sin table, products and sums rounded separately, then bf16); appends K' and V
+// to the paged cache at the row's position p (the tentative column); keeps q' (bf16,
+// the MFMA A operand) and k'_p, v_p in LDS, and copies the row's page indices for
+// positions < p into LDS.
+// Main loop: wave w takes the pages w, w + 4, ... of positions 0..p-1 (16 positions
+// per step).  Scores on MFMA: S[h][pos] = Q[h][:] . K[pos][:] with the
+// query heads as the rows of a 16-row A operand (rows >= G are zero) and 16
+// positions of a page as the B operand read straight from the page (lane (j, q) reads
+// 16 bytes of position j).  Softmax online in the exp2 domain; O += P V on the vector
+// ALU with the wave split as hd/8 d-groups x 512/hd positions per 16-byte load.  The
+// K and V of the wave's next step are requested before the current step's
+// arithmetic (register ping-pong); values of positions >= p are zeroed when used.
+// Epilogue: each wave's (m, l, O) goes to LDS; position p contributes its own partial
+// (m = score of q' . k'_p, l = 1, O = v_p); the five partials are merged and
+// out = bf16(O / L).
+// The summation order depends on the context length and the split of positions over
+// waves: this path is not the verifier's order.
+#include "mg_device.h"
+#include "mg_kernels.h"
+
+namespace mg {
+
+typedef __bf16 bf16x8_ft __attribute__((ext_vector_type(8)));
+typedef float f32x4_ft __attribute__((ext_vector_type(4)));
+
+constexpr int FA_WAVES = 4;
+constexpr int FA_PGCAP = 1024;  // page indices held in LDS (positions < 16384); more are read from memory
+
+__device__ __forceinline__ float fa_scale(int hd) { return hd == 128 ? 0x1.6a09e6p-4f : 0x1.0p-3f; }
+
+template <int HD, int GP>
+__global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
+    constexpr int DG = HD / 8;    // 16-byte d-groups per row
+    constexpr int PPI = 64 / DG;  // positions per V load instruction
+    constexpr int VL = 16 / PPI;  // V loads per lane per page step
+    constexpr int KST = HD / 32;  // MFMA k-steps over d
+    constexpr int H2 = HD / 2;
+    const ModelDims& m = a.m;
+    const int kh = blockIdx.x, r = blockIdx.y;
+    const int G = m.Hq / m.Hkv, Nq = m.Hq * HD, Nk = m.Hkv * HD, N = Nq + 2 * Nk;
+    const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
+    const int jl = lane & 15, qg = lane >> 4;
+    const int dg = lane % DG, po = lane / DG;
+    const float sl2 = fa_scale(HD) * 1.4426950408889634f;  // scores in log2 units
+
+    __shared__ float y[(GP + 2) * HD];
+    __shared__ __attribute__((aligned(16))) uint16_t qb[GP * HD];
+    __shared__ float kps[HD], vps[HD];
+    __shared__ int pgs[FA_PGCAP];
+    __shared__ float sp[GP];
+    __shared__ float wm[FA_WAVES][GP], wl[FA_WAVES][GP];
+    __shared__ float wo[FA_WAVES][GP * HD];
+
+    const int p = a.positions[r];
+    const int32_t* ptab = a.page_table + (size_t)r * m.max_pages_per_row;
+    const int npg = (p + 15) / 16;  // pages holding positions 0..p-1
+    const bool pg_lds = npg <= FA_PGCAP;
+
+    // ---- prologue: split sum + bias + bf16 of this block's q, k, v features
+    {
+        const float* pp = a.part + (size_t)r * N;
+        const size_t sstride = (size_t)a.B * N;
+        const int nf = (G + 2) * HD;
+        for (int q4 = t; q4 < nf / 4; q4 += 256) {
+            const int f = 4 * q4;
+            int n, nb;
+            const uint16_t* b;
+            if (f < G * HD) { n = kh * G * HD + f; b = a.bq; nb = n; }
+            else if (f < (G + 1) * HD) { nb = kh * HD + f - G * HD; n = Nq + nb; b = a.bk; }
+            else { nb = kh * HD + f - (G + 1) * HD; n = Nq + Nk + nb; b = a.bv; }
+            // splits summed in split order; loads issued in batches of 8
+            float4 v = *reinterpret_cast<const float4*>(pp + n);
+            int sp2 = 1;
+            for (; sp2 + 8 <= a.S; sp2 += 8) {
+                float4 u[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) u[k] = *reinterpret_cast<const float4*>(pp + (size_t)(sp2 + k) * sstride + n);
+#pragma unroll
+                for (int k = 0; k < 8; ++k) { v.x += u[k].x; v.y += u[k].y; v.z += u[k].z; v.w += u[k].w; }
+            }
+            for (; sp2 < a.S; ++sp2) {
+                const float4 u = *reinterpret_cast<const float4*>(pp + (size_t)sp2 * sstride + n);
+                v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+            }
+            if (b) { v.x += bf2f(b[nb]); v.y += bf2f(b[nb + 1]); v.z += bf2f(b[nb + 2]); v.w += bf2f(b[nb + 3]); }
+            y[f] = bf2f(f2bf(v.x));
+            y[f + 1] = bf2f(f2bf(v.y));
+            y[f + 2] = bf2f(f2bf(v.z));
+            y[f + 3] = bf2f(f2bf(v.w));
+        }
+        if (pg_lds)
+            for (int j = t; j < npg; j += 256) pgs[j] = ptab[j];
+        for (int e = G * HD + t; e < GP * HD; e += 256) qb[e] = 0;
+    }
+    __syncthreads();
+    // ---- RoPE on q and k, tentative K/V append at p, q' / k'_p / v_p into LDS
+    {
+        const float* csp = a.cs + (size_t)p * HD;  // [pos][i][cos, sin]
+        uint16_t* kdst = a.kv_pool + ((((size_t)a.layer * m.n_pages + ptab[p / 16]) * 2) * m.Hkv + kh) * (size_t)16 * HD +
+                         (size_t)(p % 16) * HD;
+        uint16_t* vdst = kdst + (size_t)m.Hkv * 16 * HD;
+        for (int t2 = t; t2 < (G + 1) * H2; t2 += 256) {
+            const int head = t2 / H2, ii = t2 % H2;  // head == G: the k head
+            const float* s = y + head * HD;
+            const float x1 = s[ii], x2 = s[ii + H2];
+            const float c = csp[2 * ii], sn = csp[2 * ii + 1];
+            const float ac = x1 * c, bs = x2 * sn, bc = x2 * c, as = x1 * sn;
+            const uint32_t o1 = f2bf(ac - bs), o2 = f2bf(bc + as);
+            if (head < G) {
+                qb[head * HD + ii] = (uint16_t)o1;
+                qb[head * HD + ii + H2] = (uint16_t)o2;
+            } else {
+                kdst[ii] = (uint16_t)o1;
+                kdst[ii + H2] = (uint16_t)o2;
+                kps[ii] = bf2f(o1);
+                kps[ii + H2] = bf2f(o2);
+            }
+        }
+        for (int d = t; d < HD; d += 256) {
+            const float v = y[(G + 1) * HD + d];
+            vdst[d] = (uint16_t)f2bf(v);
+            vps[d] = v;
+        }
+    }
+    __syncthreads();
+
+    // ---- position p's own score (log2 units): wave w takes heads w, w + 4
+#pragma unroll
+    for (int hh = 0; hh < (GP + FA_WAVES - 1) / FA_WAVES; ++hh) {
+        const int h = wave + FA_WAVES * hh;
+        if (h < G) {
+            float s = 0.0f;
+            for (int d = lane; d < HD; d += 64) s += bf2f(qb[h * HD + d]) * kps[d];
+            s = wave_sum_fast(s);
+            if (lane == 0) sp[h] = s * sl2;
+        }
+    }
+
+    // ---- main loop over positions 0..p-1
+    uint4 qa[KST];
+#pragma unroll
+    for (int st = 0; st < KST; ++st)
+        qa[st] = jl < G ? *reinterpret_cast<const uint4*>(qb + jl * HD + st * 32 + qg * 8) : make_uint4(0, 0, 0, 0);
+    float mrow[4], lrow[4];  // per head h = 4 qg + v (lanes of group qg)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) { mrow[v] = -__builtin_inff(); lrow[v] = 0.0f; }
+    float o[GP][8];
+#pragma unroll
+    for (int h = 0; h < GP; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[h][e] = 0.0f;
+
+    const size_t kv_stride = (size_t)m.Hkv * 16 * HD;  // K -> V of the same page
+    // loads of page step s (positions 16 s .. 16 s + 15): K rows straight into B-operand
+    // registers, V rows for the P V product; positions >= p read the step's last valid
+    // row (never used: their scores are masked and their V zeroed)
+    auto fetch = [&](int s, uint4 (&kb)[KST], uint4 (&vb)[VL]) {
+        int page;
+        if (pg_lds)
+            page = pgs[s];
+        else
+            page = ptab[s];
+        const uint16_t* kp = a.kv_pool + ((((size_t)a.layer * m.n_pages + page) * 2) * m.Hkv + kh) * (size_t)16 * HD;
+#pragma unroll
+        for (int st = 0; st < KST; ++st) kb[st] = *reinterpret_cast<const uint4*>(kp + jl * HD + st * 32 + qg * 8);
+#pragma unroll
+        for (int tt = 0; tt < VL; ++tt) {
+            const int pl = min(PPI * tt + po, p - 1 - 16 * s);
+            vb[tt] = *reinterpret_cast<const uint4*>(kp + kv_stride + pl * HD + dg * 8);
+        }
+    };
+    auto compute = [&](int s, const uint4 (&kb)[KST], const uint4 (&vb)[VL]) {
+        const int base = 16 * s;
+        f32x4_ft sc = f32x4_ft{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int st = 0; st < KST; ++st)
+            sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_ft, qa[st]),
+                                                         __builtin_bit_cast(bf16x8_ft, kb[st]), sc, 0, 0, 0);
+        float alpha[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const float x = (base + jl < p) ? sc[v] * sl2 : -__builtin_inff();
+            float mx = x;
+#pragma unroll
+            for (int o2 = 1; o2 < 16; o2 <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o2, 64));
+            const float mn = fmaxf(mrow[v], mx);
+            alpha[v] = exp2f(mrow[v] - mn);
+            mrow[v] = mn;
+            const float pv = exp2f(x - mn);
+            sc[v] = pv;
+            lrow[v] = lrow[v] * alpha[v] + pv;
+        }
+        // rescale O and accumulate P V; head h's P of position pl sits in lane pl + 16 (h / 4)
+#pragma unroll
+        for (int h = 0; h < GP; ++h) {
+            const float al = __shfl(alpha[h & 3], 16 * (h >> 2), 64);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o[h][e] *= al;
+        }
+#pragma unroll
+        for (int tt = 0; tt < VL; ++tt) {
+            const int pl = PPI * tt + po;
+            const uint4 vr = base + pl < p ? vb[tt] : make_uint4(0, 0, 0, 0);
+            const float v8[8] = {bf_lo(vr.x), bf_hi(vr.x), bf_lo(vr.y), bf_hi(vr.y),
+                                 bf_lo(vr.z), bf_hi(vr.z), bf_lo(vr.w), bf_hi(vr.w)};
+#pragma unroll
+            for (int h = 0; h < GP; ++h) {
+                const float ph = __shfl(sc[h & 3], pl + 16 * (h >> 2), 64);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) o[h][e] = __builtin_fmaf(ph, v8[e], o[h][e]);
+            }
+        }
+    };
+    const int nst = npg;  // page steps over positions 0..p-1
+    int s = wave;
+    if (s < nst) {
+        uint4 kA[KST], vA[VL], kB[KST], vB[VL];
+        fetch(s, kA, vA);
+        while (true) {
+            if (s + FA_WAVES >= nst) { compute(s, kA, vA); break; }
+            fetch(s + FA_WAVES, kB, vB);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(s, kA, vA);
+            s += FA_WAVES;
+            if (s + FA_WAVES >= nst) { compute(s, kB, vB); break; }
+            fetch(s + FA_WAVES, kA, vA);
+            __builtin_amdgcn_sched_barrier(0);
+            compute(s, kB, vB);
+            s += FA_WAVES;
+        }
+    }
+
+    // ---- wave partials: O reduced over the position groups, l over the 16 position lanes
+#pragma unroll
+    for (int h = 0; h < GP; ++h)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            for (int off = DG; off < 64; off <<= 1) o[h][e] += __shfl_xor(o[h][e], off, 64);
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+        for (int off = 1; off < 16; off <<= 1) lrow[v] += __shfl_xor(lrow[v], off, 64);
+#pragma unroll
+    for (int h = 0; h < GP; ++h) {
+        const float mh = __shfl(mrow[h & 3], 16 * (h >> 2), 64);
+        const float lh = __shfl(lrow[h & 3], 16 * (h >> 2), 64);
+        if (lane == 0) {
+            wm[wave][h] = mh;
+            wl[wave][h] = lh;
+        }
+        if (po == 0) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) wo[wave][h * HD + dg * 8 + e] = o[h][e];
+        }
+    }
+    __syncthreads();
+
+    // ---- merge the wave partials and position p
+    for (int oi = t; oi < G * HD; oi += 256) {
+        const int h = oi / HD, d = oi % HD;
+        float M = sp[h];
+#pragma unroll
+        for (int w = 0; w < FA_WAVES; ++w) M = fmaxf(M, wm[w][h]);
+        const float ws = exp2f(sp[h] - M);
+        float L = ws, O = ws * vps[d];
+#pragma unroll
+        for (int w = 0; w < FA_WAVES; ++w) {
+            const float ww = exp2f(wm[w][h] - M);
+            L += ww * wl[w][h];
+            O += ww * wo[w][h * HD + d];
+        }
+        a.out[(size_t)r * Nq + (size_t)(kh * G + h) * HD + d] = (uint16_t)f2bf(O / L);
+    }
+}
+
+template <int HD>
+static void launch_hd(const FastAttnArgs& a, int gp, dim3 grid, hipStream_t s) {
+    switch (gp) {
+        case 1: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 1>), grid, dim3(256), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 2>), grid, dim3(256), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 4>), grid, dim3(256), 0, s, a); break;
+        default: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 8>), grid, dim3(256), 0, s, a); break;
+    }
+}
+
+hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s) {
+    if (a.B <= 0) return hipSuccess;
+    const int G = a.m.Hq / a.m.Hkv;
+    if (G < 1 || G > 8 || a.m.page_size != 16 || (a.m.hd != 64 && a.m.hd != 128)) return hipErrorInvalidValue;
+    const int gp = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
+    const dim3 grid(a.m.Hkv, a.B);
+    if (a.m.hd == 128)
+        launch_hd<128>(a, gp, grid, s);
+    else
+        launch_hd<64>(a, gp, grid, s);
+    return hipGetLastError();
+}
+
+}  // namespace mg

@@ -7,10 +7,7 @@
 // embedding table instead.
 // swiglu_part: sums the gate/up partial tiles, rounds g and u to bf16 and writes
 // a = bf16(silu(g) * u) once, for the down projection to stage.
-// rope_kv_part: one block per (row, KV head).  Sums the QKV partial tiles, adds the bias and
-// rounds to bf16 (the projection's rounding point), then rotates q and k (rotate-half
-// RoPE from the fp32 cos/sin table) and appends K' and V to the paged cache at the
-// row's position: the fast path's tentative column.
+// (The QKV partial tiles are consumed by the fused attention kernel, k_attn_fast.hip.)
 #include "mg_device.h"
 #include "mg_kernels.h"
 
@@ -125,78 +122,6 @@ hipError_t launch_swiglu_part(int B, const float* part, int S, int F, uint16_t* 
     if (B <= 0) return hipSuccess;
     if (F % 4) return hipErrorInvalidValue;
     hipLaunchKernelGGL(swiglu_part_kernel, dim3((F / 4 + 255) / 256, B), dim3(256), 0, s, B, part, S, F, act);
-    return hipGetLastError();
-}
-
-constexpr int RK_MAXF = 10 * 128;  // features of one KV group: (G + 2) * hd, G <= 8
-
-__global__ __launch_bounds__(256) void rope_kv_part_kernel(int M, const float* __restrict__ part, int S,
-                                                           const uint16_t* __restrict__ bq,
-                                                           const uint16_t* __restrict__ bk,
-                                                           const uint16_t* __restrict__ bv,
-                                                           const int32_t* __restrict__ positions,
-                                                           const int32_t* __restrict__ page_table, ModelDims m,
-                                                           int layer, const float* __restrict__ cs,
-                                                           uint16_t* __restrict__ qrot, uint16_t* __restrict__ kv_pool) {
-    const int r = blockIdx.x, kh = blockIdx.y;
-    const int hd = m.hd, h2 = hd / 2, G = m.Hq / m.Hkv, Nq = m.Hq * hd, Nk = m.Hkv * hd, N = Nq + 2 * Nk;
-    // this block's features: q heads kh*G .. kh*G+G-1, then k head kh, then v head kh
-    __shared__ float y[RK_MAXF];
-    const int nf = (G + 2) * hd;
-    const float* pp = part + (size_t)r * N;
-    const size_t sstride = (size_t)M * N;
-    for (int q = threadIdx.x; q < nf / 4; q += 256) {
-        const int f = 4 * q;                 // local feature
-        int n, nb;
-        const uint16_t* b;
-        if (f < G * hd) { n = kh * G * hd + f; b = bq; nb = n; }
-        else if (f < (G + 1) * hd) { nb = kh * hd + f - G * hd; n = Nq + nb; b = bk; }
-        else { nb = kh * hd + f - (G + 1) * hd; n = Nq + Nk + nb; b = bv; }
-        float4 v = sum_splits4(pp + n, sstride, S);
-        if (b) {
-            v.x += bf2f(b[nb]); v.y += bf2f(b[nb + 1]); v.z += bf2f(b[nb + 2]); v.w += bf2f(b[nb + 3]);
-        }
-        y[f] = bf2f(f2bf(v.x));
-        y[f + 1] = bf2f(f2bf(v.y));
-        y[f + 2] = bf2f(f2bf(v.z));
-        y[f + 3] = bf2f(f2bf(v.w));
-    }
-    __syncthreads();
-    const int pos = positions[r];
-    const float* csp = cs + (size_t)pos * hd;
-    const int page = page_table[(size_t)r * m.max_pages_per_row + pos / m.page_size];
-    const int slot = pos % m.page_size;
-    const int hs = hd * m.page_size;  // head stride inside a page
-    uint16_t* kdst = kv_pool + (((size_t)layer * m.n_pages + page) * 2) * (size_t)Nk * m.page_size + (size_t)kh * hs +
-                     (size_t)slot * hd;
-    uint16_t* vdst = kdst + (size_t)Nk * m.page_size;
-    for (int t = threadIdx.x; t < (G + 1) * h2; t += 256) {
-        const int head = t / h2, ii = t % h2;  // head == G: the k head
-        const float* s = y + head * hd;
-        const float a = s[ii], b = s[ii + h2];
-        const float c = csp[2 * ii], sn = csp[2 * ii + 1];
-        const float ac = a * c, bs = b * sn, bc = b * c, as = a * sn;
-        const uint16_t o1 = (uint16_t)f2bf(ac - bs), o2 = (uint16_t)f2bf(bc + as);
-        if (head < G) {
-            uint16_t* qd = qrot + (size_t)r * Nq + (size_t)(kh * G + head) * hd;
-            qd[ii] = o1;
-            qd[ii + h2] = o2;
-        } else {
-            kdst[ii] = o1;
-            kdst[ii + h2] = o2;
-        }
-    }
-    for (int t = threadIdx.x; t < hd; t += 256) vdst[t] = (uint16_t)f2bf(y[(G + 1) * hd + t]);
-}
-
-hipError_t launch_rope_kv_part(int B, const float* part, int S, const uint16_t* const* bias, const int32_t* positions,
-                               const int32_t* page_table, const ModelDims& m, int layer, const float* rope_cs,
-                               uint16_t* qrot, uint16_t* kv_pool, hipStream_t s) {
-    if (B <= 0) return hipSuccess;
-    if ((m.Hq / m.Hkv + 2) * m.hd > RK_MAXF) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(rope_kv_part_kernel, dim3(B, m.Hkv), dim3(256), 0, s, B, part, S, bias ? bias[0] : nullptr,
-                       bias ? bias[1] : nullptr, bias ? bias[2] : nullptr, positions, page_table, m, layer, rope_cs,
-                       qrot, kv_pool);
     return hipGetLastError();
 }
 

@@ -18,14 +18,13 @@ namespace {
 
 constexpr int WPL = 12;
 constexpr int CANON_CHUNK = 256;
-constexpr int FAST_CHUNK_MIN = 64;
 constexpr size_t ALIGN = 256;
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 struct Plan {
     size_t rope, x, h, qkv, qrot, att, gu, act, attn_part, gemm_part, top2_ws, vlog, total;
-    int rows_cap, max_pos, chunks_canon, chunks_fast, attn_rows_fast, gemm_part_floats;
+    int rows_cap, max_pos, chunks_canon;
 };
 
 bool shape_ok(const mg_model_cfg* c) {
@@ -63,7 +62,6 @@ Plan make_plan(const mg_model_cfg* c, int n_cu) {
     p.rows_cap = c->max_batch > pre ? c->max_batch : pre;
     p.max_pos = c->max_pages_per_row * c->page_size;
     p.chunks_canon = (p.max_pos + CANON_CHUNK - 1) / CANON_CHUNK;
-    p.chunks_fast = (p.max_pos + FAST_CHUNK_MIN - 1) / FAST_CHUNK_MIN;
     const size_t R = p.rows_cap;
     size_t o = 0;
     p.rope = o; o += up((size_t)p.max_pos * hd * sizeof(float));
@@ -75,8 +73,7 @@ Plan make_plan(const mg_model_cfg* c, int n_cu) {
     p.gu = o; o += up(R * 2 * (size_t)F * 2);
     p.act = o; o += up(R * (size_t)F * 2);
     const size_t ap_canon = R * Hq * (size_t)p.chunks_canon * (hd + 2);
-    const size_t ap_fast = (size_t)c->max_batch * Hq * (size_t)p.chunks_fast * (hd + 2);
-    p.attn_part = o; o += up((ap_canon > ap_fast ? ap_canon : ap_fast) * sizeof(float));
+    p.attn_part = o; o += up(ap_canon * sizeof(float));
     ProjShape ps[5];
     fast_projs(c, ps);
     // split-K partial tiles of the QKV, O, gate/up and down projections: S * M * N
@@ -389,14 +386,10 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
     const mg_model_cfg& g = c->cfg;
     const ModelDims& m = c->m;
     const int d = g.d_model, Nq = g.n_q_heads * g.head_dim, Nk = g.n_kv_heads * g.head_dim, F = g.d_ffn;
-    Items it{nullptr, nullptr, B, tokens, positions, page_table, 0};
     uint16_t* x = c->at<uint16_t>(c->plan.x);
     uint16_t* h = c->at<uint16_t>(c->plan.h);
-    uint16_t* qkv = c->at<uint16_t>(c->plan.qkv);
-    uint16_t* qrot = c->at<uint16_t>(c->plan.qrot);
     uint16_t* att = c->at<uint16_t>(c->plan.att);
     uint16_t* act = c->at<uint16_t>(c->plan.act);
-    const int chunk = fast_attention_split();
     float* part = c->at<float>(c->plan.gemm_part);
     // layer 0 input: embedding gather fused with the first RMSNorm
     HIPCHK(launch_resid_norm(B, nullptr, 0, c->W(0), tokens, d, c->LW(0, 0), g.rms_eps, x, h, s));
@@ -408,24 +401,25 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
             MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 3, nullptr, FEPI_PART, s, &S));
         }
         {
-            const uint16_t* Bs[3] = {c->LW(l, 4), c->LW(l, 5), c->LW(l, 6)};
-            HIPCHK(launch_rope_kv_part(B, part, S, g.qkv_bias ? Bs : nullptr, positions, page_table, m, l,
-                                       c->at<float>(c->plan.rope), qrot, c->kv_pool, s));
-        }
-        {
-            AttnArgs a{};
-            a.it = it;
+            // QKV split sum + bias + RoPE + tentative K/V append + attention
+            FastAttnArgs a{};
+            a.B = B;
+            a.part = part;
+            a.S = S;
+            if (g.qkv_bias) {
+                a.bq = c->LW(l, 4);
+                a.bk = c->LW(l, 5);
+                a.bv = c->LW(l, 6);
+            }
+            a.positions = positions;
+            a.page_table = page_table;
             a.m = m;
             a.layer = l;
-            a.qrot = qrot;
+            a.cs = c->at<float>(c->plan.rope);
             a.kv_pool = c->kv_pool;
-            a.own_col = nullptr;
-            a.part = c->at<float>(c->plan.attn_part);
-            a.chunk = chunk;
-            a.max_chunks = (c->plan.max_pos + chunk - 1) / chunk;
             a.out = att;
             ProfScope ps(c, MG_KIND_FAST_ATTN, s, 0.0);
-            HIPCHK(launch_attention(a, 0, s));
+            HIPCHK(launch_fast_attention(a, s));
         }
         {
             const uint16_t* W[1] = {c->LW(l, 7)};

@@ -76,12 +76,6 @@ hipError_t launch_resid_norm(int B, const float* part, int S, const uint16_t* em
                              const uint16_t* gamma, float eps, uint16_t* x, uint16_t* h, hipStream_t s);
 // act[r] = bf16(silu(bf16(sum gate partials)) * bf16(sum up partials)); part rows [gate F | up F]
 hipError_t launch_swiglu_part(int B, const float* part, int S, int F, uint16_t* act, hipStream_t s);
-// qkv[r] = bf16(sum_s part[s][r] + bias), then RoPE of q and k, q' -> qrot, K' and V into
-// the paged cache at the row's position
-hipError_t launch_rope_kv_part(int B, const float* part, int S, const uint16_t* const* bias, const int32_t* positions,
-                               const int32_t* page_table, const ModelDims& m, int layer, const float* rope_cs,
-                               uint16_t* qrot, uint16_t* kv_pool, hipStream_t s);
-
 // ---------------------------------------------------------------- small kernels
 hipError_t launch_embed(const Items& it, const uint16_t* embed, int d, uint16_t* x, hipStream_t s);
 hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, int n_host, const int32_t* n_dev, int cap, int d,
@@ -107,8 +101,24 @@ struct AttnArgs {
     int max_chunks;
     uint16_t* out;             // [n][Hq*hd]
 };
-hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s);
-int fast_attention_split();  // positions per split of the fast attention
+hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s);  // canonical (canon = 1) only
+
+// fast path: QKV split sum + bias + RoPE + tentative K/V append + attention, one block
+// per (row, KV head); rows 0..B-1 of the step batch
+struct FastAttnArgs {
+    int B;
+    const float* part;          // QKV split partials [S][B][Nq + 2 Nk]
+    int S;
+    const uint16_t *bq, *bk, *bv;  // biases or NULL
+    const int32_t* positions;   // [B]
+    const int32_t* page_table;  // [B][max_pages_per_row]
+    ModelDims m;
+    int layer;
+    const float* cs;            // RoPE table [max_pos][hd] (cos, sin interleaved)
+    uint16_t* kv_pool;
+    uint16_t* out;              // [B][Hq * hd] bf16
+};
+hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s);
 
 // ---------------------------------------------------------------- gate / repair / misc
 // top-1 / top-2 of B <= 256 logit rows in two launches (vocabulary slices, then a

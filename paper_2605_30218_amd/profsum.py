@@ -45,7 +45,7 @@ def _short(name: str) -> str:
     return n.replace("void ", "").replace("mg::", "")
 
 
-MODE_KERNELS = ("fast_gemm_kernel", "canon_gemv_kernel", "attn_fast_kernel", "attn_canon_kernel")
+MODE_KERNELS = ("fast_gemm_kernel", "canon_gemv_kernel", "attn_fast_fused_kernel", "attn_canon_kernel")
 
 
 def _mode_tables(rows, modes):
