@@ -111,10 +111,14 @@ mg_status mg_decode_step(mg_ctx* ctx, int B, const int32_t* tokens, const int32_
  * logits [device fp32 B*V]; protected_mask [device uint8 B] or NULL (= all rows
  * protected, Sec. 3.3's per-request policy); top1, gated_rows [device int32 B];
  * margin [device fp32 B]; gate [device uint8 B]; n_gated [device int32 1].
+ * n_gated_host: NULL, or one int32 of pinned host memory (allocated with
+ * hipHostMalloc) that also receives the count, stored with system scope after
+ * gated_rows and *n_gated are written, so a host can poll it instead of
+ * synchronising the stream (the caller sets it to a negative value first).
  * Bit-exact: comparisons only, no rounding. */
 mg_status mg_margin_gate(mg_ctx* ctx, int B, const float* logits, const uint8_t* protected_mask, float tau,
                          int32_t* top1, float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated,
-                         void* stream);
+                         int32_t* n_gated_host, void* stream);
 
 /* (3) The deterministic verifier (Sec. 3.2, deterministic verifier contract):
  * runs the current step again for rows rows[0..n) of the step batch with

@@ -286,7 +286,8 @@ __global__ __launch_bounds__(256) void top2_slice_kernel(int B, int V, int slice
 __global__ __launch_bounds__(1024) void top2_final_kernel(int B, const Top2* __restrict__ part, int nsl,
                                                           const uint8_t* __restrict__ prot, float tau, int32_t* top1,
                                                           float* margin, uint8_t* gate, int32_t* gated_rows,
-                                                          int32_t* n_gated, const int32_t* n_dev) {
+                                                          int32_t* n_gated, int32_t* n_gated_host,
+                                                          const int32_t* n_dev) {
     const int nrows = n_dev ? min(max(*n_dev, 0), B) : B;
     const int t = threadIdx.x;
     const int tpr = nsl / 2;            // threads per row (power of two, <= 64)
@@ -324,7 +325,13 @@ __global__ __launch_bounds__(1024) void top2_final_kernel(int B, const Top2* __r
         int base = 0;
         for (int k = 0; k < w; ++k) base += wave_cnt[k];
         if (f) gated_rows[base + __popcll(bal & ((1ull << l) - 1ull))] = t;
-        if (t == 0) *n_gated = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+        if (t == 0) {
+            const int cnt = wave_cnt[0] + wave_cnt[1] + wave_cnt[2] + wave_cnt[3];
+            *n_gated = cnt;
+            // mirror for a host that polls pinned memory (a system-scope release store; the
+            // device-side consumers of the rows are ordered by the stream)
+            if (n_gated_host) __hip_atomic_store(n_gated_host, cnt, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
     }
 }
 
@@ -336,8 +343,8 @@ int top2_slices(int B, int V) {
 }
 
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1, float* margin,
-                       uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, void* part_ws, const int32_t* n_dev,
-                       hipStream_t s) {
+                       uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* n_gated_host, void* part_ws,
+                       const int32_t* n_dev, hipStream_t s) {
     if (B <= 0) return hipSuccess;
     if (B > 256) return hipErrorInvalidValue;
     const int nsl = top2_slices(B, V);
@@ -346,7 +353,7 @@ hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, f
     Top2* part = static_cast<Top2*>(part_ws);
     hipLaunchKernelGGL(top2_slice_kernel, dim3(nsl, B), dim3(256), 0, s, B, V, slice, logits, part, nsl, n_dev);
     hipLaunchKernelGGL(top2_final_kernel, dim3(1), dim3(1024), 0, s, B, part, nsl, prot, tau, top1, margin, gate,
-                       gated_rows, n_gated, n_dev);
+                       gated_rows, n_gated, n_gated_host, n_dev);
     return hipGetLastError();
 }
 

@@ -449,14 +449,14 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
 
 mg_status mg_margin_gate(mg_ctx* c, int B, const float* logits, const uint8_t* protected_mask, float tau,
                          int32_t* top1, float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated,
-                         void* stream) {
+                         int32_t* n_gated_host, void* stream) {
     if (!c || !logits || !top1 || !margin || !gate || !gated_rows || !n_gated) return MG_ERR_ARG;
     if (B < 0 || B > c->cfg.max_batch) return MG_ERR_ARG;
     if (B == 0) return MG_OK;
     hipStream_t s = static_cast<hipStream_t>(stream);
     ProfScope ps(c, MG_KIND_GATE, s, (double)B * c->cfg.vocab * 4.0);
     HIPCHK(launch_top2(B, c->cfg.vocab, logits, protected_mask, tau, top1, margin, gate, gated_rows, n_gated,
-                       c->ws + c->plan.top2_ws, nullptr, s));
+                       n_gated_host, c->ws + c->plan.top2_ws, nullptr, s));
     return MG_OK;
 }
 
@@ -472,7 +472,7 @@ mg_status mg_verify_rows(mg_ctx* c, int n, const int32_t* rows, const int32_t* n
     Items it{rows, n == -1 ? n_dev : nullptr, cap, tokens, positions, page_table, 0};
     float* lg = v_logits ? v_logits : c->at<float>(c->plan.vlog);
     MGCHK(canon_forward(c, it, v_kvcol, lg, s));
-    HIPCHK(launch_top2(cap, c->cfg.vocab, lg, nullptr, 0.0f, v_tok, nullptr, nullptr, nullptr, nullptr,
+    HIPCHK(launch_top2(cap, c->cfg.vocab, lg, nullptr, 0.0f, v_tok, nullptr, nullptr, nullptr, nullptr, nullptr,
                        c->ws + c->plan.top2_ws, it.n_dev, s));
     return MG_OK;
 }

@@ -125,8 +125,8 @@ hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s);
 // per-row merge and the ordered compaction); part_ws holds TOP2_WS_BYTES
 constexpr size_t TOP2_WS_BYTES = 256 * 128 * 16;
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1,
-                       float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, void* part_ws,
-                       const int32_t* n_dev, hipStream_t s);
+                       float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* n_gated_host,
+                       void* part_ws, const int32_t* n_dev, hipStream_t s);
 hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_t* rows, const int32_t* positions,
                          const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
                          const uint16_t* v_kvcol, const ModelDims& m, uint16_t* kv_pool, int32_t* emitted,

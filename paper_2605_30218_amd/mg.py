@@ -9,6 +9,7 @@ from __future__ import annotations
 import ctypes as C
 import os
 
+import numpy as np
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
@@ -46,7 +47,7 @@ SIGNATURES = {
     "mg_create": (I, [P, P, P, SZ, P, SZ, P]),
     "mg_destroy": (I, [P]),
     "mg_decode_step": (I, [P, I, P, P, P, P, P]),
-    "mg_margin_gate": (I, [P, I, P, P, F, P, P, P, P, P, P]),
+    "mg_margin_gate": (I, [P, I, P, P, F, P, P, P, P, P, P, P]),
     "mg_verify_rows": (I, [P, I, P, P, P, P, P, P, P, P, P]),
     "mg_repair_kv_column": (I, [P, I, P, P, P, P, P, P, P, P, P, P]),
     "mg_prefill": (I, [P, I, P, P, P, P, P]),
@@ -79,6 +80,22 @@ def load():
             f.argtypes = args
         _lib = lib
     return _lib
+
+
+def host_count_slot():
+    """A few int32 of coherent, mapped pinned host memory (hipHostMalloc), for a count that
+    a kernel stores with system scope and the host polls.  Returns (device pointer, numpy
+    view of the int32s).  The memory is held until the process ends."""
+    hip = C.CDLL("libamdhip64.so")
+    host = C.c_void_p()
+    flags = 0x40000000 | 0x2  # hipHostMallocCoherent | hipHostMallocMapped
+    if hip.hipHostMalloc(C.byref(host), C.c_size_t(64), C.c_uint(flags)) != 0 or not host.value:
+        raise RuntimeError("hipHostMalloc of the gate count slot failed")
+    dev = C.c_void_p()
+    if hip.hipHostGetDevicePointer(C.byref(dev), host, C.c_uint(0)) != 0 or not dev.value:
+        raise RuntimeError("hipHostGetDevicePointer of the gate count slot failed")
+    view = np.ctypeslib.as_array((C.c_int32 * 16).from_address(host.value))
+    return dev.value, view
 
 
 def _ptr(t):
@@ -151,10 +168,12 @@ class Engine:
         _check("mg_decode_step", self.lib.mg_decode_step(self.ctx, B, _ptr(tokens), _ptr(positions),
                                                          _ptr(page_table), _ptr(logits), _stream(stream)))
 
-    def margin_gate(self, B, logits, protected_mask, tau, top1, margin, gate, gated_rows, n_gated, stream=None):
+    def margin_gate(self, B, logits, protected_mask, tau, top1, margin, gate, gated_rows, n_gated,
+                    n_gated_host=None, stream=None):
+        """n_gated_host: optional pinned CPU int32 tensor that receives the count too."""
         _check("mg_margin_gate", self.lib.mg_margin_gate(self.ctx, B, _ptr(logits), _ptr(protected_mask), float(tau),
                                                          _ptr(top1), _ptr(margin), _ptr(gate), _ptr(gated_rows),
-                                                         _ptr(n_gated), _stream(stream)))
+                                                         _ptr(n_gated), _ptr(n_gated_host), _stream(stream)))
 
     def verify_rows(self, n, rows, n_dev, tokens, positions, page_table, v_logits, v_tok, v_kvcol, stream=None):
         _check("mg_verify_rows", self.lib.mg_verify_rows(self.ctx, n, _ptr(rows), _ptr(n_dev), _ptr(tokens),

@@ -1,17 +1,21 @@
 """Host-side sequencing of the MarginGate decode loop over libmg (arXiv 2605.30218, Sec. 3).
 
-Per step: the fast batched forward (tentative K/V append), the margin gate, one
-device-to-host read of the gated-row count, the verifier on exactly those rows, and
-the commit / single-column repair.  Modes: "off" (fast path only, r_verify = 0),
+Per step: the fast batched forward (tentative K/V append), the margin gate (which
+also stores the gated-row count into pinned host memory, polled here instead of a
+stream synchronisation), the verifier on exactly those rows, and the commit /
+single-column repair.  Modes: "off" (fast path only, r_verify = 0),
 "gated" (MarginGate), "always" (the verifier on every protected row, r_verify = 1:
 the always-on baseline of Sec. 3.3).  All arithmetic runs in libmg; this module only
 orders calls and keeps counters.
 """
 from __future__ import annotations
 
+import time
+
 import numpy as np
 import torch
 
+from . import mg
 from .mg import Engine
 
 
@@ -38,8 +42,9 @@ class GatedDecoder:
         self.v_tok = torch.empty(B, **i32)
         self.v_kvcol = torch.empty((B, engine.col_elems), dtype=torch.int16, device=dev)
         self.n_repaired = torch.zeros(1, **i32)
-        self._n_host = torch.zeros(1, dtype=torch.int32, pin_memory=True)
-        self._ev = torch.cuda.Event()
+        # the gate mirrors its count into pinned host memory; the host polls it instead of
+        # synchronising the stream
+        self._count_dev, self._count = mg.host_count_slot()
         self.steps = 0
         self.protected_row_steps = 0
         self.verified_row_steps = 0
@@ -54,18 +59,18 @@ class GatedDecoder:
         logits / top1 / margin / gate / rows / v_tok (tests)."""
         e, B = self.e, self.B
         e.decode_step(B, self.tokens, self.positions, self.page_table, self.logits)
+        gated = mode not in ("off", "always")
+        if gated:
+            self._count[0] = -1
         e.margin_gate(B, self.logits, self.protected, self.tau, self.top1, self.margin, self.gate, self.gated_rows,
-                      self.n_gated)
+                      self.n_gated, self._count_dev if gated else None)
         if mode == "off":
             n, rows = 0, self.gated_rows
         elif mode == "always":
             rows = self.always_rows
             n = int(rows.numel())
         else:
-            self._n_host.copy_(self.n_gated, non_blocking=True)
-            self._ev.record()
-            self._ev.synchronize()
-            n, rows = int(self._n_host[0]), self.gated_rows
+            n, rows = self._wait_count(), self.gated_rows
         if keep is not None:
             keep.update(logits=self.logits.cpu().numpy(), top1=self.top1.cpu().numpy(),
                         margin=self.margin.cpu().numpy(), gate=self.gate.cpu().numpy(),
@@ -84,6 +89,24 @@ class GatedDecoder:
         self.verified_row_steps += n
         self.hist.append(n)
         return n
+
+    def _wait_count(self, limit_s: float = 60.0) -> int:
+        """Poll the pinned count slot until the gate kernel has stored the count."""
+        spins, t0 = 0, None
+        while True:
+            v = int(self._count[0])
+            if v >= 0:
+                return v
+            spins += 1
+            if spins % 4096 == 0:
+                now = time.perf_counter()
+                t0 = now if t0 is None else t0
+                if now - t0 > limit_s:
+                    torch.cuda.synchronize()  # surfaces a kernel error, if any
+                    v = int(self._count[0])
+                    if v < 0:
+                        raise RuntimeError("the margin gate's count never reached host memory")
+                    return v
 
     @property
     def r_verify(self):

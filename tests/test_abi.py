@@ -61,7 +61,7 @@ def test_null_arguments_are_rejected_before_any_work():
     assert lib.mg_create(None, None, None, 0, None, 0, C.byref(out)) == -1
     assert lib.mg_create(C.byref(cfg), None, None, 0, None, 0, C.byref(out)) == -1
     assert lib.mg_decode_step(None, 1, None, None, None, None, None) == -1
-    assert lib.mg_margin_gate(None, 1, None, None, 0.5, None, None, None, None, None, None) == -1
+    assert lib.mg_margin_gate(None, 1, None, None, 0.5, None, None, None, None, None, None, None) == -1
     assert lib.mg_verify_rows(None, 1, None, None, None, None, None, None, None, None, None) == -1
     assert lib.mg_repair_kv_column(None, 1, None, None, None, None, None, None, None, None, None, None) == -1
     assert lib.mg_prefill(None, 1, None, None, None, None, None) == -1
