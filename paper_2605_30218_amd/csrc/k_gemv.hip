@@ -8,8 +8,8 @@
 //   group) starting from +0; the 64 lane sums are combined by the xor butterfly
 //   over offsets 32, 16, 8, 4, 2, 1 (all J*R butterflies of a wave are run
 //   together with the same pairings, see butterfly_sum_multi).
-// A wave owns J features; a block of 4 waves owns 4J features and a tile of R
-// rows.  K is walked in chunks of 512 elements (one group per lane).  While the
+// A wave owns J features; a block of 8 waves owns 8J features and a tile of R
+// rows (so the tile's activations, staged once per block, serve 8J features).  K is walked in chunks of 512 elements (one group per lane).  While the
 // fma work of chunk c runs, the weights of chunk c+1 are in flight (register
 // double buffer: one 16-byte group per feature and lane, 1 KiB coalesced per
 // feature, in a ping-pong register pair) and the rows' activations of chunk c+1 are
@@ -33,10 +33,14 @@ constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
 #ifndef MG_GEMV_J_R16
 #define MG_GEMV_J_R16 2
 #endif
+#ifndef MG_GEMV_NW
+#define MG_GEMV_NW 8  // waves per block (measured: 8 beats 4 and 16)
+#endif
+constexpr int GV_NW = MG_GEMV_NW, GV_THREADS = 64 * MG_GEMV_NW;
 
 template <int R>
 struct GemvShape {
-    static constexpr int XLD = R * 64 / 256;  // staging loads (16 bytes) per thread per chunk
+    static constexpr int XLD = (R * 64 + GV_THREADS - 1) / GV_THREADS;  // staging loads (16 bytes) per thread per chunk
 };
 
 // activations of chunk kc for rows r0 .. r0+R-1: rows past nr read row nr-1 and k past
@@ -46,8 +50,8 @@ template <int R>
 __device__ __forceinline__ void gemv_load_x(const GemvArgs& a, int r0, int nr, int kc, uint4 (&xr)[GemvShape<R>::XLD]) {
 #pragma unroll
     for (int it = 0; it < GemvShape<R>::XLD; ++it) {
-        const int t = threadIdx.x + 256 * it;
-        const int rr = min(t >> 6, nr - 1), k = min(kc + (t & 63) * 8, a.K - 8);
+        const int t = threadIdx.x + GV_THREADS * it;
+        const int rr = min(min(t >> 6, R - 1), nr - 1), k = min(kc + (t & 63) * 8, a.K - 8);
         xr[it] = *reinterpret_cast<const uint4*>(a.X + (size_t)(r0 + rr) * a.K + k);
     }
 }
@@ -56,8 +60,9 @@ template <int R>
 __device__ __forceinline__ void gemv_store_x(float4 (*xs)[2][64], const uint4 (&xr)[GemvShape<R>::XLD]) {
 #pragma unroll
     for (int it = 0; it < GemvShape<R>::XLD; ++it) {
-        const int t = threadIdx.x + 256 * it;
+        const int t = threadIdx.x + GV_THREADS * it;
         const int rr = t >> 6, gl = t & 63;
+        if (GV_THREADS * GemvShape<R>::XLD > R * 64 && rr >= R) continue;
         const uint4 v = xr[it];
         xs[rr][0][gl] = make_float4(bf_lo(v.x), bf_hi(v.x), bf_lo(v.y), bf_hi(v.y));
         xs[rr][1][gl] = make_float4(bf_lo(v.z), bf_hi(v.z), bf_lo(v.w), bf_hi(v.w));
@@ -107,7 +112,7 @@ __device__ __forceinline__ void gemv_fma_chunk(const float4 (*xb)[2][64], int la
 }
 
 template <int J, int R, int EPI>
-__global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, int n_rt) {
+__global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int n_fb, int n_rt) {
     const int b = blockIdx.x;
     const int xcd = b & 7, slot = b >> 3;
     const int fb = (slot / n_rt) * 8 + xcd;
@@ -119,7 +124,7 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, i
     if (r0 >= n) return;
     const int nr = min(R, n - r0);
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-    const int jw = (fb * 4 + wave) * J;
+    const int jw = (fb * GV_NW + wave) * J;
     const int K = a.K, G = K >> 3;
 
     // LDS chunk: element 8*lane + 4*half + c of row rr at xs[rr][half][lane].c
@@ -206,13 +211,13 @@ __global__ __launch_bounds__(256) void canon_gemv_kernel(GemvArgs a, int n_fb, i
 
 template <int J, int R>
 static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s) {
-    const int n_fb = (a.N + 4 * J - 1) / (4 * J);
+    const int n_fb = (a.N + GV_NW * J - 1) / (GV_NW * J);
     const int n_rt = (rows + R - 1) / R;
     const dim3 grid(8 * ((n_fb + 7) / 8) * n_rt);
     switch (epi) {
-        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16>), grid, dim3(256), 0, s, a, n_fb, n_rt); break;
-        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID>), grid, dim3(256), 0, s, a, n_fb, n_rt); break;
-        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32>), grid, dim3(256), 0, s, a, n_fb, n_rt); break;
+        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
     }
     return hipGetLastError();
 }
