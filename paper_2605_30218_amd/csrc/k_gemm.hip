@@ -1,8 +1,8 @@
 // k_gemm.hip -- the fast path's weight-streaming projection on MFMA (gfx950).
 //
 // Y[M][N] = X[M][K] * W[N][K]^T with v_mfma_f32_16x16x32_bf16, M <= 256 (rows
-// padded to 16-row tiles).  A block of 4 waves owns 64*FT output features; a wave
-// owns 16*FT of them for all rows.  Weights go straight from HBM into MFMA
+// padded to 16-row tiles).  A block of 8 waves owns 128 output features; a wave
+// owns 16 of them for all rows (the activation tile staged in LDS serves all eight).  Weights go straight from HBM into MFMA
 // B-operand registers: lane (j, q) loads W[n+j][k+8q .. k+8q+7] (16 bytes), so a
 // 32-wide k step of 16 features reads 16 rows x 64 contiguous bytes.  The block
 // walks its K range in chunks of KC.  Chunk c+1 is requested while the MFMAs of
@@ -29,6 +29,10 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 #ifndef MG_GEMM_KC_SMALL
 #define MG_GEMM_KC_SMALL 128
 #endif
+#ifndef MG_GEMM_NW
+#define MG_GEMM_NW 8  // waves per block (measured: 8 beats 4 and 16)
+#endif
+constexpr int GM_NW = MG_GEMM_NW, GM_THREADS = 64 * MG_GEMM_NW;
 // K per chunk for a tile of MT 16-row tiles (host and device must agree)
 __host__ __device__ constexpr int gemm_kc(int MT) { return MT <= 4 ? MG_GEMM_KC_SMALL : MT <= 8 ? 128 : 64; }
 
@@ -39,8 +43,7 @@ struct GemmShape {
     static constexpr int STRIDE = KC * 2 + 16;    // LDS bytes per staged row
     static constexpr int NST = KC / 32;           // MFMA k-steps per chunk
     static constexpr int GPR = KC / 8;            // 16-byte groups per staged row
-    static constexpr int XLD = ROWS * GPR / 256;  // staging loads per thread per chunk
-    static_assert(XLD * 256 == ROWS * GPR, "staging must divide evenly");
+    static constexpr int XLD = (ROWS * GPR + GM_THREADS - 1) / GM_THREADS;  // staging loads per thread per chunk
 };
 
 template <int EPI>
@@ -64,8 +67,8 @@ __device__ __forceinline__ void load_x(const FastGemmArgs& a, int kc, uint4 (&xr
     using S = GemmShape<MT>;
 #pragma unroll
     for (int it = 0; it < S::XLD; ++it) {
-        const int t = threadIdx.x + 256 * it;
-        const int row = min(t / S::GPR, a.M - 1), k = kc + (t % S::GPR) * 8;
+        const int t = threadIdx.x + GM_THREADS * it;
+        const int row = min(min(t / S::GPR, S::ROWS - 1), a.M - 1), k = kc + (t % S::GPR) * 8;
         xr[it] = *reinterpret_cast<const uint4*>(a.X + (size_t)row * a.K + min(k, a.K - 8));
     }
 }
@@ -75,8 +78,9 @@ __device__ __forceinline__ void store_x(unsigned char* buf, int kc, int K, const
     using S = GemmShape<MT>;
 #pragma unroll
     for (int it = 0; it < S::XLD; ++it) {
-        const int t = threadIdx.x + 256 * it;
+        const int t = threadIdx.x + GM_THREADS * it;
         const int row = t / S::GPR, g = t % S::GPR;
+        if (GM_THREADS * S::XLD > S::ROWS * S::GPR && row >= S::ROWS) continue;
         const uint32_t keep = 0u - (uint32_t)(kc + g * 8 < K);
         const uint4 v = make_uint4(xr[it].x & keep, xr[it].y & keep, xr[it].z & keep, xr[it].w & keep);
         *reinterpret_cast<uint4*>(buf + row * S::STRIDE + g * 16) = v;
@@ -115,13 +119,13 @@ __device__ __forceinline__ void mfma_chunk(const unsigned char* buf, int jl, int
 }
 
 template <int MT, int FT, int EPI>
-__global__ __launch_bounds__(256) void fast_gemm_kernel(FastGemmArgs a) {
+__global__ __launch_bounds__(GM_THREADS) void fast_gemm_kernel(FastGemmArgs a) {
     using S = GemmShape<MT>;
     __shared__ __attribute__((aligned(16))) unsigned char xs[2][S::ROWS * S::STRIDE];
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int jl = lane & 15, q = lane >> 4;
     const int nb = blockIdx.x, split = blockIdx.y;
-    const int FB = 64 * FT;  // features per block
+    const int FB = 16 * GM_NW * FT;  // features per block
     const int K = a.K, M = a.M;
 
     const uint16_t* wrow[FT];
@@ -215,28 +219,25 @@ static int mt_for(int M) {
     return t <= 1 ? 1 : t <= 2 ? 2 : t <= 4 ? 4 : t <= 8 ? 8 : 16;
 }
 
-// Features per wave / 16: two B tiles per wave when the output is wide enough for
-// two 128-feature blocks per CU, one otherwise.
 static int g_n_cu = 256;
-int fast_gemm_ft(int M, int N) {
-    (void)M;
-#ifndef MG_GEMM_FT2_MIN_N
-#define MG_GEMM_FT2_MIN_N 8192
-#endif
-    return N >= MG_GEMM_FT2_MIN_N ? 2 : 1;
-}
+// One 16-feature B tile per wave: 8-wave blocks of 128 features with one tile each
+// measured faster than two tiles per wave (fewer blocks, more registers per wave).
+constexpr int GM_FT = 1;
 
 int fast_gemm_splits(int M, int N, int K, int n_cu) {
     g_n_cu = n_cu;
     const int KC = gemm_kc(mt_for(M));
     const int nchunks = (K + KC - 1) / KC;
-    const int FB = 64 * fast_gemm_ft(M, N);
+    const int FB = 16 * GM_NW * GM_FT;
     const int nb = (N + FB - 1) / FB;
     // enough blocks for about two per CU (four for small batches, whose blocks carry
     // little MFMA work per weight byte), each with at least 4 chunks, and the
     // partial tiles (S*M*N fp32, written once and read once by the consumer) at most
     // a quarter of the weight bytes
-    const int target = (M <= 16 ? 4 : 2) * n_cu;
+#ifndef MG_GEMM_BLOCKS_PER_CU
+#define MG_GEMM_BLOCKS_PER_CU 2
+#endif
+    const int target = (M <= 16 ? 2 * MG_GEMM_BLOCKS_PER_CU : MG_GEMM_BLOCKS_PER_CU) * n_cu;
     int S = (target + nb - 1) / nb;
     const int by_chunks = nchunks / 4 > 1 ? nchunks / 4 : 1;
     const long by_traffic = (long)K / (8L * (M < 16 ? 16 : M));
@@ -248,7 +249,7 @@ int fast_gemm_splits(int M, int N, int K, int n_cu) {
 
 template <int MT, int FT, int EPI>
 static void launch_epi(const FastGemmArgs& a, dim3 g, hipStream_t s) {
-    hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI>), g, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI>), g, dim3(GM_THREADS), 0, s, a);
 }
 
 template <int MT, int FT>
@@ -261,25 +262,21 @@ static void launch_ft(const FastGemmArgs& a, int epi, dim3 g, hipStream_t s) {
 }
 
 template <int MT>
-static void launch_mt(const FastGemmArgs& a, int epi, int ft, hipStream_t s) {
-    dim3 g((a.N + 64 * ft - 1) / (64 * ft), a.S);
-    if (ft == 2)
-        launch_ft<MT, 2>(a, epi, g, s);
-    else
-        launch_ft<MT, 1>(a, epi, g, s);
+static void launch_mt(const FastGemmArgs& a, int epi, hipStream_t s) {
+    dim3 g((a.N + 16 * GM_NW * GM_FT - 1) / (16 * GM_NW * GM_FT), a.S);
+    launch_ft<MT, GM_FT>(a, epi, g, s);
 }
 
 hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s) {
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
     if (a.K < 8 || a.K % 8 || a.N % 16) return hipErrorInvalidValue;
     if (epi != FEPI_PART && a.S != 1) return hipErrorInvalidValue;  // only partial tiles may be split
-    const int ft = fast_gemm_ft(a.M, a.N);
     switch (mt_for(a.M)) {
-        case 1: launch_mt<1>(a, epi, ft, s); break;
-        case 2: launch_mt<2>(a, epi, ft, s); break;
-        case 4: launch_mt<4>(a, epi, ft, s); break;
-        case 8: launch_mt<8>(a, epi, ft, s); break;
-        default: launch_mt<16>(a, epi, ft, s); break;
+        case 1: launch_mt<1>(a, epi, s); break;
+        case 2: launch_mt<2>(a, epi, s); break;
+        case 4: launch_mt<4>(a, epi, s); break;
+        case 8: launch_mt<8>(a, epi, s); break;
+        default: launch_mt<16>(a, epi, s); break;
     }
     return hipGetLastError();
 }
