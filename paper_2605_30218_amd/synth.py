@@ -137,3 +137,54 @@ def small_int_bf16(shape, seed: int, lo: int = -3, hi: int = 3):
     g.manual_seed(seed)
     v = torch.randint(lo, hi + 1, shape, generator=g).to(torch.float32)
     return v.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def perturb_lm_head_tie_pairs(weights, shape: ModelShape, seed: int = 4, n_pairs: int = 8, boost: float = 8.0,
+                              tau: float = 0.5):
+    """The high-trigger regime of the Qwen2.5-7B-shaped workload: a seeded low-rank change of the
+    LM head that makes about half of the steps have a top-1/top-2 margin below tau.
+
+    P seeded pairs of distinct token ids (a_k, b_k) and directions u_k ~ N(0, 1/d) give
+        W'_a = W_a + s u_k,    W'_b = c W_b + (1 - c) W_a + s u_k        (rank <= 2P).
+    Both rows of a pair gain the same logit s u_k . h, so with s = 8 one pair usually holds the
+    top two logits, and their gap becomes c (W_a - W_b) . h ~ N(0, 2 c^2 sigma^2), where
+    sigma = 0.02 sqrt(d) is the logit scale of an RMS-normalised h (||h||^2 = d).  The margin
+    is then |N(0, sqrt(2) c sigma)|, below tau with probability erf(tau / (2 c sigma));
+    c = tau / (0.954 sigma) makes that 1/2.  Returns a new weight list with the LM head
+    replaced (rows rounded to bf16); the other tensors are shared."""
+    d, V = shape.d_model, shape.vocab
+    sigma = 0.02 * float(np.sqrt(d))
+    c = tau / (0.954 * sigma)
+    g = torch.Generator()
+    g.manual_seed(seed)
+    ids = torch.randperm(V, generator=g)[: 2 * n_pairs]
+    a_ids, b_ids = ids[:n_pairs], ids[n_pairs:]
+    u = torch.randn((n_pairs, d), generator=g, dtype=torch.float32) / float(np.sqrt(d))
+    lm = weights[-1]
+    dev = lm.device
+    W = lm.clone()
+    wa = W[a_ids.to(dev)].view(torch.bfloat16).float()
+    wb = W[b_ids.to(dev)].view(torch.bfloat16).float()
+    su = (boost * u).to(dev)
+    na = wa + su
+    nb = c * wb + (1.0 - c) * wa + su
+    W[a_ids.to(dev)] = na.to(torch.bfloat16).view(torch.int16)
+    W[b_ids.to(dev)] = nb.to(torch.bfloat16).view(torch.int16)
+    return list(weights[:-1]) + [W]
+
+
+def fill_synthetic_kv(kv_view, pages, seed: int, std: float = 1.0):
+    """Seeded N(0, std) bf16 values in every layer, K and V, of the given pages of a paged KV
+    pool view [L][n_pages][2][Hkv][page][hd] (int16 tensor holding bf16 bits).  Stands in for
+    the cache of a long prompt where a prefill would take minutes; the parity tests copy the
+    cache to the oracle, so its contents need not come from a forward pass."""
+    dev = kv_view.device
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    idx = torch.as_tensor(np.asarray(pages, np.int64), device=dev)
+    shp = (idx.numel(),) + tuple(kv_view.shape[2:])
+    for layer in range(kv_view.shape[0]):
+        vals = torch.randn(shp, generator=g, device=dev, dtype=torch.float32)
+        vals.mul_(std)
+        kv_view[layer, idx] = vals.to(torch.bfloat16).view(torch.int16)
+        del vals

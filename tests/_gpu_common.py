@@ -48,3 +48,68 @@ def normwise(a, ref):
     a = np.asarray(a, np.float64)
     ref = np.asarray(ref, np.float64)
     return float(np.abs(a - ref).max() / np.abs(ref).max())
+
+
+def oracle_for_rows(shape, wn, eng, page_table, rows):
+    """State-forcing for full-size runs: an oracle that holds only the given batch rows, with
+    their KV pages copied from the GPU pool.  Returns (oracle, its page table [n][maxp]);
+    unmapped (-1) entries of the batch page table stay unmapped."""
+    sub = np.asarray(page_table, np.int32)[list(rows)]
+    valid = sub >= 0
+    n_pages = int(valid.sum())
+    ptl = np.full(sub.shape, -1, np.int32)
+    ptl[valid] = np.arange(n_pages, dtype=np.int32)
+    om = mgo.OracleModel(shape, wn, len(rows), sub.shape[1], max(n_pages, 1))
+    src = torch.as_tensor(sub[valid].astype(np.int64)).to(eng.kv_pool.device)
+    torch.cuda.synchronize()
+    om.kv_view()[:, :n_pages] = u16(eng.kv_view()[:, src])
+    return om, ptl
+
+
+
+def forced_step_check(shape, eng, page_table, pre_tok, pre_pos, sample, om, ptl, keep, emitted, tau,
+                      protected=None):
+    """State-forced parity of one gated step of a full-size run, on sampled batch rows.
+
+    `om`/`ptl` come from oracle_for_rows() on the PRE-step cache of `sample`; `pre_tok` /
+    `pre_pos` are the step's input tokens and positions, `keep` the step's kept outputs and
+    `emitted` the committed tokens.  The verifier attends to positions 0..p-1 plus its own
+    column, and a step writes only column p, so the GPU verifier can be re-run after the step on
+    the pre-step inputs.  Returns a dict of findings (the tests assert on it):
+      gate      the gate over the whole batch equals the oracle's (top1, margin bits, gate, rows)
+      err       worst normwise fast-vs-oracle(plain) logit error over `sample`
+      spread    worst normwise canonical-vs-plain spread of the oracle on the same rows
+      verifier  GPU verifier logits / tokens / K-V columns of `sample` bit-equal to the oracle's
+      commit    gated sampled rows emit the verifier token and, on a repair, hold its column;
+                the others emit top-1 with margin >= tau"""
+    sample = list(sample)
+    n = len(sample)
+    ref = om.decode_step(mgo.PLAIN, pre_tok[sample], pre_pos[sample], ptl)
+    vl, vt, vc = om.verify_rows(np.arange(n, dtype=np.int32), pre_tok[sample], pre_pos[sample], ptl)
+    rt, rm, rg, rr = mgo.OracleModel.margin_gate(keep["logits"], protected, tau)
+    gate = (np.array_equal(keep["top1"], rt) and np.array_equal(keep["margin"].view(np.uint32), rm.view(np.uint32))
+            and np.array_equal(keep["gate"], rg) and np.array_equal(keep["rows"], rr))
+    spread = max(normwise(vl[k], ref[k]) for k in range(n))
+    err = max(normwise(keep["logits"][r], ref[k]) for k, r in enumerate(sample))
+    gl = torch.empty((n, shape.vocab), dtype=torch.float32, device="cuda")
+    gt = torch.empty(n, dtype=torch.int32, device="cuda")
+    gc = torch.empty((n, eng.col_elems), dtype=torch.int16, device="cuda")
+    eng.verify_rows(n, dev_i32(sample), None, dev_i32(pre_tok), dev_i32(pre_pos), dev_i32(page_table), gl, gt, gc)
+    torch.cuda.synchronize()
+    verifier = (np.array_equal(gl.cpu().numpy().view(np.uint32), vl.view(np.uint32))
+                and np.array_equal(gt.cpu().numpy(), vt) and np.array_equal(u16(gc), vc))
+    gated = {int(r): i for i, r in enumerate(keep["rows"])}
+    kv = eng.kv_view()
+    commit, repaired = True, 0
+    for k, r in enumerate(sample):
+        if r in gated:
+            commit &= int(keep["v_tok"][gated[r]]) == int(vt[k]) and int(emitted[r]) == int(vt[k])
+            if vt[k] != rt[r]:
+                p = int(pre_pos[r])
+                col = u16(kv[:, int(page_table[r][p // shape.page_size]), :, :, p % shape.page_size, :])
+                commit &= np.array_equal(col.reshape(-1), vc[k].reshape(-1))
+                repaired += 1
+        else:
+            commit &= int(emitted[r]) == int(rt[r]) and float(keep["margin"][r]) >= tau
+    return dict(gate=gate, err=err, spread=spread, verifier=verifier, commit=commit,
+                gated_in_sample=sum(r in gated for r in sample), repaired=repaired, n_gated=len(keep["rows"]))
