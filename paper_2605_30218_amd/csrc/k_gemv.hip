@@ -17,6 +17,11 @@
 // (one buffer keeps the LDS footprint at R * 2 KiB, so more blocks fit per CU).  No
 // split-K, no atomics: a row's arithmetic is the same whatever R, J, the tile or the
 // count.
+// Row tiles: when the host knows the row count (up to 24 rows) one tile of exactly
+// ceil(n/4)*4 rows runs every row without a branch, which lets the compiler read later
+// rows' activations from LDS while earlier rows compute (the dead rows compute on a copy
+// of the last live row and are not written); other counts use 16-row tiles that skip
+// dead rows by a uniform branch.  The tile never changes a row's arithmetic.
 // Block order: the row tiles of one feature block get consecutive slots on the
 // same XCD (blocks are dealt to the 8 XCDs round-robin), so they share its L2
 // copy of the weights.
@@ -33,10 +38,15 @@ constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
 #ifndef MG_GEMV_J_R16
 #define MG_GEMV_J_R16 2
 #endif
+#ifndef MG_GEMV_EXACT_MAX
+#define MG_GEMV_EXACT_MAX 24  // largest host row count served by one branch-free tile
+#endif
 #ifndef MG_GEMV_NW
 #define MG_GEMV_NW 8  // waves per block (measured: 8 beats 4 and 16)
 #endif
 constexpr int GV_NW = MG_GEMV_NW, GV_THREADS = 64 * MG_GEMV_NW;
+
+__host__ __device__ constexpr int pow2_at_least(int v) { return v <= 1 ? 1 : 2 * pow2_at_least((v + 1) / 2); }
 
 template <int R>
 struct GemvShape {
@@ -78,7 +88,7 @@ __device__ __forceinline__ void gemv_load_w(const uint16_t* const (&wrow)[J], in
 }
 
 // this lane's group of one chunk for every live row: sequential fma in element order
-template <int J, int R>
+template <int J, int R, bool EXACT>
 __device__ __forceinline__ void gemv_fma_chunk(const float4 (*xb)[2][64], int lane, int nr, const uint4 (&wv)[J],
                                                float (&acc)[J][R]) {
     float w[J][8];
@@ -88,11 +98,13 @@ __device__ __forceinline__ void gemv_fma_chunk(const float4 (*xb)[2][64], int la
         w[jj][0] = bf_lo(v.x); w[jj][1] = bf_hi(v.x); w[jj][2] = bf_lo(v.y); w[jj][3] = bf_hi(v.y);
         w[jj][4] = bf_lo(v.z); w[jj][5] = bf_hi(v.z); w[jj][6] = bf_lo(v.w); w[jj][7] = bf_hi(v.w);
     }
-    // rows past nr are skipped by a uniform branch; the loop stays fully unrolled so
-    // every accumulator index is a compile-time constant (no scratch)
+    // EXACT tiles (sized by the host to the row count) run every row with no branch, so
+    // the compiler reads later rows' activations from LDS while earlier rows compute;
+    // otherwise rows past nr are skipped by a uniform branch.  The loop stays fully
+    // unrolled so every accumulator index is a compile-time constant (no scratch).
 #pragma unroll
     for (int rr = 0; rr < R; ++rr) {
-        if (rr < nr) {
+        if (EXACT || rr < nr) {
             const float4 x0 = xb[rr][0][lane], x1 = xb[rr][1][lane];
 #pragma unroll
             for (int jj = 0; jj < J; ++jj) {
@@ -111,7 +123,7 @@ __device__ __forceinline__ void gemv_fma_chunk(const float4 (*xb)[2][64], int la
     }
 }
 
-template <int J, int R, int EPI>
+template <int J, int R, int EPI, bool EXACT>
 __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int n_fb, int n_rt) {
     const int b = blockIdx.x;
     const int xcd = b & 7, slot = b >> 3;
@@ -162,7 +174,7 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
         gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, xr);
         gemv_load_w<J>(wrow, (c + 1) * 64 + lane, G, nxt);
         __builtin_amdgcn_sched_barrier(0);
-        if (c * 64 + lane < G) gemv_fma_chunk<J, R>(xs, lane, nr, cur, acc);
+        if (c * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs, lane, nr, cur, acc);
         __syncthreads();
         gemv_store_x<R>(xs, xr);
         __syncthreads();
@@ -174,22 +186,23 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
     }
     if (c + 1 < nch) {
         step(c, wA, wB);
-        if ((c + 1) * 64 + lane < G) gemv_fma_chunk<J, R>(xs, lane, nr, wB, acc);
+        if ((c + 1) * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs, lane, nr, wB, acc);
     } else if (c * 64 + lane < G) {
-        gemv_fma_chunk<J, R>(xs, lane, nr, wA, acc);
+        gemv_fma_chunk<J, R, EXACT>(xs, lane, nr, wA, acc);
     }
 
-    // all J*R butterflies at once; value jj*R + rr ends in the lanes multi_index names
-    float flat[J * R];
+    // all J*R butterflies at once (padded to a power of two; each value is summed over the
+    // lanes on its own, so the padding never mixes in); value jj*R + rr ends in the lanes
+    // multi_index names
+    constexpr int NV = pow2_at_least(J * R);
+    float flat[NV];
 #pragma unroll
-    for (int jj = 0; jj < J; ++jj)
-#pragma unroll
-        for (int rr = 0; rr < R; ++rr) flat[jj * R + rr] = acc[jj][rr];
-    const float v = butterfly_sum_multi<J * R>(flat, lane);
+    for (int k = 0; k < NV; ++k) flat[k] = k < J * R ? acc[k / R][k % R] : 0.0f;
+    const float v = butterfly_sum_multi<NV>(flat, lane);
     bool writer;
-    const int idx = multi_index<J * R>(lane, &writer);
+    const int idx = multi_index<NV>(lane, &writer);
     const int jj = idx / R, rr = idx % R;
-    bool ok = writer && rr < nr;
+    bool ok = writer && idx < J * R && rr < nr;
 #pragma unroll
     for (int k = 0; k < J; ++k)
         if (k == jj) ok = ok && valid[k];
@@ -209,24 +222,38 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
     }
 }
 
-template <int J, int R>
+template <int J, int R, bool EXACT>
 static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s) {
     const int n_fb = (a.N + GV_NW * J - 1) / (GV_NW * J);
     const int n_rt = (rows + R - 1) / R;
     const dim3 grid(8 * ((n_fb + 7) / 8) * n_rt);
     switch (epi) {
-        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
-        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
-        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
     }
     return hipGetLastError();
 }
 
+// A host row count up to 24 gets one tile of exactly ceil(n/4)*4 rows (branch-free rows,
+// at most three of them dead); larger counts and device-side counts use 16-row tiles
+// (8-row when at most 8 rows can occur) that skip dead rows by a uniform branch.
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
-    if (rows > 8) return launch_jr<MG_GEMV_J_R16, 16>(a, epi, rows, s);
-    return launch_jr<MG_GEMV_J_R8, 8>(a, epi, rows, s);
+    if (!a.n_dev && rows <= MG_GEMV_EXACT_MAX) {
+        switch ((rows + 3) / 4) {
+            case 1: return launch_jr<MG_GEMV_J_R8, 4, true>(a, epi, rows, s);
+            case 2: return launch_jr<MG_GEMV_J_R8, 8, true>(a, epi, rows, s);
+            case 3: return launch_jr<MG_GEMV_J_R16, 12, true>(a, epi, rows, s);
+            case 4: return launch_jr<MG_GEMV_J_R16, 16, true>(a, epi, rows, s);
+            case 5: return launch_jr<MG_GEMV_J_R16, 20, true>(a, epi, rows, s);
+            default: return launch_jr<MG_GEMV_J_R16, 24, true>(a, epi, rows, s);
+        }
+    }
+    if (!a.n_dev && rows % 16 == 0) return launch_jr<MG_GEMV_J_R16, 16, true>(a, epi, rows, s);
+    if (rows > 8) return launch_jr<MG_GEMV_J_R16, 16, false>(a, epi, rows, s);
+    return launch_jr<MG_GEMV_J_R8, 8, false>(a, epi, rows, s);
 }
 
 }  // namespace mg
