@@ -30,13 +30,17 @@ namespace mg {
 typedef __bf16 bf16x8_ft __attribute__((ext_vector_type(8)));
 typedef float f32x4_ft __attribute__((ext_vector_type(4)));
 
-constexpr int FA_WAVES = 4;
+#ifndef MG_FA_WAVES
+#define MG_FA_WAVES 4
+#endif
+constexpr int FA_WAVES = MG_FA_WAVES;
+constexpr int FA_THREADS = 64 * FA_WAVES;
 constexpr int FA_PGCAP = 1024;  // page indices held in LDS (positions < 16384); more are read from memory
 
 __device__ __forceinline__ float fa_scale(int hd) { return hd == 128 ? 0x1.6a09e6p-4f : 0x1.0p-3f; }
 
 template <int HD, int GP>
-__global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
+__global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArgs a) {
     constexpr int DG = HD / 8;    // 16-byte d-groups per row
     constexpr int PPI = 64 / DG;  // positions per V load instruction
     constexpr int VL = 16 / PPI;  // V loads per lane per page step
@@ -68,7 +72,7 @@ __global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
         const float* pp = a.part + (size_t)r * N;
         const size_t sstride = (size_t)a.B * N;
         const int nf = (G + 2) * HD;
-        for (int q4 = t; q4 < nf / 4; q4 += 256) {
+        for (int q4 = t; q4 < nf / 4; q4 += FA_THREADS) {
             const int f = 4 * q4;
             int n, nb;
             const uint16_t* b;
@@ -96,8 +100,8 @@ __global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
             y[f + 3] = bf2f(f2bf(v.w));
         }
         if (pg_lds)
-            for (int j = t; j < npg; j += 256) pgs[j] = ptab[j];
-        for (int e = G * HD + t; e < GP * HD; e += 256) qb[e] = 0;
+            for (int j = t; j < npg; j += FA_THREADS) pgs[j] = ptab[j];
+        for (int e = G * HD + t; e < GP * HD; e += FA_THREADS) qb[e] = 0;
     }
     __syncthreads();
     // ---- RoPE on q and k, tentative K/V append at p, q' / k'_p / v_p into LDS
@@ -106,7 +110,7 @@ __global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
         uint16_t* kdst = a.kv_pool + ((((size_t)a.layer * m.n_pages + ptab[p / 16]) * 2) * m.Hkv + kh) * (size_t)16 * HD +
                          (size_t)(p % 16) * HD;
         uint16_t* vdst = kdst + (size_t)m.Hkv * 16 * HD;
-        for (int t2 = t; t2 < (G + 1) * H2; t2 += 256) {
+        for (int t2 = t; t2 < (G + 1) * H2; t2 += FA_THREADS) {
             const int head = t2 / H2, ii = t2 % H2;  // head == G: the k head
             const float* s = y + head * HD;
             const float x1 = s[ii], x2 = s[ii + H2];
@@ -123,7 +127,7 @@ __global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
                 kps[ii + H2] = bf2f(o2);
             }
         }
-        for (int d = t; d < HD; d += 256) {
+        for (int d = t; d < HD; d += FA_THREADS) {
             const float v = y[(G + 1) * HD + d];
             vdst[d] = (uint16_t)f2bf(v);
             vps[d] = v;
@@ -262,7 +266,7 @@ __global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
     __syncthreads();
 
     // ---- merge the wave partials and position p
-    for (int oi = t; oi < G * HD; oi += 256) {
+    for (int oi = t; oi < G * HD; oi += FA_THREADS) {
         const int h = oi / HD, d = oi % HD;
         float M = sp[h];
 #pragma unroll
@@ -282,10 +286,10 @@ __global__ __launch_bounds__(256) void attn_fast_fused_kernel(FastAttnArgs a) {
 template <int HD>
 static void launch_hd(const FastAttnArgs& a, int gp, dim3 grid, hipStream_t s) {
     switch (gp) {
-        case 1: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 1>), grid, dim3(256), 0, s, a); break;
-        case 2: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 2>), grid, dim3(256), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 4>), grid, dim3(256), 0, s, a); break;
-        default: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 8>), grid, dim3(256), 0, s, a); break;
+        case 1: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 1>), grid, dim3(FA_THREADS), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 2>), grid, dim3(FA_THREADS), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 4>), grid, dim3(FA_THREADS), 0, s, a); break;
+        default: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 8>), grid, dim3(FA_THREADS), 0, s, a); break;
     }
 }
 
