@@ -29,7 +29,7 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2605_30218_amd import mg, profsum, synth  # noqa: E402
+from paper_2605_30218_amd import calibrate, mg, profsum, synth  # noqa: E402
 from paper_2605_30218_amd.runtime import GatedDecoder, prefill_fast, prefill_rows  # noqa: E402
 
 METRIC = "decode tok/s + gated-vs-always-on verifier overhead, Llama-3.1-8B-shape bs=64"
@@ -144,6 +144,9 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=4)
     ap.add_argument("--cpu-steps", type=int, default=2)
     ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--pareto-steps", type=int, default=None,
+                    help="steps of the tau calibration recipe (reference decode, eps_pert, sweep; default --steps, "
+                         "0 = skip)")
     ap.add_argument("--profile-steps", type=int, default=32,
                     help="timed gated steps (from the first) whose kernel launches are bracketed by HIP events")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -193,6 +196,15 @@ def main():
                                                               PAPER_TRIGGER)
     dec.tau = tau
     log(f"[bench] tau = {tau:.5f}")
+    # the paper's threshold recipe (Sec. 3.1, Appendix A): eps_pert against the deterministic
+    # reference, a sweep over 2 max(eps) x {1/8 .. 4}, tau_100
+    pareto_steps = args.steps if args.pareto_steps is None else args.pareto_steps
+    calib = None
+    if pareto_steps > 0:
+        log(f"[bench] tau calibration recipe over {pareto_steps} steps")
+        calib = calibrate.calibrate(dec, state, kv_snap, pareto_steps)
+        dec.tau = tau
+        log(f"[bench] eps median {calib['eps_median']:.4f} max {calib['eps_max']:.4f}, tau_100 {calib['tau_100']}")
     modes = {}
     for mode in args.modes.split(","):
         steps = always_steps if mode == "always" else args.steps
@@ -244,6 +256,8 @@ def main():
                                     f"prompts, gated greedy decode (all rows protected, tau for an 18.56% trigger)",
                            global_batch=B, seq_len=P, parallelism="single GPU"),
                roofline=roofline, tau=tau, prefill=args.prefill, prefill_s=prefill_s, modes=modes, kernels=kernels)
+    if calib is not None:
+        out["calibration"] = calib
     if "off" in modes:
         t_off = modes["off"]["ms_per_step"]
         ov = {}

@@ -1,0 +1,78 @@
+"""The tau calibration recipe (Sec. 3.1 threshold setting, Appendix A) on the tiny decoder (GPU).
+
+  reference decode   the deterministic reference (verifier on every row, its column always
+                     kept) equals the oracle's canonical greedy decode token for token, with a
+                     bit-identical cache, and a row decoded alone equals the same row in the batch
+  recipe             eps statistics, a frontier point per tau, tau_100 the smallest fully
+                     deterministic tau of the grid"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2605_30218_amd import calibrate, synth
+from paper_2605_30218_amd.runtime import GatedDecoder
+
+from _gpu_common import Pair, u16
+
+pytestmark = pytest.mark.gpu
+S = synth.TINY
+STEPS = 24
+
+
+@pytest.fixture(scope="module")
+def pair():
+    return Pair(S, max_batch=8, ctx_cap=96)
+
+
+@pytest.fixture(scope="module")
+def prompts():
+    return synth.make_prompts(4, [32, 20, 32, 9], S.vocab, seed=1)
+
+
+def fresh(pair, prompts):
+    pair.eng.kv_pool.zero_()
+    pair.om.kv_pool[:] = 0
+    return pair.prefill(prompts)
+
+
+def test_reference_decode_is_the_oracle_canonical_greedy_decode(pair, prompts):
+    last, pos0 = fresh(pair, prompts)
+    dec = GatedDecoder(pair.eng, pair.pt[:4], None, tau=0.0)
+    dec.set_state(last, pos0)
+    got = calibrate.reference_decode(dec, STEPS)
+    torch.cuda.synchronize()
+    rows = np.arange(4, dtype=np.int32)
+    tok, pos = last.copy(), pos0.copy()
+    never = np.full(4, -1, np.int32)
+    for s in range(STEPS):
+        _, vt, vc = pair.om.verify_rows(rows, tok, pos, pair.pt[:4], want_logits=False)
+        emitted, _ = pair.om.repair(rows, pos, pair.pt[:4], never, vt, vc, never)
+        np.testing.assert_array_equal(got[:, s], emitted, err_msg=f"step {s}")
+        tok, pos = emitted, pos + 1
+    np.testing.assert_array_equal(u16(pair.eng.kv_pool), pair.om.kv_pool)
+
+
+def test_reference_decode_is_batch_invariant(pair, prompts):
+    last, pos0 = fresh(pair, prompts)
+    dec = GatedDecoder(pair.eng, pair.pt[:4], None, tau=0.0)
+    dec.set_state(last, pos0)
+    batch = calibrate.reference_decode(dec, STEPS)
+    last, pos0 = fresh(pair, prompts)
+    one = GatedDecoder(pair.eng, pair.pt[2:3], None, tau=0.0)
+    one.set_state(last[2:3], pos0[2:3])
+    alone = calibrate.reference_decode(one, STEPS)
+    np.testing.assert_array_equal(alone[0], batch[2])
+
+
+def test_calibration_recipe(pair, prompts):
+    last, pos0 = fresh(pair, prompts)
+    snap = pair.eng.kv_pool.clone()
+    dec = GatedDecoder(pair.eng, pair.pt[:4], None, tau=0.0)
+    res = calibrate.calibrate(dec, (last, pos0), snap, STEPS)
+    print(res)
+    assert 0.0 <= res["eps_median"] <= res["eps_max"] and res["pert_tau"] == pytest.approx(2 * res["eps_max"])
+    assert len(res["frontier"]) == 6
+    for f in res["frontier"]:
+        assert 0.0 <= f["r_verify"] <= 1.0 and 0.0 <= f["seq_det"] <= 1.0
+    det = [f["tau"] for f in res["frontier"] if f["seq_det"] == 1.0]
+    assert res["tau_100"] == (min(det) if det else None)

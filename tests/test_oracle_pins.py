@@ -531,3 +531,4 @@ def test_gated_loop_canonical_fast_path_never_repairs():
         assert rec["n_repaired"] == 0
         np.testing.assert_array_equal(emitted, rec["top1"])
         toks, pos = emitted, pos + 1
+
