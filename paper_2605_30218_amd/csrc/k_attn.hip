@@ -31,9 +31,9 @@ __device__ __forceinline__ float attn_scale(int hd) { return hd == 128 ? 0x1.6a0
 // batches, so their loads are in flight together.
 //   scores  thread j: s_j for each query head of the group, sequential fma over d, * scale
 //   chunk   wave w: heads w, w + 4: m = max_j s_j, e_j = EXP(s_j - m) in place
-//   l       thread h < G: sequential sum of e_j in position order
 //   values  thread t: d pair (2 dp, 2 dp + 1) of the heads hg, hg + 256 / (hd/2), ...:
-//           a[d] = sequential fma over j of e_j v_jd
+//           a[d] = sequential fma over j of e_j v_jd, and in the same loop
+//           l = sequential sum of e_j in position order
 template <int HD>
 __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     constexpr int U4 = HD / 8;                // 16-byte pieces per K/V row
@@ -47,7 +47,7 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint32_t vs[ATT_MAXC * HP];
     __shared__ __attribute__((aligned(16))) float qs[ATT_MAXG * HD];
     __shared__ __attribute__((aligned(16))) float ps[ATT_MAXG * ATT_MAXC];
-    __shared__ float red[ATT_MAXG][2];
+    __shared__ float red[ATT_MAXG][1];
     __shared__ const uint16_t* pgk[NPG];
 
     const int i = blockIdx.z;
@@ -150,25 +150,15 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     }
     __syncthreads();
 
-    // ---- l (sequential in position order) and the weighted values
+    // ---- the weighted values, with l (the sequential sum of e_j in position order) carried
+    // along in the same loop: every thread of head h forms the same l, the d-pair-0 thread
+    // stores it
     const int nb = nj / UB * UB;  // positions handled in whole batches
-    if (t < G) {
-        const float* ph = ps + t * ATT_MAXC;
-        float l = 0.0f;
-        for (int j = 0; j < nb; j += UB) {
-            const float4 e0 = *reinterpret_cast<const float4*>(ph + j);
-            const float4 e1 = *reinterpret_cast<const float4*>(ph + j + 4);
-            l = l + e0.x; l = l + e0.y; l = l + e0.z; l = l + e0.w;
-            l = l + e1.x; l = l + e1.y; l = l + e1.z; l = l + e1.w;
-        }
-        for (int j = nb; j < nj; ++j) l = l + ph[j];
-        red[t][1] = l;
-    }
     const int dp = t % HP, hg = t / HP;
     constexpr int NH = (ATT_MAXG + HPT - 1) / HPT;  // heads per thread
-    float acc[NH][2];
+    float acc[NH][2], lsum[NH];
 #pragma unroll
-    for (int u = 0; u < NH; ++u) acc[u][0] = acc[u][1] = 0.0f;
+    for (int u = 0; u < NH; ++u) acc[u][0] = acc[u][1] = lsum[u] = 0.0f;
     for (int j = 0; j < nb; j += UB) {
         uint32_t vw[UB];
 #pragma unroll
@@ -182,6 +172,7 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
                 const float e[UB] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
 #pragma unroll
                 for (int b = 0; b < UB; ++b) {
+                    lsum[u] = lsum[u] + e[b];
                     acc[u][0] = __builtin_fmaf(e[b], bf_lo(vw[b]), acc[u][0]);
                     acc[u][1] = __builtin_fmaf(e[b], bf_hi(vw[b]), acc[u][1]);
                 }
@@ -195,12 +186,12 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
             const int h = hg + HPT * u;
             if (h < G) {
                 const float e = ps[h * ATT_MAXC + j];
+                lsum[u] = lsum[u] + e;
                 acc[u][0] = __builtin_fmaf(e, bf_lo(vw), acc[u][0]);
                 acc[u][1] = __builtin_fmaf(e, bf_hi(vw), acc[u][1]);
             }
         }
     }
-    __syncthreads();
     constexpr int stride = HD + 2;
 #pragma unroll
     for (int u = 0; u < NH; ++u) {
@@ -209,7 +200,7 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
             float* dst = a.part + (((size_t)i * m.Hq + kh * G + h) * a.max_chunks + c) * stride;
             if (dp == 0) {
                 dst[0] = red[h][0];
-                dst[1] = red[h][1];
+                dst[1] = lsum[u];
             }
             dst[2 + 2 * dp] = acc[u][0];
             dst[3 + 2 * dp] = acc[u][1];

@@ -137,9 +137,9 @@ def read_traffic(path: str):
     sha = per = None
     for line in open(path):
         if line.startswith("source sha256[:16]:"):
-            sha = line.split(":", 1)[1].strip()
+            sha = line[len("source sha256[:16]:"):].strip()
         if line.startswith("traffic_bytes_per_launch:"):
-            per = float(line.split(":", 1)[1])
+            per = float(line[len("traffic_bytes_per_launch:"):])
     return (per, sha) if per is not None and sha else None
 
 
