@@ -34,7 +34,7 @@ __device__ __forceinline__ float attn_scale(int hd) { return hd == 128 ? 0x1.6a0
 //   values  thread t: d pair (2 dp, 2 dp + 1) of the heads hg, hg + 256 / (hd/2), ...:
 //           a[d] = sequential fma over j of e_j v_jd, and in the same loop
 //           l = sequential sum of e_j in position order
-template <int HD>
+template <int HD, int GP>  // GP: query heads per KV head, 1..8
 __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     constexpr int U4 = HD / 8;                // 16-byte pieces per K/V row
     constexpr int NLD = ATT_MAXC * U4 / 256;  // V pieces per thread
@@ -45,10 +45,9 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     static_assert(NLD * 256 == ATT_MAXC * U4, "pieces must divide evenly");
 
     __shared__ __attribute__((aligned(16))) uint32_t vs[ATT_MAXC * HP];
-    __shared__ __attribute__((aligned(16))) float qs[ATT_MAXG * HD];
-    __shared__ __attribute__((aligned(16))) float ps[ATT_MAXG * ATT_MAXC];
-    __shared__ float red[ATT_MAXG][1];
-    __shared__ const uint16_t* pgk[NPG];
+    __shared__ __attribute__((aligned(16))) float qs[GP * HD];
+    __shared__ __attribute__((aligned(16))) float ps[GP * ATT_MAXC];
+    __shared__ float red[GP][1];
 
     const int i = blockIdx.z;
     if (i >= items_n(a.it)) return;
@@ -58,42 +57,58 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     if (j0 > p) return;
     const int nj = min(ATT_MAXC, p + 1 - j0);
     const ModelDims& m = a.m;
-    const int G = m.Hq / m.Hkv, Nk = m.Hkv * HD;
+    constexpr int G = GP;  // query heads per KV head (a template parameter, so the head loops have no branch)
+    const int Nk = m.Hkv * HD;
     const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
     const size_t kv_stride = (size_t)m.Hkv * m.page_size * HD;  // K -> V of the same page
 
-    // K base of each page of the chunk (page_size is 16)
-    if (t < NPG) {
-        const int jp = j0 + 16 * t;
-        pgk[t] = jp <= p ? a.kv_pool + ((((size_t)a.layer * m.n_pages + a.it.page_table[(size_t)r * m.max_pages_per_row +
-                                                                                           jp / 16]) * 2) * m.Hkv + kh) *
-                                           (size_t)m.page_size * HD
-                         : nullptr;
-    }
+    // page indices of the chunk (uniform, so read through the scalar cache together with the
+    // queries); entries past the current position's page are clamped to it (always mapped)
+    const int32_t* ptab = a.it.page_table + (size_t)r * m.max_pages_per_row;
+    int pgs[NPG];
+#pragma unroll
+    for (int k = 0; k < NPG; ++k) pgs[k] = ptab[min(j0 / 16 + k, p >> 4)];
+    // the group's rotated queries: one 16-byte load per thread
+    static_assert(GP * HD <= 8 * 256, "one 16-byte load per thread covers the group's queries");
     const uint16_t* qrow = a.qrot + (size_t)i * m.Hq * HD + (size_t)kh * G * HD;
-    for (int e = t; e < G * HD; e += 256) qs[e] = bf2f(qrow[e]);
+    if (t < G * HD / 8) {
+        const uint4 qv = *reinterpret_cast<const uint4*>(qrow + 8 * t);
+        float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
+        qd[0] = make_float4(bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y));
+        qd[1] = make_float4(bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w));
+    }
     const uint16_t* own = a.own_col ? a.own_col + ((size_t)i * m.L + a.layer) * 2 * Nk + (size_t)kh * HD : nullptr;
-    __syncthreads();
-
-    auto row_ptr = [&](int jj) -> const uint16_t* {  // K row of chunk position jj < nj
-        if (own && j0 + jj == p) return own;
-        return pgk[jj >> 4] + (size_t)(jj & 15) * HD;
+    // K block of page pg for this KV head
+    auto page_k = [&](int pg) -> const uint16_t* {
+        return a.kv_pool + ((((size_t)a.layer * m.n_pages + pg) * 2) * m.Hkv + kh) * (size_t)m.page_size * HD;
     };
+
+    // K row of position t and the V pieces of positions < nj (the only bytes the chunk needs:
+    // every block loads at once, so the load phase streams the whole launch's K/V); the
+    // verifier's own column stands in for the cache's tentative column p
     uint4 kr[U4], vr[NLD];
     if (t < nj) {
-        const uint4* kp = reinterpret_cast<const uint4*>(row_ptr(t));
+        int pg = pgs[0];
+#pragma unroll
+        for (int k = 1; k < NPG; ++k) pg = (t >> 4) == k ? pgs[k] : pg;
+        const uint4* kp = reinterpret_cast<const uint4*>((own && j0 + t == p) ? own : page_k(pg) + (size_t)(t & 15) * HD);
 #pragma unroll
         for (int k = 0; k < U4; ++k) kr[k] = kp[k];
     }
+    // V: iteration k covers positions PPI*k .. PPI*k + PPI-1, i.e. PPI/16 pages
+    constexpr int PPI = 256 / U4, PGI = PPI / 16;
+    const int sub = (t / U4) >> 4;
+    const size_t voff = kv_stride + (size_t)((t / U4) & 15) * HD + (size_t)(t % U4) * 8;
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
-        const int e = t + 256 * k;
-        const int jj = e / U4, pc = e % U4;
+        const int jj = t / U4 + PPI * k;
         vr[k] = make_uint4(0, 0, 0, 0);
         if (jj < nj) {
-            const uint16_t* kp = row_ptr(jj);
-            const uint16_t* vp = (own && j0 + jj == p) ? own + Nk : kp + kv_stride;
-            vr[k] = *reinterpret_cast<const uint4*>(vp + pc * 8);
+            int pg = pgs[PGI * k];
+#pragma unroll
+            for (int q2 = 1; q2 < PGI; ++q2) pg = sub == q2 ? pgs[PGI * k + q2] : pg;
+            const uint16_t* vp = (own && j0 + jj == p) ? own + Nk + (size_t)(t % U4) * 8 : page_k(pg) + voff;
+            vr[k] = *reinterpret_cast<const uint4*>(vp);
         }
     }
 #pragma unroll
@@ -101,20 +116,21 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
         const int e = t + 256 * k;
         *reinterpret_cast<uint4*>(vs + (e / U4) * HP + (e % U4) * 4) = vr[k];
     }
+    __syncthreads();
 
     // ---- scores: position t, all heads of the group at once (K in registers)
     const float scale = attn_scale(HD);
     if (t < nj) {
-        float sc[ATT_MAXG];
+        float sc[GP];
 #pragma unroll
-        for (int h = 0; h < ATT_MAXG; ++h) sc[h] = 0.0f;
+        for (int h = 0; h < GP; ++h) sc[h] = 0.0f;
 #pragma unroll
         for (int k = 0; k < U4; ++k) {
             const float kf[8] = {bf_lo(kr[k].x), bf_hi(kr[k].x), bf_lo(kr[k].y), bf_hi(kr[k].y),
                                  bf_lo(kr[k].z), bf_hi(kr[k].z), bf_lo(kr[k].w), bf_hi(kr[k].w)};
 #pragma unroll
-            for (int h = 0; h < ATT_MAXG; ++h) {
-                if (h < G) {
+            for (int h = 0; h < GP; ++h) {
+                {
                     const float4 q0 = *reinterpret_cast<const float4*>(qs + h * HD + 8 * k);
                     const float4 q1 = *reinterpret_cast<const float4*>(qs + h * HD + 8 * k + 4);
                     float s = sc[h];
@@ -131,8 +147,7 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
             }
         }
 #pragma unroll
-        for (int h = 0; h < ATT_MAXG; ++h)
-            if (h < G) ps[h * ATT_MAXC + t] = sc[h] * scale;
+        for (int h = 0; h < GP; ++h) ps[h * ATT_MAXC + t] = sc[h] * scale;
     }
     __syncthreads();
 
@@ -155,7 +170,7 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     // stores it
     const int nb = nj / UB * UB;  // positions handled in whole batches
     const int dp = t % HP, hg = t / HP;
-    constexpr int NH = (ATT_MAXG + HPT - 1) / HPT;  // heads per thread
+    constexpr int NH = (GP + HPT - 1) / HPT;  // heads per thread
     float acc[NH][2], lsum[NH];
 #pragma unroll
     for (int u = 0; u < NH; ++u) acc[u][0] = acc[u][1] = lsum[u] = 0.0f;
@@ -254,15 +269,31 @@ __global__ void attn_combine_kernel(AttnArgs a) {
     a.out[(size_t)i * a.m.Hq * hd + (size_t)h * hd + d] = (uint16_t)f2bf(ieee_div(O, L));
 }
 
+template <int HD>
+static void launch_canon_g(const AttnArgs& a, int G, dim3 g1, hipStream_t s) {
+    switch (G) {
+        case 1: hipLaunchKernelGGL((attn_canon_kernel<HD, 1>), g1, dim3(256), 0, s, a); break;
+        case 2: hipLaunchKernelGGL((attn_canon_kernel<HD, 2>), g1, dim3(256), 0, s, a); break;
+        case 3: hipLaunchKernelGGL((attn_canon_kernel<HD, 3>), g1, dim3(256), 0, s, a); break;
+        case 4: hipLaunchKernelGGL((attn_canon_kernel<HD, 4>), g1, dim3(256), 0, s, a); break;
+        case 5: hipLaunchKernelGGL((attn_canon_kernel<HD, 5>), g1, dim3(256), 0, s, a); break;
+        case 6: hipLaunchKernelGGL((attn_canon_kernel<HD, 6>), g1, dim3(256), 0, s, a); break;
+        case 7: hipLaunchKernelGGL((attn_canon_kernel<HD, 7>), g1, dim3(256), 0, s, a); break;
+        default: hipLaunchKernelGGL((attn_canon_kernel<HD, 8>), g1, dim3(256), 0, s, a); break;
+    }
+}
+
 hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s) {
     const int n = a.it.n_host;
     if (n <= 0) return hipSuccess;
     if (!canon || a.chunk != ATT_MAXC) return hipErrorInvalidValue;  // the fast path has its own kernel
     dim3 g1(a.max_chunks, a.m.Hkv, n), g2(a.m.Hq, n);
+    const int G = a.m.Hq / a.m.Hkv;
+    if (G < 1 || G > ATT_MAXG) return hipErrorInvalidValue;
     if (a.m.hd == 128)
-        hipLaunchKernelGGL(attn_canon_kernel<128>, g1, dim3(256), 0, s, a);
+        launch_canon_g<128>(a, G, g1, s);
     else
-        hipLaunchKernelGGL(attn_canon_kernel<64>, g1, dim3(256), 0, s, a);
+        launch_canon_g<64>(a, G, g1, s);
     hipLaunchKernelGGL(attn_combine_kernel, g2, dim3(a.m.hd), 0, s, a);
     return hipGetLastError();
 }
