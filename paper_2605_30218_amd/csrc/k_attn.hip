@@ -45,7 +45,7 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     static_assert(NLD * 256 == ATT_MAXC * U4, "pieces must divide evenly");
 
     __shared__ __attribute__((aligned(16))) uint32_t vs[ATT_MAXC * HP];
-    __shared__ __attribute__((aligned(16))) float qs[GP * HD];
+    __shared__ __attribute__((aligned(16))) float qs[8 * 256];  // the group's queries, then padding
     __shared__ __attribute__((aligned(16))) float ps[GP * ATT_MAXC];
     __shared__ float red[GP][1];
 
@@ -68,57 +68,63 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     int pgs[NPG];
 #pragma unroll
     for (int k = 0; k < NPG; ++k) pgs[k] = ptab[min(j0 / 16 + k, p >> 4)];
-    // the group's rotated queries: one 16-byte load per thread
+    // the group's rotated queries: one 16-byte load per thread (threads past the group's
+    // 8-element pieces re-read the last piece and stage it into an unused part of qs)
     static_assert(GP * HD <= 8 * 256, "one 16-byte load per thread covers the group's queries");
     const uint16_t* qrow = a.qrot + (size_t)i * m.Hq * HD + (size_t)kh * G * HD;
-    if (t < G * HD / 8) {
-        const uint4 qv = *reinterpret_cast<const uint4*>(qrow + 8 * t);
-        float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
-        qd[0] = make_float4(bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y));
-        qd[1] = make_float4(bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w));
-    }
+    const uint4 qv = *reinterpret_cast<const uint4*>(qrow + 8 * min(t, G * HD / 8 - 1));
     const uint16_t* own = a.own_col ? a.own_col + ((size_t)i * m.L + a.layer) * 2 * Nk + (size_t)kh * HD : nullptr;
     // K block of page pg for this KV head
     auto page_k = [&](int pg) -> const uint16_t* {
         return a.kv_pool + ((((size_t)a.layer * m.n_pages + pg) * 2) * m.Hkv + kh) * (size_t)m.page_size * HD;
     };
-
-    // K row of position t and the V pieces of positions < nj (the only bytes the chunk needs:
-    // every block loads at once, so the load phase streams the whole launch's K/V); the
-    // verifier's own column stands in for the cache's tentative column p
-    uint4 kr[U4], vr[NLD];
-    if (t < nj) {
+    // K row of position t and the V pieces.  Every load is unconditional, so the waits
+    // below count requests exactly and the queries can be staged while K and V are in
+    // flight: positions past the chunk's last live one (nj - 1) re-read that position (a
+    // cache hit; those values are never used).  The verifier's own column stands in for
+    // the cache's tentative column p.
+    // (V pieces as a native vector type: a struct copy held across the scores stays in memory)
+    using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+    uint4 kr[U4];
+    u32x4 vr[NLD];
+    // (the page is taken from the unclamped position: pgs is clamped to the current
+    // position's page, which is also the page of the clamped position nj - 1)
+    {
+        const int jt = min(t, nj - 1);
         int pg = pgs[0];
 #pragma unroll
         for (int k = 1; k < NPG; ++k) pg = (t >> 4) == k ? pgs[k] : pg;
-        const uint4* kp = reinterpret_cast<const uint4*>((own && j0 + t == p) ? own : page_k(pg) + (size_t)(t & 15) * HD);
+        const uint16_t* kc = page_k(pg) + (size_t)(jt & 15) * HD;
+        const uint4* kp = reinterpret_cast<const uint4*>((own && j0 + jt == p) ? own : kc);
 #pragma unroll
         for (int k = 0; k < U4; ++k) kr[k] = kp[k];
     }
     // V: iteration k covers positions PPI*k .. PPI*k + PPI-1, i.e. PPI/16 pages
     constexpr int PPI = 256 / U4, PGI = PPI / 16;
     const int sub = (t / U4) >> 4;
-    const size_t voff = kv_stride + (size_t)((t / U4) & 15) * HD + (size_t)(t % U4) * 8;
-#pragma unroll
-    for (int k = 0; k < NLD; ++k) {
-        const int jj = t / U4 + PPI * k;
-        vr[k] = make_uint4(0, 0, 0, 0);
-        if (jj < nj) {
-            int pg = pgs[PGI * k];
-#pragma unroll
-            for (int q2 = 1; q2 < PGI; ++q2) pg = sub == q2 ? pgs[PGI * k + q2] : pg;
-            const uint16_t* vp = (own && j0 + jj == p) ? own + Nk + (size_t)(t % U4) * 8 : page_k(pg) + voff;
-            vr[k] = *reinterpret_cast<const uint4*>(vp);
-        }
-    }
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
         const int e = t + 256 * k;
-        *reinterpret_cast<uint4*>(vs + (e / U4) * HP + (e % U4) * 4) = vr[k];
+        const int jj = min(e / U4, nj - 1), pc = e % U4;
+        int pg = pgs[PGI * k];
+#pragma unroll
+        for (int q2 = 1; q2 < PGI; ++q2) pg = sub == q2 ? pgs[PGI * k + q2] : pg;
+        const uint16_t* vc = page_k(pg) + kv_stride + (size_t)(jj & 15) * HD;
+        const uint16_t* vp = (own && j0 + jj == p) ? own + Nk : vc;
+        vr[k] = *reinterpret_cast<const u32x4*>(vp + pc * 8);
     }
+    {
+        float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
+        qd[0] = make_float4(bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y));
+        qd[1] = make_float4(bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w));
+    }
+    // the queries staged by other threads are needed from here on; the K and V requests stay
+    // in flight across this barrier (loads complete in order: the queries came first)
     __syncthreads();
 
-    // ---- scores: position t, all heads of the group at once (K in registers)
+    // ---- scores: position t, all heads of the group at once (K in registers), computed
+    // while the V requests are still in flight
+
     const float scale = attn_scale(HD);
     if (t < nj) {
         float sc[GP];
@@ -148,6 +154,11 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
         }
 #pragma unroll
         for (int h = 0; h < GP; ++h) ps[h * ATT_MAXC + t] = sc[h] * scale;
+    }
+#pragma unroll
+    for (int k = 0; k < NLD; ++k) {
+        const int e = t + 256 * k;
+        *reinterpret_cast<u32x4*>(vs + (e / U4) * HP + (e % U4) * 4) = vr[k];
     }
     __syncthreads();
 
