@@ -8,15 +8,16 @@
 //   group) starting from +0; the 64 lane sums are combined by the xor butterfly
 //   over offsets 32, 16, 8, 4, 2, 1 (all J*R butterflies of a wave are run
 //   together with the same pairings, see butterfly_sum_multi).
-// A wave owns J features; a block of 8 waves owns 8J features and a tile of R
-// rows (so the tile's activations, staged once per block, serve 8J features).  K is walked in chunks of 512 elements (one group per lane).  While the
-// fma work of chunk c runs, the weights of chunk c+1 are in flight (register
-// double buffer: one 16-byte group per feature and lane, 1 KiB coalesced per
-// feature, in a ping-pong register pair) and the rows' activations of chunk c+1 are
-// loaded into registers, then staged into the fp32 LDS tile between two barriers
-// (one buffer keeps the LDS footprint at R * 2 KiB, so more blocks fit per CU).  No
-// split-K, no atomics: a row's arithmetic is the same whatever R, J, the tile or the
-// count.
+// A wave owns J features (2, or 3 for wide outputs); a block of 8 waves owns 8J
+// features and a tile of R rows (so the tile's activations, staged once per block,
+// serve 8J features).  K is walked in chunks of 512 elements (one group per lane).
+// While the fma work of chunk c runs, the weights of chunk c+1 are in flight (register
+// double buffer: one 16-byte group per feature and lane, 1 KiB coalesced per feature,
+// in a ping-pong register pair) and the rows' activations of chunk c+1 are loaded into
+// registers, then staged into the fp32 LDS tile: tiles up to 16 rows have two buffers
+// and one barrier per chunk; larger tiles restage one buffer between two barriers,
+// which keeps their LDS footprint at R * 2 KiB.  No split-K, no atomics: a row's
+// arithmetic is the same whatever R, J, the tile or the count.
 // Row tiles: when the host knows the row count (up to 24 rows) one tile of exactly
 // ceil(n/4)*4 rows runs every row without a branch, which lets the compiler read later
 // rows' activations from LDS while earlier rows compute (the dead rows compute on a copy
@@ -38,6 +39,20 @@ constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
 #ifndef MG_GEMV_J_R16
 #define MG_GEMV_J_R16 2
 #endif
+#ifndef MG_GEMV_J_R12
+#define MG_GEMV_J_R12 2  // features per wave of the exact 9..16-row tiles
+#endif
+// exact 9..16-row tiles of a wide output (N >= MG_GEMV_BIG_N: the MLP up projection, the
+// LM head) give each wave 3 features: a third fewer LDS activation reads per fma, and
+// still over a thousand blocks (measured at 12 rows: LM head 239 vs 261 us, gate/up 60 vs
+// 61 us; 4 features drop to 3 waves per SIMD and are slower; narrower outputs keep 2 for
+// the block count)
+#ifndef MG_GEMV_J_BIG
+#define MG_GEMV_J_BIG 3
+#endif
+#ifndef MG_GEMV_BIG_N
+#define MG_GEMV_BIG_N 16384
+#endif
 #ifndef MG_GEMV_EXACT_MAX
 #define MG_GEMV_EXACT_MAX 24  // largest host row count served by one branch-free tile
 #endif
@@ -48,9 +63,14 @@ constexpr int GV_NW = MG_GEMV_NW, GV_THREADS = 64 * MG_GEMV_NW;
 
 __host__ __device__ constexpr int pow2_at_least(int v) { return v <= 1 ? 1 : 2 * pow2_at_least((v + 1) / 2); }
 
+#ifndef MG_GEMV_XB_MAXR
+#define MG_GEMV_XB_MAXR 16  // row tiles up to this size get two LDS activation buffers
+#endif
+
 template <int R>
 struct GemvShape {
     static constexpr int XLD = (R * 64 + GV_THREADS - 1) / GV_THREADS;  // staging loads (16 bytes) per thread per chunk
+    static constexpr int XB = R <= MG_GEMV_XB_MAXR ? 2 : 1;               // LDS activation buffers
 };
 
 // activations of chunk kc for rows r0 .. r0+R-1: rows past nr read row nr-1 and k past
@@ -139,8 +159,9 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
     const int jw = (fb * GV_NW + wave) * J;
     const int K = a.K, G = K >> 3;
 
-    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[rr][half][lane].c
-    __shared__ float4 xs[R][2][64];
+    // LDS chunk: element 8*lane + 4*half + c of row rr at xs[buf][rr][half][lane].c
+    constexpr int XB = GemvShape<R>::XB;
+    __shared__ float4 xs[XB][R][2][64];
 
     const uint16_t* wrow[J];
     bool valid[J];
@@ -164,19 +185,22 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
     uint4 xr[GemvShape<R>::XLD];
     gemv_load_x<R>(a, r0, nr, 0, xr);
     gemv_load_w<J>(wrow, lane, G, wA);
-    gemv_store_x<R>(xs, xr);
+    gemv_store_x<R>(xs[0], xr);
     __syncthreads();
     // one chunk with a successor: request chunk c+1 (activations first, then weights
-    // into `nxt`), run chunk c, then restage the LDS tile between two barriers.  Loads
-    // complete in order, so the restaging waits for the activations only and the
-    // weights of chunk c+1 stay in flight.
+    // into `nxt`), run chunk c, then stage chunk c+1's activations.  Loads complete in
+    // order, so the staging waits for the activations only and the weights of chunk c+1
+    // stay in flight.  With two LDS buffers chunk c+1 goes to the other buffer and one
+    // barrier per chunk suffices (the buffer it overwrites was last read by chunk c-1,
+    // which every wave finished before the previous barrier); with one buffer the
+    // restaging sits between two barriers.
     auto step = [&](int c, const uint4 (&cur)[J], uint4 (&nxt)[J]) {
         gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, xr);
         gemv_load_w<J>(wrow, (c + 1) * 64 + lane, G, nxt);
         __builtin_amdgcn_sched_barrier(0);
-        if (c * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs, lane, nr, cur, acc);
-        __syncthreads();
-        gemv_store_x<R>(xs, xr);
+        if (c * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs[c % XB], lane, nr, cur, acc);
+        if (XB == 1) __syncthreads();
+        gemv_store_x<R>(xs[(c + 1) % XB], xr);
         __syncthreads();
     };
     int c = 0;
@@ -186,9 +210,9 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
     }
     if (c + 1 < nch) {
         step(c, wA, wB);
-        if ((c + 1) * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs, lane, nr, wB, acc);
+        if ((c + 1) * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs[(c + 1) % XB], lane, nr, wB, acc);
     } else if (c * 64 + lane < G) {
-        gemv_fma_chunk<J, R, EXACT>(xs, lane, nr, wA, acc);
+        gemv_fma_chunk<J, R, EXACT>(xs[c % XB], lane, nr, wA, acc);
     }
 
     // all J*R butterflies at once (padded to a power of two; each value is summed over the
@@ -236,17 +260,23 @@ static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s)
 }
 
 // A host row count up to 24 gets one tile of exactly ceil(n/4)*4 rows (branch-free rows,
-// at most three of them dead); larger counts and device-side counts use 16-row tiles
-// (8-row when at most 8 rows can occur) that skip dead rows by a uniform branch.
+// at most three of them dead; 9..16 rows of a wide output with 3 features per wave);
+// larger counts and device-side counts use 16-row tiles (8-row when at most 8 rows can
+// occur) that skip dead rows by a uniform branch.
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
     if (!a.n_dev && rows <= MG_GEMV_EXACT_MAX) {
-        switch ((rows + 3) / 4) {
+        const int nt = (rows + 3) / 4;
+        if (nt == 3 || nt == 4) {
+            if (a.N >= MG_GEMV_BIG_N) return nt == 3 ? launch_jr<MG_GEMV_J_BIG, 12, true>(a, epi, rows, s)
+                                                     : launch_jr<MG_GEMV_J_BIG, 16, true>(a, epi, rows, s);
+        }
+        switch (nt) {
             case 1: return launch_jr<MG_GEMV_J_R8, 4, true>(a, epi, rows, s);
             case 2: return launch_jr<MG_GEMV_J_R8, 8, true>(a, epi, rows, s);
-            case 3: return launch_jr<MG_GEMV_J_R16, 12, true>(a, epi, rows, s);
-            case 4: return launch_jr<MG_GEMV_J_R16, 16, true>(a, epi, rows, s);
+            case 3: return launch_jr<MG_GEMV_J_R12, 12, true>(a, epi, rows, s);
+            case 4: return launch_jr<MG_GEMV_J_R12, 16, true>(a, epi, rows, s);
             case 5: return launch_jr<MG_GEMV_J_R16, 20, true>(a, epi, rows, s);
             default: return launch_jr<MG_GEMV_J_R16, 24, true>(a, epi, rows, s);
         }
