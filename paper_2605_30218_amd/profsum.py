@@ -8,7 +8,8 @@ Both summaries cover the decode window only: the dispatches from the first fast-
 residual/RMSNorm kernel on (the canonical prompt prefill before it uses other kernels).
 The benchmark restores the KV cache from its snapshot (one copy of more than 1 ms) before
 each mode, so the trace summary also splits the window at those copies into the tau
-calibration steps and the modes named by [modes] (comma separated, benchmark order).
+calibration steps, the runs of the threshold recipe, and the modes named by [modes]
+(comma separated, benchmark order; they are the last windows).
 The traffic summary scales FETCH_SIZE and WRITE_SIZE (KiB per dispatch) by what each
 counter reads for a plain copy kernel of known size, and records the sha256 of the
 kernel's source file so that a later change of the kernel makes the figure stale.
@@ -51,12 +52,19 @@ MODE_KERNELS = ("fast_gemm_kernel", "canon_gemv_kernel", "attn_fast_fused_kernel
 def _mode_tables(rows, modes):
     cuts = [i for i, r in enumerate(rows) if "copyBuffer" in r["Kernel_Name"]
             and int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) > 1_000_000]
-    names = ["tau calibration"] + modes
     bounds = [0] + cuts + [len(rows)]
+    # windows that run decode steps (copies after the last mode, e.g. for the CPU baseline,
+    # leave windows without any); the modes are the last of them, before them the quantile
+    # tau calibration and the runs of the threshold recipe (reference decode, fast run, one
+    # run per tau)
+    segs = [rows[bounds[w]:bounds[w + 1]] for w in range(len(bounds) - 1)]
+    segs = [seg for seg in segs if any(MODE_KERNELS[0] in r["Kernel_Name"] for r in seg)]
+    nrec = max(0, len(segs) - 1 - len(modes))
+    names = ["tau calibration"] + [f"recipe run {k}" for k in range(1, nrec + 1)] + modes
     lines = ["", "per mode (windows split at the KV snapshot restores; warmup steps included):",
              f"{'mode':16s} {'kernel':22s} {'calls':>7s} {'avg_us':>9s} {'total_ms':>9s}"]
-    for w in range(min(len(names), len(bounds) - 1)):
-        seg = rows[bounds[w]:bounds[w + 1]]
+    for w in range(min(len(names), len(segs))):
+        seg = segs[w]
         for kn in MODE_KERNELS:
             d = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in seg if kn in r["Kernel_Name"]]
             if d:
