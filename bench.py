@@ -14,8 +14,10 @@ rate is reported.
 One JSON line on stdout: value = gated decode tokens/s (B * steps / time of the timed
 steps, inputs resident in HBM), plus the other modes, the verifier overhead
 (inc_mode = T_mode / T_off - 1, cut = inc_always / inc_gated), the roofline of the
-dominant kernel measured with HIP events over the timed region, and the CPU oracle
-baseline on a bounded sample.
+dominant kernel measured with HIP events over the timed region, the HBM roofline fraction
+of each mode and of the fast forward and the verifier alone (algorithmic bytes: every
+streamed weight once per forward, the live K/V of the rows involved, the fp32 logits), the
+histogram of verified rows per step, and the CPU oracle baseline on a bounded sample.
 """
 import argparse
 import json
@@ -46,6 +48,17 @@ def attn_bytes(shape, rows, ctx):
     kv = ctx * shape.n_kv_heads * shape.head_dim * 2 * 2
     qo = 2 * shape.n_q_heads * shape.head_dim * 2
     return rows * (kv + qo)
+
+
+def streamed_weight_bytes(shape):
+    """bf16 bytes of every weight a forward streams (the embedding is gathered, not streamed)."""
+    return 2 * (shape.n_params() - shape.vocab * shape.d_model)
+
+
+def forward_bytes(shape, rows, ctx):
+    """Algorithmic HBM bytes of one forward over `rows` rows at context `ctx`: every streamed
+    weight once, each layer's attention bytes, the fp32 logits written."""
+    return streamed_weight_bytes(shape) + shape.n_layers * attn_bytes(shape, rows, ctx) + rows * shape.vocab * 4
 
 
 def log(*a):
@@ -91,9 +104,16 @@ def run_mode(dec, mode, warmup, steps, state, kv_snap, eng, profile_kinds=(), pr
             ran = [(s, r) for s, r in enumerate(rows) if r][:n // L]
             b = sum(L * attn_bytes(eng.shape, r, ctx0 + s) for s, r in ran)
             prof[k] = (n, ms, float(b), f)
+    # algorithmic bytes of the timed steps: the fast forward of all rows, and the verifier's
+    # forward of its rows on the steps that ran it (the weights are streamed again)
+    fast_b = sum(forward_bytes(eng.shape, B, ctx0 + s) for s in range(steps))
+    ver_b = sum(forward_bytes(eng.shape, r, ctx0 + s) for s, r in enumerate(dec.hist) if r)
     return dict(ms_per_step=wall * 1e3 / steps, tok_s=B * steps / wall, p50_ms=float(np.median(per)),
                 p99_ms=float(np.percentile(per, 99)), r_verify=dec.r_verify, r_repair=dec.r_repair(),
-                verified_rows_per_step=float(np.mean(dec.hist)), prof=prof)
+                verified_rows_per_step=float(np.mean(dec.hist)),
+                verified_rows_hist=np.bincount(np.asarray(dec.hist, dtype=np.int64), minlength=1).tolist(),
+                fast_bytes_per_step=fast_b / steps, verifier_bytes_per_step=ver_b / steps,
+                hbm_frac=(fast_b + ver_b) / wall / HBM_PEAK, prof=prof)
 
 
 def calibrate_tau(dec, eng, state, kv_snap, steps, rate):
@@ -267,6 +287,13 @@ def main():
         if "inc_gated" in ov and "inc_always" in ov and ov["inc_gated"] > 0:
             ov["cut"] = ov["inc_always"] / ov["inc_gated"]
         out["verifier_overhead"] = ov
+        # HBM roofline fraction of the fast forward alone (off) and of the verifier alone (its
+        # algorithmic bytes per step over the time a mode adds to off)
+        rf = {"fast_forward": modes["off"]["hbm_frac"]}
+        for m in ("gated", "always"):
+            if m in modes and modes[m]["ms_per_step"] > t_off:
+                rf[f"verifier_{m}"] = modes[m]["verifier_bytes_per_step"] / ((modes[m]["ms_per_step"] - t_off) * 1e-3) / HBM_PEAK
+        out["hbm_frac"] = rf
     if not args.no_cpu_baseline:
         log("[bench] cpu baseline (oracle)")
         eng.kv_pool.copy_(kv_snap)

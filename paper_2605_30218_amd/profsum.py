@@ -3,6 +3,7 @@
     python -m paper_2605_30218_amd.profsum trace <kernel_trace.csv> <out.txt> "<command>" [modes]
     python -m paper_2605_30218_amd.profsum traffic <kernel> <fetch_csv> <write_csv> <copy_fetch_csv> \
         <copy_write_csv> <copy_bytes> <out.txt> "<command>" "<copy command>"
+    python -m paper_2605_30218_amd.profsum util <counter_collection.csv> <out.txt> "<command>" <k1,k2,..>
 
 Both summaries cover the decode window only: the dispatches from the first fast-path
 residual/RMSNorm kernel on (the canonical prompt prefill before it uses other kernels).
@@ -138,6 +139,27 @@ def traffic(kernel, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_b
     open(out, "w").write("\n".join(lines) + "\n")
 
 
+def util(pmc_csv: str, out: str, command: str, kernels: str) -> None:
+    """Mean of each collected counter (derived percentages such as MfmaUtil and VALUBusy)
+    over the decode-window dispatches of each named kernel."""
+    rows = _decode_window(list(csv.DictReader(open(pmc_csv))), "Dispatch_Id")
+    agg = collections.defaultdict(lambda: collections.defaultdict(list))
+    names = kernels.split(",")
+    for r in rows:
+        for k in names:
+            if k in r["Kernel_Name"]:
+                agg[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    counters = sorted({c for k in agg for c in agg[k]})
+    lines = [f"command: {command}", "window: decode steps; mean over each kernel's dispatches", "",
+             f"{'kernel':26s} {'dispatches':>10s} " + " ".join(f"{c:>12s}" for c in counters)]
+    for k in names:
+        if k in agg:
+            n = max(len(v) for v in agg[k].values())
+            lines.append(f"{k:26s} {n:10d} " + " ".join(
+                f"{sum(agg[k][c]) / len(agg[k][c]):12.2f}" if agg[k][c] else f"{'-':>12s}" for c in counters))
+    open(out, "w").write("\n".join(lines) + "\n")
+
+
 def read_traffic(path: str):
     """(bytes per launch, source sha) from a traffic summary, or None."""
     if not os.path.exists(path):
@@ -156,5 +178,7 @@ if __name__ == "__main__":
         trace(*sys.argv[2:6])
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:11])
+    elif sys.argv[1] == "util":
+        util(*sys.argv[2:6])
     else:
         raise SystemExit(__doc__)

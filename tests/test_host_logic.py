@@ -50,3 +50,34 @@ def test_trace_mode_windows_are_named_from_the_last_decode_windows():
     assert got[("always", "canon_gemv_kernel")] == 70.0
     assert ("off", "canon_gemv_kernel") not in got
     assert ("recipe run 1", "canon_gemv_kernel") in got
+
+
+def test_forward_bytes_of_the_llama8b_shape():
+    """The benchmark's algorithmic bytes: 7.505 B streamed parameters (embedding gathered, not
+    streamed) and 128 KiB of K/V per token over all layers on the Llama-3.1-8B shape."""
+    import bench
+    from paper_2605_30218_amd import synth
+    s = synth.LLAMA8B
+    assert abs(bench.streamed_weight_bytes(s) / 2 - 7.505e9) < 0.001e9
+    one = bench.forward_bytes(s, 1, 1000) - bench.forward_bytes(s, 1, 999)
+    assert one == 128 * 1024
+    assert bench.forward_bytes(s, 2, 10) - bench.forward_bytes(s, 1, 10) == \
+        s.n_layers * bench.attn_bytes(s, 1, 10) + s.vocab * 4
+
+
+def test_util_summary_means_per_kernel(tmp_path):
+    """The counter-utilisation summary averages each counter over a kernel's dispatches in
+    the decode window (dispatches before the first fast-path RMSNorm are prefill)."""
+    from paper_2605_30218_amd import profsum
+    p = tmp_path / "c.csv"
+    rows = [("1", "prefill_kernel", "MfmaUtil", "99"), ("2", "resid_norm_kernel", "MfmaUtil", "0"),
+            ("3", "fast_gemm_kernel<4>", "MfmaUtil", "10"), ("4", "fast_gemm_kernel<4>", "MfmaUtil", "30"),
+            ("3", "fast_gemm_kernel<4>", "VALUBusy", "5"), ("5", "canon_gemv_kernel<2>", "VALUBusy", "80")]
+    p.write_text("Dispatch_Id,Kernel_Name,Counter_Name,Counter_Value\n" + "".join(",".join(r) + "\n" for r in rows))
+    out = tmp_path / "o.txt"
+    profsum.util(str(p), str(out), "cmd", "fast_gemm_kernel,canon_gemv_kernel")
+    lines = out.read_text().splitlines()
+    fg = [ln for ln in lines if ln.startswith("fast_gemm_kernel")][0].split()
+    assert fg[1] == "2" and float(fg[2]) == 20.0 and float(fg[3]) == 5.0
+    cg = [ln for ln in lines if ln.startswith("canon_gemv_kernel")][0].split()
+    assert cg[2] == "-" and float(cg[3]) == 80.0
