@@ -89,7 +89,10 @@ def test_fast_gemm_within_tolerance(n, N, K):
     assert np.all(np.abs(Y - ref) <= bound)
 
 
-@pytest.mark.parametrize("n,N,K", [(3, 48, 688), (64, 256, 4096), (130, 64, 1032)])
+# (64, 256, 4096), (20, 128, 1024), (128, 96, 2048), (9, 64, 512): the direct-to-LDS
+# operand path at 4-, 2-, 8- and 1-tile row counts; the others the register path
+@pytest.mark.parametrize("n,N,K", [(3, 48, 688), (64, 256, 4096), (130, 64, 1032), (20, 128, 1024), (128, 96, 2048),
+                                   (9, 64, 512)])
 def test_fast_gemm_small_integers_exact(n, N, K):
     X = synth.small_int_bf16((n, K), seed=21)
     W = synth.small_int_bf16((N, K), seed=22)
