@@ -477,15 +477,21 @@ int mgo_verify_rows(const mgo_cfg* c, const void* const* w, int mode, int n, con
     return 0;
 }
 
-int mgo_repair_kv_column(const mgo_cfg* c, int n, const int32_t* rows, const int32_t* positions,
-                         const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
-                         const uint16_t* v_kvcol, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired) {
-    if (!cfg_ok(c) || n < 0 || !n_repaired) return -1;
+/* Sec. 3.2 commit rule (action 0) and the two variants around it: token only -- the
+ * verifier's token is emitted and the tentative BF16 column stays, the ablation of Sec. 4
+ * (Ablations and Robustness, repair action); copy always -- the verifier's column is copied
+ * on every verified row, agreeing ones included. */
+int mgo_repair_kv_column_action(const mgo_cfg* c, int n, const int32_t* rows, const int32_t* positions,
+                                const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
+                                const uint16_t* v_kvcol, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired,
+                                int action) {
+    if (!cfg_ok(c) || n < 0 || !n_repaired || action < 0 || action > 2) return -1;
     const int hd = c->head_dim, Hkv = c->n_kv_heads, ps = c->page_size;
     for (int i = 0; i < n; ++i) {
         const int r = rows[i];
         emitted[r] = v_tok[i];
-        if (v_tok[i] == top1[r]) continue; /* verified commit: keep the tentative column */
+        const int copy = action == 2 || (action == 0 && v_tok[i] != top1[r]);
+        if (!copy) continue; /* verified commit (or token only): keep the tentative column */
         const int p = positions[r];
         const int pg = page_table[(size_t)r * c->max_pages_per_row + p / ps], sl = p % ps;
         for (int l = 0; l < c->n_layers; ++l)
@@ -496,6 +502,13 @@ int mgo_repair_kv_column(const mgo_cfg* c, int n, const int32_t* rows, const int
         *n_repaired += 1;
     }
     return 0;
+}
+
+int mgo_repair_kv_column(const mgo_cfg* c, int n, const int32_t* rows, const int32_t* positions,
+                         const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
+                         const uint16_t* v_kvcol, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired) {
+    return mgo_repair_kv_column_action(c, n, rows, positions, page_table, top1, v_tok, v_kvcol, kv_pool, emitted,
+                                       n_repaired, 0);
 }
 
 int mgo_prefill(const mgo_cfg* c, const void* const* w, int mode, int n_tok, const int32_t* tokens,

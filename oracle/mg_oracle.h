@@ -83,6 +83,12 @@ int mgo_verify_rows(const mgo_cfg* c, const void* const* w, int mode, int n, con
 int mgo_repair_kv_column(const mgo_cfg* c, int n, const int32_t* rows, const int32_t* positions,
                          const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
                          const uint16_t* v_kvcol, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired);
+/* the commit rule with a repair action: 0 copy the verifier column when the tokens differ
+ * (Sec. 3.2), 1 token only (the repair-action ablation of Sec. 4), 2 copy on every verified row */
+int mgo_repair_kv_column_action(const mgo_cfg* c, int n, const int32_t* rows, const int32_t* positions,
+                                const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
+                                const uint16_t* v_kvcol, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired,
+                                int action);
 /* prompt prefill of one row, positions [0, n_tok), causal, in `mode` */
 int mgo_prefill(const mgo_cfg* c, const void* const* w, int mode, int n_tok, const int32_t* tokens,
                 const int32_t* page_table_row, uint16_t* kv_pool);

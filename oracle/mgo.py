@@ -21,6 +21,10 @@ LIB_PATH = os.path.join(HERE, "liboracle_mg.so")
 
 PLAIN = 0
 CANON = 1
+# repair actions of the commit (Sec. 3.2; the token-only ablation of Sec. 4)
+REPAIR_ON_MISMATCH = 0
+REPAIR_TOKEN_ONLY = 1
+REPAIR_COPY_ALWAYS = 2
 WPL = 12  # weight pointers per layer
 
 
@@ -67,6 +71,7 @@ def lib():
             ("mgo_margin_gate", [i32, i32, P, P, f32, P, P, P, P, P]),
             ("mgo_verify_rows", [P, P, i32, i32, P, P, P, P, P, P, P, P]),
             ("mgo_repair_kv_column", [P, i32, P, P, P, P, P, P, P, P, P]),
+            ("mgo_repair_kv_column_action", [P, i32, P, P, P, P, P, P, P, P, P, i32]),
             ("mgo_prefill", [P, P, i32, i32, P, P, P]),
         ):
             f = getattr(_lib, name)
@@ -235,17 +240,19 @@ class OracleModel:
              "verify_rows")
         return v_logits, v_tok, v_kvcol
 
-    def repair(self, rows, positions, page_table, top1, v_tok, v_kvcol, emitted):
+    def repair(self, rows, positions, page_table, top1, v_tok, v_kvcol, emitted, action=REPAIR_ON_MISMATCH):
+        """Commit (Sec. 3.2).  action: REPAIR_ON_MISMATCH (the method), REPAIR_TOKEN_ONLY (the
+        repair-action ablation of Sec. 4), REPAIR_COPY_ALWAYS (copy on every verified row)."""
         rows = np.ascontiguousarray(rows, np.int32)
         emitted = np.array(emitted, np.int32, copy=True)
         nrep = np.zeros(1, np.int32)
-        _chk(lib().mgo_repair_kv_column(C.byref(self.cfg), rows.size, _p(rows),
-                                        _p(np.ascontiguousarray(positions, np.int32)),
-                                        _p(np.ascontiguousarray(page_table, np.int32)),
-                                        _p(np.ascontiguousarray(top1, np.int32)),
-                                        _p(np.ascontiguousarray(v_tok, np.int32)),
-                                        _p(np.ascontiguousarray(v_kvcol, np.uint16)), _p(self.kv_pool),
-                                        _p(emitted), _p(nrep)), "repair")
+        _chk(lib().mgo_repair_kv_column_action(C.byref(self.cfg), rows.size, _p(rows),
+                                               _p(np.ascontiguousarray(positions, np.int32)),
+                                               _p(np.ascontiguousarray(page_table, np.int32)),
+                                               _p(np.ascontiguousarray(top1, np.int32)),
+                                               _p(np.ascontiguousarray(v_tok, np.int32)),
+                                               _p(np.ascontiguousarray(v_kvcol, np.uint16)), _p(self.kv_pool),
+                                               _p(emitted), _p(nrep), int(action)), "repair")
         return emitted, int(nrep[0])
 
     def prefill(self, mode, tokens, page_table_row):
@@ -256,7 +263,8 @@ class OracleModel:
 
     # -------------------------------------------------------------- the gated loop
 
-    def gated_step(self, fast_mode, tokens, positions, page_table, protected, tau, verify="gated"):
+    def gated_step(self, fast_mode, tokens, positions, page_table, protected, tau, verify="gated",
+                   action=REPAIR_ON_MISMATCH):
         """One MarginGate step (Sec. 3.1-3.3).  verify in {"off", "gated", "always"}.
         Returns (emitted, record) where record holds logits, top1, margin, gate, rows, v_tok, n_repaired."""
         logits = self.decode_step(fast_mode, tokens, positions, page_table)
@@ -272,6 +280,6 @@ class OracleModel:
         nrep = 0
         if rows.size:
             _, v_tok, v_kvcol = self.verify_rows(rows, tokens, positions, page_table, want_logits=False)
-            emitted, nrep = self.repair(rows, positions, page_table, top1, v_tok, v_kvcol, emitted)
+            emitted, nrep = self.repair(rows, positions, page_table, top1, v_tok, v_kvcol, emitted, action)
         return emitted, dict(logits=logits, top1=top1, margin=margin, gate=gate, rows=rows, v_tok=v_tok,
                              n_repaired=nrep)

@@ -506,6 +506,38 @@ def test_repair_overwrites_only_the_current_column():
     np.testing.assert_array_equal(kv[mask], kb[mask])
 
 
+@pytest.mark.parametrize("action", [mgo.REPAIR_TOKEN_ONLY, mgo.REPAIR_COPY_ALWAYS])
+def test_repair_action_variants(action):
+    """The two repair actions around the commit rule (Sec. 3.2): token only -- the
+    repair-action ablation of Sec. 4, the verifier's token is emitted and the cache keeps
+    the tentative column (no byte changes, no repair counted); copy always -- every verified
+    row's column is overwritten, agreeing rows included, and nothing else."""
+    om, w, pt = _tiny_model(max_batch=3, ctx=48)
+    rng = np.random.default_rng(1)
+    om.kv_pool[:] = rng.integers(0, 1 << 16, om.kv_pool.size, dtype=np.uint16)
+    before = om.kv_pool.copy()
+    rows = np.array([0, 2], np.int32)
+    pos = np.array([5, 40, 17], np.int32)
+    top1 = np.array([10, 11, 12], np.int32)
+    v_tok = np.array([10, 99], np.int32)      # row 0 agrees, row 2 differs
+    col = rng.integers(0, 1 << 16, (2, om.col_elems()), dtype=np.uint16)
+    emitted, nrep = om.repair(rows, pos, pt, top1, v_tok, col, top1, action)
+    assert list(emitted) == [10, 11, 99]
+    kv, kb = om.kv_view(), before.reshape(om.kv_view().shape)
+    s = synth.TINY
+    if action == mgo.REPAIR_TOKEN_ONLY:
+        assert nrep == 0
+        np.testing.assert_array_equal(om.kv_pool, before)
+        return
+    assert nrep == 2
+    mask = np.ones(kv.shape, bool)
+    for i, r in enumerate(rows):
+        page, slot = pt[r, pos[r] // 16], pos[r] % 16
+        np.testing.assert_array_equal(kv[:, page, :, :, slot, :], col[i].reshape(s.n_layers, 2, s.n_kv_heads, s.head_dim))
+        mask[:, page, :, :, slot, :] = False
+    np.testing.assert_array_equal(kv[mask], kb[mask])
+
+
 def test_plain_and_canonical_agree_within_tolerance():
     om, w, pt = _tiny_model(max_batch=1, ctx=48)
     toks = synth.make_prompts(1, [33], synth.TINY.vocab, seed=9)[0]
