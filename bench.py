@@ -225,6 +225,11 @@ def main():
         calib = calibrate.calibrate(dec, state, kv_snap, pareto_steps)
         dec.tau = tau
         log(f"[bench] eps median {calib['eps_median']:.4f} max {calib['eps_max']:.4f}, tau_100 {calib['tau_100']}")
+        # the repair actions of the commit at the benchmark's tau, against the same reference
+        calib["repair_actions"] = calibrate.repair_actions(dec, state, kv_snap, pareto_steps, tau,
+                                                           reference=calib.pop("reference"), t_off=calib.pop("t_off"))
+        log("[bench] repair actions: " + ", ".join(f"{k} seq_det {v['seq_det']:.3f} first div {v['first_divergence_mean']:.1f}"
+                                                     for k, v in calib["repair_actions"]["actions"].items()))
     modes = {}
     for mode in args.modes.split(","):
         steps = always_steps if mode == "always" else args.steps

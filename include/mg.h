@@ -148,6 +148,22 @@ mg_status mg_repair_kv_column(mg_ctx* ctx, int n, const int32_t* rows, const int
                               const int32_t* v_tok, const uint16_t* v_kvcol, int32_t* emitted,
                               int32_t* n_repaired, void* stream);
 
+/* The same commit with a choice of repair action (the variants around the rule of
+ * Sec. 3.2; Sec. 4, Ablations and Robustness, describes the token-only one):
+ *   MG_REPAIR_ON_MISMATCH  the method: copy the verifier column when v_tok[i] != top1[r]
+ *                          (mg_repair_kv_column is this action);
+ *   MG_REPAIR_TOKEN_ONLY   emit the verifier token, never copy (the tentative BF16 column
+ *                          stays; *n_repaired is not incremented);
+ *   MG_REPAIR_COPY_ALWAYS  copy the verifier column for every listed row, agreeing rows
+ *                          included (*n_repaired counts every copy).
+ * Arguments, layout and errors as mg_repair_kv_column; an action outside the three
+ * returns MG_ERR_ARG and enqueues nothing. */
+enum { MG_REPAIR_ON_MISMATCH = 0, MG_REPAIR_TOKEN_ONLY = 1, MG_REPAIR_COPY_ALWAYS = 2 };
+mg_status mg_repair_kv_column_action(mg_ctx* ctx, int n, const int32_t* rows, const int32_t* n_dev,
+                                     const int32_t* positions, const int32_t* page_table, const int32_t* top1,
+                                     const int32_t* v_tok, const uint16_t* v_kvcol, int32_t* emitted,
+                                     int32_t* n_repaired, int action, void* stream);
+
 /* Prompt prefill with the verifier's canonical arithmetic, so that runs at any
  * batch size start from bit-identical prompt caches.  Item i consumes
  * tokens[i] at position positions[i] of row item_rows[i] (a row of page_table)

@@ -2,6 +2,7 @@
 // top-1/top-2 margin gate, the K/V column repair, step bookkeeping, numerics probes.
 #include "mg_device.h"
 #include "mg_kernels.h"
+#include "../../include/mg.h"
 
 namespace mg {
 
@@ -368,14 +369,16 @@ __global__ __launch_bounds__(256) void repair_kernel(RowCount rc, const int32_t*
                                                      const int32_t* __restrict__ v_tok,
                                                      const uint16_t* __restrict__ v_kvcol, ModelDims m,
                                                      uint16_t* __restrict__ kv_pool, int32_t* emitted,
-                                                     int32_t* n_repaired) {
+                                                     int32_t* n_repaired, int action) {
     const int i = blockIdx.x;
     if (i >= rc.get()) return;
     __shared__ int decide[2];
     const int r = rows[i];
     if (threadIdx.x == 0) {
         decide[0] = v_tok[i];
-        decide[1] = (v_tok[i] != top1[r]);
+        // the method copies on a disagreement; the variants never copy (token only) or
+        // always copy
+        decide[1] = action == MG_REPAIR_COPY_ALWAYS ? 1 : action == MG_REPAIR_TOKEN_ONLY ? 0 : (v_tok[i] != top1[r]);
     }
     __syncthreads();
     const int vt = decide[0];
@@ -403,12 +406,12 @@ __global__ __launch_bounds__(256) void repair_kernel(RowCount rc, const int32_t*
 
 hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_t* rows, const int32_t* positions,
                          const int32_t* page_table, const int32_t* top1, const int32_t* v_tok, const uint16_t* v_kvcol,
-                         const ModelDims& m, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired, hipStream_t s) {
+                         const ModelDims& m, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired, int action, hipStream_t s) {
     const int grid = n_dev ? cap : n_host;
     if (grid <= 0) return hipSuccess;
     RowCount rc{n_dev, n_host, cap};
     hipLaunchKernelGGL(repair_kernel, dim3(grid), dim3(256), 0, s, rc, rows, positions, page_table, top1, v_tok,
-                       v_kvcol, m, kv_pool, emitted, n_repaired);
+                       v_kvcol, m, kv_pool, emitted, n_repaired, action);
     return hipGetLastError();
 }
 

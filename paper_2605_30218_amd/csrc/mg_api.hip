@@ -480,14 +480,24 @@ mg_status mg_verify_rows(mg_ctx* c, int n, const int32_t* rows, const int32_t* n
 mg_status mg_repair_kv_column(mg_ctx* c, int n, const int32_t* rows, const int32_t* n_dev, const int32_t* positions,
                               const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
                               const uint16_t* v_kvcol, int32_t* emitted, int32_t* n_repaired, void* stream) {
+    return mg_repair_kv_column_action(c, n, rows, n_dev, positions, page_table, top1, v_tok, v_kvcol, emitted,
+                                      n_repaired, MG_REPAIR_ON_MISMATCH, stream);
+}
+
+mg_status mg_repair_kv_column_action(mg_ctx* c, int n, const int32_t* rows, const int32_t* n_dev,
+                                     const int32_t* positions, const int32_t* page_table, const int32_t* top1,
+                                     const int32_t* v_tok, const uint16_t* v_kvcol, int32_t* emitted,
+                                     int32_t* n_repaired, int action, void* stream) {
     if (!c) return MG_ERR_ARG;
+    if (action != MG_REPAIR_ON_MISMATCH && action != MG_REPAIR_TOKEN_ONLY && action != MG_REPAIR_COPY_ALWAYS)
+        return MG_ERR_ARG;
     if (n == 0) return MG_OK;
     if (n < -1 || n > c->cfg.max_batch || (n == -1 && !n_dev)) return MG_ERR_ARG;
     if (!rows || !positions || !page_table || !top1 || !v_tok || !v_kvcol || !emitted || !n_repaired)
         return MG_ERR_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
     HIPCHK(launch_repair(n == -1 ? 0 : n, n == -1 ? n_dev : nullptr, c->cfg.max_batch, rows, positions, page_table,
-                         top1, v_tok, v_kvcol, c->m, c->kv_pool, emitted, n_repaired, s));
+                         top1, v_tok, v_kvcol, c->m, c->kv_pool, emitted, n_repaired, action, s));
     return MG_OK;
 }
 

@@ -130,7 +130,7 @@ hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, f
 hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_t* rows, const int32_t* positions,
                          const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
                          const uint16_t* v_kvcol, const ModelDims& m, uint16_t* kv_pool, int32_t* emitted,
-                         int32_t* n_repaired, hipStream_t s);
+                         int32_t* n_repaired, int action, hipStream_t s);
 hipError_t launch_advance(int B, const int32_t* emitted, int32_t* tokens, int32_t* positions, hipStream_t s);
 
 // element-wise numerics probes used by the tests

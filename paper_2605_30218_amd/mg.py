@@ -16,6 +16,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libmg.so")
 
 MG_OK = 0
+# repair actions (include/mg.h)
+REPAIR_ON_MISMATCH, REPAIR_TOKEN_ONLY, REPAIR_COPY_ALWAYS = 0, 1, 2
 KIND_FAST_GEMM, KIND_FAST_ATTN, KIND_CANON_GEMV, KIND_CANON_ATTN, KIND_GATE = range(5)
 WPL = 12
 
@@ -50,6 +52,7 @@ SIGNATURES = {
     "mg_margin_gate": (I, [P, I, P, P, F, P, P, P, P, P, P, P]),
     "mg_verify_rows": (I, [P, I, P, P, P, P, P, P, P, P, P]),
     "mg_repair_kv_column": (I, [P, I, P, P, P, P, P, P, P, P, P, P]),
+    "mg_repair_kv_column_action": (I, [P, I, P, P, P, P, P, P, P, P, P, I, P]),
     "mg_prefill": (I, [P, I, P, P, P, P, P]),
     "mg_advance": (I, [P, I, P, P, P, P]),
     "mg_profile_begin": (I, [P, I, I]),
@@ -185,6 +188,12 @@ class Engine:
         _check("mg_repair_kv_column", self.lib.mg_repair_kv_column(
             self.ctx, n, _ptr(rows), _ptr(n_dev), _ptr(positions), _ptr(page_table), _ptr(top1), _ptr(v_tok),
             _ptr(v_kvcol), _ptr(emitted), _ptr(n_repaired), _stream(stream)))
+
+    def repair_kv_column_action(self, n, rows, n_dev, positions, page_table, top1, v_tok, v_kvcol, emitted,
+                                n_repaired, action, stream=None):
+        _check("mg_repair_kv_column_action", self.lib.mg_repair_kv_column_action(
+            self.ctx, n, _ptr(rows), _ptr(n_dev), _ptr(positions), _ptr(page_table), _ptr(top1), _ptr(v_tok),
+            _ptr(v_kvcol), _ptr(emitted), _ptr(n_repaired), int(action), _stream(stream)))
 
     def prefill(self, n_items, tokens, positions, item_rows, page_table, stream=None):
         _check("mg_prefill", self.lib.mg_prefill(self.ctx, n_items, _ptr(tokens), _ptr(positions), _ptr(item_rows),

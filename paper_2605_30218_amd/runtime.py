@@ -42,6 +42,10 @@ class GatedDecoder:
         self.v_tok = torch.empty(B, **i32)
         self.v_kvcol = torch.empty((B, engine.col_elems), dtype=torch.int16, device=dev)
         self.n_repaired = torch.zeros(1, **i32)
+        # the commit's repair action: the method's (copy the verifier column when the tokens
+        # differ), or a variant for the repair-action measurements (mg.REPAIR_TOKEN_ONLY,
+        # mg.REPAIR_COPY_ALWAYS)
+        self.repair_action = mg.REPAIR_ON_MISMATCH
         # the gate mirrors its count into pinned host memory; the host polls it instead of
         # synchronising the stream
         self._count_dev, self._count = mg.host_count_slot()
@@ -77,8 +81,12 @@ class GatedDecoder:
                         positions=self.positions.cpu().numpy(), tokens=self.tokens.cpu().numpy())
         if n:
             e.verify_rows(n, rows, None, self.tokens, self.positions, self.page_table, None, self.v_tok, self.v_kvcol)
-            e.repair_kv_column(n, rows, None, self.positions, self.page_table, self.top1, self.v_tok, self.v_kvcol,
-                               self.top1, self.n_repaired)
+            if self.repair_action == mg.REPAIR_ON_MISMATCH:
+                e.repair_kv_column(n, rows, None, self.positions, self.page_table, self.top1, self.v_tok, self.v_kvcol,
+                                   self.top1, self.n_repaired)
+            else:
+                e.repair_kv_column_action(n, rows, None, self.positions, self.page_table, self.top1, self.v_tok,
+                                          self.v_kvcol, self.top1, self.n_repaired, self.repair_action)
             if keep is not None:
                 keep.update(rows=rows[:n].cpu().numpy(), v_tok=self.v_tok[:n].cpu().numpy())
         elif keep is not None:

@@ -4,12 +4,14 @@
                      kept) equals the oracle's canonical greedy decode token for token, with a
                      bit-identical cache, and a row decoded alone equals the same row in the batch
   recipe             eps statistics, a frontier point per tau, tau_100 the smallest fully
-                     deterministic tau of the grid"""
+                     deterministic tau of the grid
+  repair actions     the three commits (copy on disagreement, token only, copy always); with
+                     every step verified, copy always is the reference decode itself"""
 import numpy as np
 import pytest
 import torch
 
-from paper_2605_30218_amd import calibrate, synth
+from paper_2605_30218_amd import calibrate, mg, synth
 from paper_2605_30218_amd.runtime import GatedDecoder
 
 from _gpu_common import Pair, u16
@@ -76,3 +78,25 @@ def test_calibration_recipe(pair, prompts):
         assert 0.0 <= f["r_verify"] <= 1.0 and 0.0 <= f["seq_det"] <= 1.0
     det = [f["tau"] for f in res["frontier"] if f["seq_det"] == 1.0]
     assert res["tau_100"] == (min(det) if det else None)
+
+
+def test_repair_actions(pair, prompts):
+    """MarginGate under each repair action from one state, against the reference decode.
+    Token only never copies (r_repair 0); copy always copies every verified row (r_repair =
+    r_verify); at a tau above every margin (all rows verified every step) copy always is the
+    reference decode token for token."""
+    last, pos0 = fresh(pair, prompts)
+    snap = pair.eng.kv_pool.clone()
+    dec = GatedDecoder(pair.eng, pair.pt[:4], None, tau=0.0)
+    res = calibrate.repair_actions(dec, (last, pos0), snap, STEPS, 0.05)
+    print(res)
+    a = res["actions"]
+    assert set(a) == {"on_mismatch", "token_only", "copy_always"}
+    assert a["token_only"]["r_repair"] == 0.0
+    assert a["copy_always"]["r_repair"] == pytest.approx(a["copy_always"]["r_verify"])
+    for v in a.values():
+        assert a["on_mismatch"]["r_verify"] == pytest.approx(v["r_verify"], abs=0.5) and 0 <= v["seq_det"] <= 1
+    assert dec.repair_action == mg.REPAIR_ON_MISMATCH and dec.tau == 0.0
+    top = calibrate.repair_actions(dec, (last, pos0), snap, STEPS, float("inf"))
+    assert top["actions"]["copy_always"]["r_verify"] == 1.0
+    assert top["actions"]["copy_always"]["seq_det"] == 1.0

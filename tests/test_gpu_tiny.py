@@ -13,7 +13,7 @@ import pytest
 import torch
 
 from oracle import mgo
-from paper_2605_30218_amd import synth
+from paper_2605_30218_amd import mg, synth
 
 from _gpu_common import Pair, dev_i32, normwise, u16
 
@@ -162,6 +162,43 @@ def test_repair_bitexact(pair):
     np.testing.assert_array_equal(emitted.cpu().numpy(), ref_em)
     assert int(nrep.item()) == ref_n == 2
     np.testing.assert_array_equal(u16(e.kv_pool), pair.om.kv_pool)
+
+
+@pytest.mark.parametrize("action", [mg.REPAIR_ON_MISMATCH, mg.REPAIR_TOKEN_ONLY, mg.REPAIR_COPY_ALWAYS])
+def test_repair_action_bitexact(pair, action):
+    """The commit with each repair action (Sec. 3.2; the token-only ablation of Sec. 4)
+    equals the oracle's: emitted tokens, the repair count and every cache byte; the device
+    count path included."""
+    e = pair.eng
+    rng = np.random.default_rng(6 + action)
+    pool = rng.integers(0, 1 << 16, e.kv_pool.numel(), dtype=np.uint16)
+    e.kv_pool.copy_(torch.from_numpy(pool.view(np.int16)))
+    pair.om.kv_pool[:] = pool
+    B = 6
+    rows = np.array([4, 0, 5, 2], np.int32)
+    pos = np.array([3, 50, 17, 95, 40, 64], np.int32)
+    top1 = rng.integers(0, V, B).astype(np.int32)
+    v_tok = top1[rows].copy()
+    v_tok[[1, 2]] += 1                                      # rows 0 and 5 disagree, 4 and 2 agree
+    col = rng.integers(0, 1 << 16, (rows.size, e.col_elems), dtype=np.uint16)
+    emitted = dev_i32(top1)
+    nrep = torch.zeros(1, dtype=torch.int32, device="cuda")
+    n_dev = dev_i32(np.array([rows.size], np.int32))
+    e.repair_kv_column_action(-1, dev_i32(rows), n_dev, dev_i32(pos), dev_i32(pair.pt[:B]), emitted, dev_i32(v_tok),
+                              torch.from_numpy(col.view(np.int16)).cuda(), emitted, nrep, action)
+    torch.cuda.synchronize()
+    ref_em, ref_n = pair.om.repair(rows, pos, pair.pt[:B], top1, v_tok, col, top1, action)
+    np.testing.assert_array_equal(emitted.cpu().numpy(), ref_em)
+    assert int(nrep.item()) == ref_n == {mg.REPAIR_ON_MISMATCH: 2, mg.REPAIR_TOKEN_ONLY: 0, mg.REPAIR_COPY_ALWAYS: 4}[action]
+    np.testing.assert_array_equal(u16(e.kv_pool), pair.om.kv_pool)
+
+
+def test_repair_action_out_of_range_is_rejected(pair):
+    e = pair.eng
+    z = torch.zeros(8, dtype=torch.int32, device="cuda")
+    col = torch.zeros((1, e.col_elems), dtype=torch.int16, device="cuda")
+    with pytest.raises(mg.MgError):
+        e.repair_kv_column_action(1, z, None, z, dev_i32(pair.pt[:1]), z, z, col, z, z, 3)
 
 
 def test_state_forced_gated_loop(pair, prompts):
