@@ -31,7 +31,7 @@ import torch
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-from paper_2605_30218_amd import calibrate, mg, profsum, synth  # noqa: E402
+from paper_2605_30218_amd import calibrate, diagnostics, mg, profsum, synth  # noqa: E402
 from paper_2605_30218_amd.runtime import GatedDecoder, prefill_fast, prefill_rows  # noqa: E402
 
 METRIC = "decode tok/s + gated-vs-always-on verifier overhead, Llama-3.1-8B-shape bs=64"
@@ -230,6 +230,13 @@ def main():
                                                            reference=calib.pop("reference"), t_off=calib.pop("t_off"))
         log("[bench] repair actions: " + ", ".join(f"{k} seq_det {v['seq_det']:.3f} first div {v['first_divergence_mean']:.1f}"
                                                      for k, v in calib["repair_actions"]["actions"].items()))
+        # the divergence diagnostics of Sec. 2 (Obs. 1-3) and the oracle-position repair
+        div, ref = diagnostics.flip_study(dec, state, kv_snap, pareto_steps, tau)
+        div["oracle_repair"] = diagnostics.oracle_position_repair(dec, state, kv_snap, pareto_steps, ref)
+        calib["divergence"] = div
+        log(f"[bench] flips: rate {div['flips']['rate']:.4f} ({div['flips']['events']} events), K spike "
+            f"{div['kv']['k_spike']}, oracle-position repairs/seq {div['oracle_repair']['repairs_per_sequence']:.2f} "
+            f"seq_det {div['oracle_repair']['seq_det']:.3f}")
     modes = {}
     for mode in args.modes.split(","):
         steps = always_steps if mode == "always" else args.steps

@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 import torch
 
-from paper_2605_30218_amd import calibrate, mg, synth
+from paper_2605_30218_amd import calibrate, diagnostics, mg, synth
 from paper_2605_30218_amd.runtime import GatedDecoder
 
 from _gpu_common import Pair, u16
@@ -100,3 +100,20 @@ def test_repair_actions(pair, prompts):
     top = calibrate.repair_actions(dec, (last, pos0), snap, STEPS, float("inf"))
     assert top["actions"]["copy_always"]["r_verify"] == 1.0
     assert top["actions"]["copy_always"]["seq_det"] == 1.0
+
+
+def test_divergence_diagnostics(pair, prompts):
+    """Obs. 1-3 and the oracle-position repair on the tiny decoder: the statistics are well
+    formed; until its first divergence a row of the oracle-position run is its ungated run, so
+    every ungated divergence event costs at least one verification there."""
+    last, pos0 = fresh(pair, synth.make_prompts(4, [32] * 4, S.vocab, seed=3))
+    snap = pair.eng.kv_pool.clone()
+    dec = GatedDecoder(pair.eng, pair.pt[:4], None, tau=0.0)
+    st, ref = diagnostics.flip_study(dec, (last, pos0), snap, STEPS, tau=0.05)
+    print(st)
+    assert st["rows"] == 4 and ref.shape == (4, STEPS)
+    assert 0.0 <= st["flips"]["rate"] <= 1.0 and st["flips"]["synchronous_samples"] >= 4
+    assert st["near_tie"]["events"] == st["flips"]["events"]
+    orc = diagnostics.oracle_position_repair(dec, (last, pos0), snap, STEPS, ref)
+    print(orc)
+    assert orc["verified_row_steps"] >= st["flips"]["events"] and 0.0 <= orc["seq_det"] <= 1.0

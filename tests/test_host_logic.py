@@ -81,3 +81,32 @@ def test_util_summary_means_per_kernel(tmp_path):
     assert fg[1] == "2" and float(fg[2]) == 20.0 and float(fg[3]) == 5.0
     cg = [ln for ln in lines if ln.startswith("canon_gemv_kernel")][0].split()
     assert cg[2] == "-" and float(cg[3]) == 80.0
+
+
+def test_divergence_statistics():
+    """Obs. 1-3 statistics (Sec. 2): events over synchronous samples, the K/V deviation aligned
+    at the first divergent cache step (first divergent token + 1), the reference token's rank
+    and the margin at each event."""
+    from paper_2605_30218_amd import diagnostics
+    steps = 10
+    ref = np.arange(30, dtype=np.int32).reshape(3, steps)
+    toks = ref.copy()
+    toks[1, 4] += 1          # row 1 diverges at step 4
+    toks[2, 0] += 1          # row 2 at step 0 (too early for the K/V window)
+    margins = np.full((3, steps), 0.5, np.float32)
+    margins[1, 4], margins[2, 0] = 0.01, 0.2
+    ranks = np.zeros((3, steps), np.int64)
+    ranks[1, 4], ranks[2, 0] = 1, 5
+    ek = np.ones((3, steps))
+    ek[1, 5:] = 50.0         # cache step 5 holds the first column from a divergent token
+    ev = 2 * np.ones((3, steps))
+    ev[1, 5:] = 40.0
+    st = diagnostics.divergence_stats(toks, ref, margins, ranks, ek, ev, tau=0.05, window=16)
+    assert st["flips"]["events"] == 2 and st["flips"]["synchronous_samples"] == 10 + 5 + 1
+    assert st["kv"]["trials"] == 1
+    assert st["kv"]["k_pre"] == 1.0 and st["kv"]["k_spike"] == 50.0
+    assert st["kv"]["v_pre"] == 2.0 and st["kv"]["v_spike"] == 20.0
+    assert abs(st["kv"]["k_slope_median"]) < 1e-12
+    nt = st["near_tie"]
+    assert (nt["top2"], nt["top3"], nt["top8"]) == (0.5, 0.5, 1.0)
+    assert nt["gate_recall"] == 0.5 and nt["stable_trigger"] == 0.0
