@@ -7,6 +7,8 @@ protected.  Three modes run from the same prefilled state:
   off     the BF16 fast path only (r_verify = 0)
   gated   MarginGate: verify rows whose top-1/top-2 margin is below tau
   always  the verifier on every row and step (the always-on baseline, r_verify = 1)
+  gated_mfma, always_mfma  the same with the matrix-core verifier (fixed tiling,
+          batch-invariant, tolerance parity) instead of the canonical one
 tau is calibrated on the fast-path margins of an untimed run of the same length so that
 the trigger rate matches the paper's Llama-3.1-8B operating point (18.56%); the measured
 rate is reported.
@@ -66,6 +68,9 @@ def log(*a):
 
 
 def run_mode(dec, mode, warmup, steps, state, kv_snap, eng, profile_kinds=(), profile_steps=32):
+    # "<mode>_mfma": the same mode with the matrix-core verifier
+    mode, _, ver = mode.partition("_")
+    dec.verifier = "mfma" if ver == "mfma" else "canonical"
     eng.kv_pool.copy_(kv_snap)
     dec.set_state(*state)
     dec.n_repaired.zero_()
@@ -158,7 +163,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--batch", type=int, default=64)
     ap.add_argument("--prompt", type=int, default=512)
-    ap.add_argument("--modes", default="off,gated,always")
+    ap.add_argument("--modes", default="off,gated,always,gated_mfma,always_mfma")
     ap.add_argument("--always-steps", type=int, default=0, help="timed steps of the always mode (0 = --steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=4)
@@ -239,13 +244,14 @@ def main():
             f"seq_det {div['oracle_repair']['seq_det']:.3f}")
     modes = {}
     for mode in args.modes.split(","):
-        steps = always_steps if mode == "always" else args.steps
+        steps = always_steps if mode.startswith("always") else args.steps
         kinds = (mg.KIND_FAST_GEMM, mg.KIND_CANON_GEMV, mg.KIND_FAST_ATTN, mg.KIND_CANON_ATTN) \
             if mode == "gated" and args.profile_steps > 0 else ()
         log(f"[bench] mode {mode}: {args.warmup} warmup + {steps} timed steps")
         modes[mode] = run_mode(dec, mode, args.warmup, steps, state, kv_snap, eng, kinds, args.profile_steps)
         log(f"[bench] mode {mode}: {modes[mode]['ms_per_step']:.3f} ms/step, {modes[mode]['tok_s']:.0f} tok/s, "
             f"r_verify {modes[mode]['r_verify']:.4f}")
+    dec.verifier = "canonical"
     g = modes.get("gated") or next(iter(modes.values()))
     prof = g.pop("prof")
     for m in modes.values():
@@ -293,16 +299,18 @@ def main():
     if "off" in modes:
         t_off = modes["off"]["ms_per_step"]
         ov = {}
-        for m in ("gated", "always"):
+        for m in ("gated", "always", "gated_mfma", "always_mfma"):
             if m in modes:
                 ov[f"inc_{m}"] = modes[m]["ms_per_step"] / t_off - 1
         if "inc_gated" in ov and "inc_always" in ov and ov["inc_gated"] > 0:
             ov["cut"] = ov["inc_always"] / ov["inc_gated"]
+        if "inc_gated_mfma" in ov and "inc_always_mfma" in ov and ov["inc_gated_mfma"] > 0:
+            ov["cut_mfma"] = ov["inc_always_mfma"] / ov["inc_gated_mfma"]
         out["verifier_overhead"] = ov
         # HBM roofline fraction of the fast forward alone (off) and of the verifier alone (its
         # algorithmic bytes per step over the time a mode adds to off)
         rf = {"fast_forward": modes["off"]["hbm_frac"]}
-        for m in ("gated", "always"):
+        for m in ("gated", "always", "gated_mfma", "always_mfma"):
             if m in modes and modes[m]["ms_per_step"] > t_off:
                 rf[f"verifier_{m}"] = modes[m]["verifier_bytes_per_step"] / ((modes[m]["ms_per_step"] - t_off) * 1e-3) / HBM_PEAK
         out["hbm_frac"] = rf

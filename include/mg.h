@@ -136,6 +136,20 @@ mg_status mg_verify_rows(mg_ctx* ctx, int n, const int32_t* rows, const int32_t*
                          const int32_t* positions, const int32_t* page_table, float* v_logits, int32_t* v_tok,
                          uint16_t* v_kvcol, void* stream);
 
+/* A matrix-core verifier for the n listed rows (host count): the BF16 forward on
+ * v_mfma_f32_16x16x32_bf16 (the fast path's kernels) with every projection's split-K
+ * fixed as for 32 rows, so a row's arithmetic depends on neither n nor its place in the
+ * list -- deterministic and batch-invariant by fixed tiling, which is what the
+ * deterministic verifier contract of Sec. 3.2 asks for.  Its order is not the canonical
+ * one of mg_verify_rows: its results match the oracle within the fast path's tolerance,
+ * not bit for bit.  Outputs as mg_verify_rows: v_logits [n][vocab] fp32 (may be NULL),
+ * v_tok[i] = argmax (lowest index on ties), v_kvcol[i] the row's K/V column [L][2][Hkv][hd]
+ * bf16; the cache is read (positions < positions[rows[i]]) and not written.  Shares the
+ * context's workspace with the other calls (one call at a time per context). */
+mg_status mg_verify_rows_mfma(mg_ctx* ctx, int n, const int32_t* rows, const int32_t* tokens,
+                              const int32_t* positions, const int32_t* page_table, float* v_logits, int32_t* v_tok,
+                              uint16_t* v_kvcol, void* stream);
+
 /* (4) Commit and single-column repair (Sec. 3.2): for list entry i with row
  * r = rows[i]: emitted[r] = v_tok[i]; if v_tok[i] != top1[r] the verifier's
  * column v_kvcol[i] overwrites the cache at position positions[r] in every

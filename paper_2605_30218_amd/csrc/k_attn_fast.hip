@@ -6,7 +6,9 @@
 // the group, then k, then v) in split order, adds the bias and rounds to bf16 (the
 // projection's rounding point); rotates q and k (rotate-half RoPE from the fp32
 // cos/sin table, products and sums rounded separately, then bf16); appends K' and V
-// to the paged cache at the row's position p (the tentative column); keeps q' (bf16,
+// to the paged cache at the row's position p (the tentative column) -- or, for the
+// matrix-core verifier, to the row's own column buffer, leaving the cache untouched;
+// keeps q' (bf16,
 // the MFMA A operand) and k'_p, v_p in LDS, and copies the row's page indices for
 // positions < p into LDS.
 // Main loop: wave w takes the pages w, w + 4, ... of positions 0..p-1 (16 positions
@@ -107,9 +109,16 @@ __global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArg
     // ---- RoPE on q and k, tentative K/V append at p, q' / k'_p / v_p into LDS
     {
         const float* csp = a.cs + (size_t)p * HD;  // [pos][i][cos, sin]
-        uint16_t* kdst = a.kv_pool + ((((size_t)a.layer * m.n_pages + ptab[p / 16]) * 2) * m.Hkv + kh) * (size_t)16 * HD +
-                         (size_t)(p % 16) * HD;
-        uint16_t* vdst = kdst + (size_t)m.Hkv * 16 * HD;
+        // the tentative column in the cache, or (own_out) the row's own column buffer
+        uint16_t *kdst, *vdst;
+        if (a.own_out) {
+            kdst = a.own_out + ((size_t)r * m.L + a.layer) * 2 * Nk + (size_t)kh * HD;
+            vdst = kdst + Nk;
+        } else {
+            kdst = a.kv_pool + ((((size_t)a.layer * m.n_pages + ptab[p / 16]) * 2) * m.Hkv + kh) * (size_t)16 * HD +
+                   (size_t)(p % 16) * HD;
+            vdst = kdst + (size_t)m.Hkv * 16 * HD;
+        }
         for (int t2 = t; t2 < (G + 1) * H2; t2 += FA_THREADS) {
             const int head = t2 / H2, ii = t2 % H2;  // head == G: the k head
             const float* s = y + head * HD;

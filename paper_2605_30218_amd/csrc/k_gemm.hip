@@ -250,9 +250,12 @@ __global__ __launch_bounds__(GM_THREADS) void fast_gemm_kernel(FastGemmArgs a) {
         wrow[f] = wok[f] ? a.W[seg] + (size_t)(nl + jl) * K : a.W[0];
     }
 
-    const int nchunks = (K + S::KC - 1) / S::KC;
-    const int c0 = (int)((long)split * nchunks / a.S);
-    const int c1 = (int)((long)(split + 1) * nchunks / a.S);
+    // split boundaries in 128-element units whatever the chunk size, so that a row's
+    // summation order depends only on the split count (the matrix-core verifier fixes it)
+    static_assert(128 % S::KC == 0, "chunks tile the 128-element split unit");
+    const int nchunks = (K + S::KC - 1) / S::KC, nunits = (K + 127) / 128;
+    const int c0 = min(nchunks, (int)((long)split * nunits / a.S) * (128 / S::KC));
+    const int c1 = min(nchunks, (int)((long)(split + 1) * nunits / a.S) * (128 / S::KC));
 
     f32x4_t acc[MT][FT];
 #pragma unroll

@@ -363,6 +363,29 @@ hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, f
 // before anything is written, so emitted may alias top1); on a mismatch the
 // verifier column [L][K|V][Hkv][hd] is copied to the row's current position in
 // every layer, then emitted and the repair counter are updated.
+__global__ void gather_rows_kernel(int n, const int32_t* __restrict__ rows, const int32_t* __restrict__ tokens,
+                                   const int32_t* __restrict__ positions, const int32_t* __restrict__ page_table,
+                                   int maxp, int32_t* __restrict__ out_tok, int32_t* __restrict__ out_pos,
+                                   int32_t* __restrict__ out_pt) {
+    const int i = blockIdx.x;
+    if (i >= n) return;
+    const int r = rows[i];
+    if (threadIdx.x == 0) {
+        out_tok[i] = tokens[r];
+        out_pos[i] = positions[r];
+    }
+    for (int k = threadIdx.x; k < maxp; k += blockDim.x) out_pt[(size_t)i * maxp + k] = page_table[(size_t)r * maxp + k];
+}
+
+hipError_t launch_gather_rows(int n, const int32_t* rows, const int32_t* tokens, const int32_t* positions,
+                              const int32_t* page_table, int maxp, int32_t* out_tok, int32_t* out_pos, int32_t* out_pt,
+                              hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(gather_rows_kernel, dim3(n), dim3(256), 0, s, n, rows, tokens, positions, page_table, maxp,
+                       out_tok, out_pos, out_pt);
+    return hipGetLastError();
+}
+
 __global__ __launch_bounds__(256) void repair_kernel(RowCount rc, const int32_t* __restrict__ rows,
                                                      const int32_t* __restrict__ positions,
                                                      const int32_t* __restrict__ page_table, const int32_t* top1,

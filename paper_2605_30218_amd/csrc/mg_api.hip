@@ -18,12 +18,15 @@ namespace {
 
 constexpr int WPL = 12;
 constexpr int CANON_CHUNK = 256;
+// The matrix-core verifier splits every projection's K as a step of this many rows would,
+// whatever its own row count, so a row's arithmetic never depends on the batch
+constexpr int MFMA_VERIFIER_SPLIT_M = 32;
 constexpr size_t ALIGN = 256;
 
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 struct Plan {
-    size_t rope, x, h, qkv, qrot, att, gu, act, attn_part, gemm_part, top2_ws, vlog, total;
+    size_t rope, x, h, qkv, qrot, att, gu, act, attn_part, gemm_part, top2_ws, vlog, vrows, total;
     int rows_cap, max_pos, chunks_canon;
 };
 
@@ -81,13 +84,19 @@ Plan make_plan(const mg_model_cfg* c, int n_cu) {
     size_t gp = 0;
     for (int M = 1; M <= c->max_batch; ++M)
         for (int k : {0, 1, 2, 3}) {
-            const int S = fast_gemm_splits(M, ps[k].N, ps[k].K, n_cu);
-            const size_t need = (size_t)S * M * ps[k].N;
+            // the step's own split, or the matrix-core verifier's fixed one
+            const int S0 = fast_gemm_splits(M, ps[k].N, ps[k].K, n_cu);
+            const int S1 = fast_gemm_splits(MFMA_VERIFIER_SPLIT_M, ps[k].N, ps[k].K, n_cu);
+            const size_t need = (size_t)(S0 > S1 ? S0 : S1) * M * ps[k].N;
             if (need > gp) gp = need;
         }
     p.gemm_part = o; o += up((gp ? gp : 1) * sizeof(float));
     p.top2_ws = o; o += up(TOP2_WS_BYTES);
     p.vlog = o; o += up((size_t)c->max_batch * c->vocab * sizeof(float));
+    // the matrix-core verifier's compact rows: token, position, page-table row, and the
+    // top-2 pass's margin / gate / row list / count
+    p.vrows = o; o += up((size_t)c->max_batch * (4 + c->max_pages_per_row) * sizeof(int32_t) + 4 * sizeof(int32_t) +
+                         (size_t)c->max_batch * (sizeof(float) + 1));
     p.total = o;
     return p;
 }
@@ -158,7 +167,7 @@ struct ProfScope {
 // for the consuming kernel to sum; the other epilogues run unsplit.
 mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, const uint16_t* const* W,
                     const uint16_t* const* bias, const int* Nseg, int nseg, void* Y, int epi, hipStream_t s,
-                    int* S_out = nullptr) {
+                    int* S_out = nullptr, int split_M = 0) {
     FastGemmArgs a{};
     a.X = X;
     a.M = M;
@@ -173,7 +182,7 @@ mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, const uint16_t* 
     a.N = N;
     a.Y = Y;
     a.part = c->at<float>(c->plan.gemm_part);
-    a.S = epi == FEPI_PART ? fast_gemm_splits(M, N, K, c->n_cu) : 1;
+    a.S = epi == FEPI_PART ? fast_gemm_splits(split_M ? split_M : M, N, K, c->n_cu) : 1;
     if (S_out) *S_out = a.S;
     const double out_bytes = epi == FEPI_PART ? 4.0 * a.S * M * N : (double)M * N * (epi == FEPI_F32 ? 4 : 2);
     const double bytes = 2.0 * N * K + 2.0 * M * K + out_bytes;
@@ -377,12 +386,12 @@ mg_status mg_destroy(mg_ctx* c) {
     return MG_OK;
 }
 
-mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t* positions, const int32_t* page_table,
-                         float* logits, void* stream) {
-    if (!c || !tokens || !positions || !page_table || !logits) return MG_ERR_ARG;
-    if (B < 0 || B > c->cfg.max_batch) return MG_ERR_ARG;
-    if (B == 0) return MG_OK;
-    hipStream_t s = static_cast<hipStream_t>(stream);
+// The fast forward of B rows: token / position / page-table row b at index b.  own_out
+// NULL: the step -- the tentative K/V column of every row is appended to the cache.  Else
+// the matrix-core verifier: the K/V columns go to own_out and the cache is only read;
+// split_M fixes every projection's split-K (0: the row count's own split).
+static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int32_t* positions, const int32_t* page_table,
+                       float* logits, uint16_t* own_out, int split_M, hipStream_t s) {
     const mg_model_cfg& g = c->cfg;
     const ModelDims& m = c->m;
     const int d = g.d_model, Nq = g.n_q_heads * g.head_dim, Nk = g.n_kv_heads * g.head_dim, F = g.d_ffn;
@@ -398,10 +407,10 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
         {
             const uint16_t* W[3] = {c->LW(l, 1), c->LW(l, 2), c->LW(l, 3)};
             const int Ns[3] = {Nq, Nk, Nk};
-            MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 3, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 3, nullptr, FEPI_PART, s, &S, split_M));
         }
         {
-            // QKV split sum + bias + RoPE + tentative K/V append + attention
+            // QKV split sum + bias + RoPE + K/V append (tentative, or own) + attention
             FastAttnArgs a{};
             a.B = B;
             a.part = part;
@@ -418,25 +427,26 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
             a.cs = c->at<float>(c->plan.rope);
             a.kv_pool = c->kv_pool;
             a.out = att;
+            a.own_out = own_out;
             ProfScope ps(c, MG_KIND_FAST_ATTN, s, 0.0);
             HIPCHK(launch_fast_attention(a, s));
         }
         {
             const uint16_t* W[1] = {c->LW(l, 7)};
             const int Ns[1] = {d};
-            MGCHK(fast_gemm(c, att, B, Nq, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, att, B, Nq, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S, split_M));
         }
         HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, c->LW(l, 8), g.rms_eps, x, h, s));
         {
             const uint16_t* W[2] = {c->LW(l, 9), c->LW(l, 10)};
             const int Ns[2] = {F, F};
-            MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 2, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 2, nullptr, FEPI_PART, s, &S, split_M));
         }
         HIPCHK(launch_swiglu_part(B, part, S, F, act, s));
         {
             const uint16_t* W[1] = {c->LW(l, 11)};
             const int Ns[1] = {d};
-            MGCHK(fast_gemm(c, act, B, F, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S));
+            MGCHK(fast_gemm(c, act, B, F, W, nullptr, Ns, 1, nullptr, FEPI_PART, s, &S, split_M));
         }
         const uint16_t* next_gamma = l + 1 < g.n_layers ? c->LW(l + 1, 0) : c->W(1 + WPL * g.n_layers);
         HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, next_gamma, g.rms_eps, x, h, s));
@@ -444,6 +454,39 @@ mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t*
     const uint16_t* W[1] = {c->W(2 + WPL * g.n_layers)};
     const int Ns[1] = {g.vocab};
     MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 1, logits, FEPI_F32, s));
+    return MG_OK;
+}
+
+mg_status mg_decode_step(mg_ctx* c, int B, const int32_t* tokens, const int32_t* positions, const int32_t* page_table,
+                         float* logits, void* stream) {
+    if (!c || !tokens || !positions || !page_table || !logits) return MG_ERR_ARG;
+    if (B < 0 || B > c->cfg.max_batch) return MG_ERR_ARG;
+    if (B == 0) return MG_OK;
+    return fast_forward(c, B, tokens, positions, page_table, logits, nullptr, 0, static_cast<hipStream_t>(stream));
+}
+
+mg_status mg_verify_rows_mfma(mg_ctx* c, int n, const int32_t* rows, const int32_t* tokens, const int32_t* positions,
+                              const int32_t* page_table, float* v_logits, int32_t* v_tok, uint16_t* v_kvcol,
+                              void* stream) {
+    if (!c) return MG_ERR_ARG;
+    if (n == 0) return MG_OK;
+    if (n < 0 || n > c->cfg.max_batch) return MG_ERR_ARG;
+    if (!rows || !tokens || !positions || !page_table || !v_tok || !v_kvcol) return MG_ERR_ARG;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const int maxp = c->cfg.max_pages_per_row, B = c->cfg.max_batch;
+    int32_t* vtok = c->at<int32_t>(c->plan.vrows);
+    int32_t* vpos = vtok + B;
+    int32_t* vrowlist = vpos + B;
+    int32_t* vn = vrowlist + B;
+    int32_t* vpt = vn + 4;
+    float* vmargin = reinterpret_cast<float*>(vpt + (size_t)B * maxp);
+    uint8_t* vgate = reinterpret_cast<uint8_t*>(vmargin + B);
+    float* logits = v_logits ? v_logits : c->at<float>(c->plan.vlog);
+    HIPCHK(launch_gather_rows(n, rows, tokens, positions, page_table, maxp, vtok, vpos, vpt, s));
+    MGCHK(fast_forward(c, n, vtok, vpos, vpt, logits, v_kvcol, MFMA_VERIFIER_SPLIT_M, s));
+    // v_tok = top-1 of each row (lowest index on ties); the gate outputs are scratch
+    HIPCHK(launch_top2(n, c->cfg.vocab, logits, nullptr, 0.0f, v_tok, vmargin, vgate, vrowlist, vn, nullptr,
+                       c->at<void>(c->plan.top2_ws), nullptr, s));
     return MG_OK;
 }
 

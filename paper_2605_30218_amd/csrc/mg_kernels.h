@@ -117,6 +117,7 @@ struct FastAttnArgs {
     const float* cs;            // RoPE table [max_pos][hd] (cos, sin interleaved)
     uint16_t* kv_pool;
     uint16_t* out;              // [B][Hq * hd] bf16
+    uint16_t* own_out;          // NULL: append K'/V at p to the cache; else [B][L][2][Hkv][hd] (the cache is not written)
 };
 hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s);
 
@@ -127,6 +128,10 @@ constexpr size_t TOP2_WS_BYTES = 256 * 128 * 16;
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1,
                        float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* n_gated_host,
                        void* part_ws, const int32_t* n_dev, hipStream_t s);
+// compact copies of the listed rows' token, position and page-table row
+hipError_t launch_gather_rows(int n, const int32_t* rows, const int32_t* tokens, const int32_t* positions,
+                              const int32_t* page_table, int maxp, int32_t* out_tok, int32_t* out_pos, int32_t* out_pt,
+                              hipStream_t s);
 hipError_t launch_repair(int n_host, const int32_t* n_dev, int cap, const int32_t* rows, const int32_t* positions,
                          const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
                          const uint16_t* v_kvcol, const ModelDims& m, uint16_t* kv_pool, int32_t* emitted,

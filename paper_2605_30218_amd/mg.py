@@ -53,6 +53,7 @@ SIGNATURES = {
     "mg_verify_rows": (I, [P, I, P, P, P, P, P, P, P, P, P]),
     "mg_repair_kv_column": (I, [P, I, P, P, P, P, P, P, P, P, P, P]),
     "mg_repair_kv_column_action": (I, [P, I, P, P, P, P, P, P, P, P, P, I, P]),
+    "mg_verify_rows_mfma": (I, [P, I, P, P, P, P, P, P, P, P]),
     "mg_prefill": (I, [P, I, P, P, P, P, P]),
     "mg_advance": (I, [P, I, P, P, P, P]),
     "mg_profile_begin": (I, [P, I, I]),
@@ -188,6 +189,11 @@ class Engine:
         _check("mg_repair_kv_column", self.lib.mg_repair_kv_column(
             self.ctx, n, _ptr(rows), _ptr(n_dev), _ptr(positions), _ptr(page_table), _ptr(top1), _ptr(v_tok),
             _ptr(v_kvcol), _ptr(emitted), _ptr(n_repaired), _stream(stream)))
+
+    def verify_rows_mfma(self, n, rows, tokens, positions, page_table, v_logits, v_tok, v_kvcol, stream=None):
+        _check("mg_verify_rows_mfma", self.lib.mg_verify_rows_mfma(
+            self.ctx, n, _ptr(rows), _ptr(tokens), _ptr(positions), _ptr(page_table), _ptr(v_logits), _ptr(v_tok),
+            _ptr(v_kvcol), _stream(stream)))
 
     def repair_kv_column_action(self, n, rows, n_dev, positions, page_table, top1, v_tok, v_kvcol, emitted,
                                 n_repaired, action, stream=None):

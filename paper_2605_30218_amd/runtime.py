@@ -46,6 +46,10 @@ class GatedDecoder:
         # differ), or a variant for the repair-action measurements (mg.REPAIR_TOKEN_ONLY,
         # mg.REPAIR_COPY_ALWAYS)
         self.repair_action = mg.REPAIR_ON_MISMATCH
+        # the verifier: "canonical" (mg_verify_rows, the oracle's order bit for bit) or "mfma"
+        # (mg_verify_rows_mfma: fixed-tile matrix-core forward, batch-invariant, tolerance
+        # parity)
+        self.verifier = "canonical"
         # the gate mirrors its count into pinned host memory; the host polls it instead of
         # synchronising the stream
         self._count_dev, self._count = mg.host_count_slot()
@@ -80,7 +84,12 @@ class GatedDecoder:
                         margin=self.margin.cpu().numpy(), gate=self.gate.cpu().numpy(),
                         positions=self.positions.cpu().numpy(), tokens=self.tokens.cpu().numpy())
         if n:
-            e.verify_rows(n, rows, None, self.tokens, self.positions, self.page_table, None, self.v_tok, self.v_kvcol)
+            if self.verifier == "mfma":
+                e.verify_rows_mfma(n, rows, self.tokens, self.positions, self.page_table, None, self.v_tok,
+                                   self.v_kvcol)
+            else:
+                e.verify_rows(n, rows, None, self.tokens, self.positions, self.page_table, None, self.v_tok,
+                              self.v_kvcol)
             if self.repair_action == mg.REPAIR_ON_MISMATCH:
                 e.repair_kv_column(n, rows, None, self.positions, self.page_table, self.top1, self.v_tok, self.v_kvcol,
                                    self.top1, self.n_repaired)

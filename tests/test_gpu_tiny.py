@@ -348,3 +348,63 @@ def test_verifier_batch_invariance_1_to_256(wide):
     rl, rt, rc = p.om.verify_rows(np.array([target], np.int32), last, pos0, p.pt)
     np.testing.assert_array_equal(rl[0].view(np.uint32), ref[0])
     np.testing.assert_array_equal(rc[0], ref[2])
+
+
+def test_mfma_verifier_batch_invariance_1_to_256(wide):
+    """The matrix-core verifier (fixed tiling: every projection's split-K fixed whatever the
+    row count): a row's logits, token and K/V column are bit-identical for every list size
+    1..256 and place (the chunking changes at 129 rows, the split boundaries do not)."""
+    p, last, pos0 = wide
+    e = p.eng
+    pt = dev_i32(p.pt)
+    toks, poss = dev_i32(last), dev_i32(pos0)
+    rng = np.random.default_rng(19)
+    target = 101
+
+    def run(rows):
+        n = len(rows)
+        vl = torch.empty((n, V), dtype=torch.float32, device="cuda")
+        vt = torch.empty(n, dtype=torch.int32, device="cuda")
+        vc = torch.empty((n, e.col_elems), dtype=torch.int16, device="cuda")
+        e.verify_rows_mfma(n, dev_i32(rows), toks, poss, pt, vl, vt, vc)
+        return vl, vt, vc
+
+    before = u16(e.kv_pool).copy()
+    vl0, vt0, vc0 = run([target])
+    ref = (vl0[0].cpu().numpy().view(np.uint32), int(vt0[0].item()), u16(vc0[0]))
+    for n in list(range(2, 257, 3)) + [128, 129, 256]:
+        others = rng.choice(np.setdiff1d(np.arange(256), [target]), n - 1, replace=False)
+        place = [0, n - 1, int(rng.integers(0, n))][n % 3]
+        rows = list(others[:place]) + [target] + list(others[place:])
+        vl, vt, vc = run(rows)
+        assert np.array_equal(vl[place].cpu().numpy().view(np.uint32), ref[0]), n
+        assert int(vt[place].item()) == ref[1], n
+        assert np.array_equal(u16(vc[place]), ref[2]), n
+    np.testing.assert_array_equal(u16(e.kv_pool), before)  # the cache is only read
+
+
+def test_mfma_verifier_within_tolerance_of_the_oracle(wide):
+    """Against the oracle's canonical verifier on the same cache: logits within the fast
+    path's tolerance (normwise 1e-2), the K/V column within bf16 rounding of the canonical
+    one, the token the oracle's argmax except at a near-tie of the oracle logits."""
+    p, last, pos0 = wide
+    e = p.eng
+    rows = np.array([0, 5, 77, 130, 255], np.int32)
+    n = rows.size
+    vl = torch.empty((n, V), dtype=torch.float32, device="cuda")
+    vt = torch.empty(n, dtype=torch.int32, device="cuda")
+    vc = torch.empty((n, e.col_elems), dtype=torch.int16, device="cuda")
+    e.verify_rows_mfma(n, dev_i32(rows), dev_i32(last), dev_i32(pos0), dev_i32(p.pt), vl, vt, vc)
+    torch.cuda.synchronize()
+    p.sync_oracle_cache()
+    rl, rt, rc = p.om.verify_rows(rows, last, pos0, p.pt)
+    gl, gt, gc = vl.cpu().numpy(), vt.cpu().numpy(), u16(vc)
+    for i in range(n):
+        err = normwise(gl[i], rl[i].astype(np.float64))
+        assert err < 1e-2, (i, err)
+        if gt[i] != rt[i]:
+            srt = np.sort(rl[i])[::-1]
+            assert srt[0] - srt[1] <= 2 * np.abs(gl[i] - rl[i]).max(), i
+    f = lambda u: (u.astype(np.uint32) << 16).view(np.float32)  # noqa: E731
+    g32, r32 = f(gc), f(rc)
+    assert np.all(np.abs(g32 - r32) <= 0.05 * np.abs(r32) + 0.05)
