@@ -41,7 +41,11 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     constexpr int HP = HD / 2;                // d pairs (words per V row)
     constexpr int HPT = 256 / HP;             // head groups over the block's threads
     constexpr int NPG = ATT_MAXC / 16;        // pages per chunk
-    constexpr int UB = 8;                     // positions per batch of LDS reads
+#ifndef MG_ATT_UB
+#define MG_ATT_UB 16
+#endif
+    constexpr int UB = MG_ATT_UB;             // positions per batch of LDS reads
+    static_assert(UB % 4 == 0 && ATT_MAXC % UB == 0, "whole float4 batches");
     static_assert(NLD * 256 == ATT_MAXC * U4, "pieces must divide evenly");
 
     __shared__ __attribute__((aligned(16))) uint32_t vs[ATT_MAXC * HP];
@@ -193,9 +197,12 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
         for (int u = 0; u < NH; ++u) {
             const int h = hg + HPT * u;
             if (h < G) {
-                const float4 e0 = *reinterpret_cast<const float4*>(ps + h * ATT_MAXC + j);
-                const float4 e1 = *reinterpret_cast<const float4*>(ps + h * ATT_MAXC + j + 4);
-                const float e[UB] = {e0.x, e0.y, e0.z, e0.w, e1.x, e1.y, e1.z, e1.w};
+                float e[UB];
+#pragma unroll
+                for (int q4 = 0; q4 < UB / 4; ++q4) {
+                    const float4 t4 = *reinterpret_cast<const float4*>(ps + h * ATT_MAXC + j + 4 * q4);
+                    e[4 * q4] = t4.x; e[4 * q4 + 1] = t4.y; e[4 * q4 + 2] = t4.z; e[4 * q4 + 3] = t4.w;
+                }
 #pragma unroll
                 for (int b = 0; b < UB; ++b) {
                     lsum[u] = lsum[u] + e[b];
