@@ -41,6 +41,11 @@ mg_status mg_op_probe_divsqrt(int64_t n, const float* a, const float* b, float* 
 size_t mg_op_linear_workspace_bytes(int n, int N, int K);
 mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const uint16_t* W, const uint16_t* bias,
                        float* Y, void* workspace, size_t workspace_bytes, void* stream);
+/* The launch the fast path's MFMA GEMM makes for n rows of an N x K projection on a
+ * device of n_cu compute units: *S = split-K factor, *waves = waves per block (4 or
+ * 8).  Host logic only (no device call); the same limits on n, N and K as above,
+ * n_cu > 0, else MG_ERR_ARG. */
+mg_status mg_op_fast_gemm_config(int n, int N, int K, int n_cu, int* S, int* waves);
 
 /* y[r] = RMSNorm(x[r]) * gamma with the canonical sum of squares (one wave per
  * row, CDOT order), r < n; d % 8 == 0.  bf16 in, bf16 out. */

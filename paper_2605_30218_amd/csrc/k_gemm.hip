@@ -1,9 +1,9 @@
 // k_gemm.hip -- the fast path's weight-streaming projection on MFMA (gfx950).
 //
 // Y[M][N] = X[M][K] * W[N][K]^T with v_mfma_f32_16x16x32_bf16, M <= 256 (rows
-// padded to 16-row tiles).  A block of 8 waves owns 128 output features; a wave
-// owns 16 of them for all rows (the activation chunk staged in LDS serves all
-// eight).  The block walks its K range in chunks of KC, requesting later chunks while
+// padded to 16-row tiles).  A block of NW waves (8, or 4 on the direct-to-LDS path)
+// owns 16 NW output features; a wave owns 16 of them for all rows (the activation
+// chunk staged in LDS serves all of the block's waves).  The block walks its K range in chunks of KC, requesting later chunks while
 // the MFMAs of the current one run.  Two operand paths:
 //  * K % 128 == 0 and up to 128 rows (128-element chunks): both operands go through
 //    LDS by direct-to-LDS loads -- each wave's weights through its own ring of DEPTH
@@ -34,10 +34,8 @@ typedef float f32x4_t __attribute__((ext_vector_type(4)));
 #ifndef MG_GEMM_KC_SMALL
 #define MG_GEMM_KC_SMALL 128
 #endif
-#ifndef MG_GEMM_NW
-#define MG_GEMM_NW 8  // waves per block (measured: 8 beats 4 and 16)
-#endif
-constexpr int GM_NW = MG_GEMM_NW, GM_THREADS = 64 * MG_GEMM_NW;
+// waves per block of the register operand path (measured: 8 beats 4 and 16)
+constexpr int GM_NW = 8, GM_THREADS = 64 * GM_NW;
 // K per chunk for a tile of MT 16-row tiles (host and device must agree)
 __host__ __device__ constexpr int gemm_kc(int MT) { return MT <= 4 ? MG_GEMM_KC_SMALL : MT <= 8 ? 128 : 64; }
 
@@ -145,10 +143,14 @@ __device__ __forceinline__ void issue_w_lds(const uint16_t* tile, int K, int kc,
 }
 
 // this wave's XI of the 4 MT activation loads of chunk kc (rows past M read row M - 1; with
-// MT = 1 two waves issue each load, writing the same bytes)
-template <int MT>
+// fewer loads than waves, several waves issue each load, writing the same bytes)
+// activation loads per wave per chunk (the 4 MT loads of a chunk shared by the NW waves)
+__host__ __device__ constexpr int gemm_xi(int MT, int NW) { return 4 * MT >= NW ? 4 * MT / NW : 1; }
+
+template <int MT, int NW>
 __device__ __forceinline__ void issue_x_lds(const FastGemmArgs& a, int kc, int wave, int lane, uint4* xt) {
-    constexpr int NI = 4 * MT, XI = MT >= 2 ? MT / 2 : 1;
+    constexpr int NI = 4 * MT, XI = gemm_xi(MT, NW);
+    static_assert(XI * NW >= NI, "the block's waves cover every activation load");
     const int r = lane >> 4, g = lane & 15;
 #pragma unroll
     for (int t = 0; t < XI; ++t) {
@@ -228,13 +230,14 @@ __device__ __forceinline__ void mfma_chunk(const unsigned char* buf, int jl, int
     }
 }
 
-template <int MT, int FT, int EPI, bool LDSP>
-__global__ __launch_bounds__(GM_THREADS) void fast_gemm_kernel(FastGemmArgs a) {
+template <int MT, int NW, int FT, int EPI, bool LDSP>
+__global__ __launch_bounds__(64 * NW) void fast_gemm_kernel(FastGemmArgs a) {
     using S = GemmShape<MT>;
+    static_assert(NW == GM_NW || (LDSP && S::LDSW), "4-wave blocks only on the direct-to-LDS path");
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int jl = lane & 15, q = lane >> 4;
     const int nb = blockIdx.x, split = blockIdx.y;
-    const int FB = 16 * GM_NW * FT;  // features per block
+    const int FB = 16 * NW * FT;  // features per block
     const int K = a.K, M = a.M;
 
     const uint16_t* wrow[FT];
@@ -265,13 +268,13 @@ __global__ __launch_bounds__(GM_THREADS) void fast_gemm_kernel(FastGemmArgs a) {
 
     if constexpr (LDSP && S::LDSW) {
         static_assert(FT == 1 && S::NST == 4, "LDS operand path: one 16-feature tile, 128-element chunks");
-        constexpr int D = S::DEPTH, XI = MT >= 2 ? MT / 2 : 1;
-        __shared__ __attribute__((aligned(16))) uint4 wring[D][GM_NW][256];
+        constexpr int D = S::DEPTH, XI = gemm_xi(MT, NW);
+        __shared__ __attribute__((aligned(16))) uint4 wring[D][NW][256];
         __shared__ __attribute__((aligned(16))) uint4 xt[2][MT * 256];
         // the tile's first weight row (a tile past N reads rows 0 .. 15: results discarded)
         const uint16_t* tile = wok[0] ? wrow[0] - (size_t)jl * K : a.W[0];
         if (c0 < c1) {
-            issue_x_lds<MT>(a, c0 * S::KC, wave, lane, xt[c0 & 1]);
+            issue_x_lds<MT, NW>(a, c0 * S::KC, wave, lane, xt[c0 & 1]);
 #pragma unroll
             for (int d = 0; d < D - 1; ++d)
                 if (c0 + d < c1) issue_w_lds(tile, K, (c0 + d) * S::KC, lane, wring[(c0 + d) % D][wave]);
@@ -287,7 +290,7 @@ __global__ __launch_bounds__(GM_THREADS) void fast_gemm_kernel(FastGemmArgs a) {
         // complete: every wave waited for its share before the last barrier.
         int c = c0;
         for (; c + D - 1 < c1; ++c) {
-            issue_x_lds<MT>(a, (c + 1) * S::KC, wave, lane, xt[(c + 1) & 1]);
+            issue_x_lds<MT, NW>(a, (c + 1) * S::KC, wave, lane, xt[(c + 1) & 1]);
             issue_w_lds(tile, K, (c + D - 1) * S::KC, lane, wring[(c + D - 1) % D][wave]);
             __builtin_amdgcn_sched_barrier(0);
             wait_vmcnt<4 * (D - 1) + XI>();
@@ -299,7 +302,7 @@ __global__ __launch_bounds__(GM_THREADS) void fast_gemm_kernel(FastGemmArgs a) {
         // the last D - 1 chunks (or fewer): no more weights to request
         for (; c < c1; ++c) {
             const bool more = c + 1 < c1;
-            if (more) issue_x_lds<MT>(a, (c + 1) * S::KC, wave, lane, xt[(c + 1) & 1]);
+            if (more) issue_x_lds<MT, NW>(a, (c + 1) * S::KC, wave, lane, xt[(c + 1) & 1]);
             __builtin_amdgcn_sched_barrier(0);
             wait_vmcnt<0>();
             mfma_chunk_lds<MT>(wring[c % D][wave], xt[c & 1], jl, q, acc);
@@ -377,72 +380,152 @@ static int mt_for(int M) {
     return t <= 1 ? 1 : t <= 2 ? 2 : t <= 4 ? 4 : t <= 8 ? 8 : 16;
 }
 
-static int g_n_cu = 256;
-// One 16-feature B tile per wave: 8-wave blocks of 128 features with one tile each
-// measured faster than two tiles per wave (fewer blocks, more registers per wave).
+// One 16-feature B tile per wave: blocks of 16 NW features with one tile each measured
+// faster than two tiles per wave (fewer blocks, more registers per wave).
 constexpr int GM_FT = 1;
+constexpr int LDS_PER_CU = 160 * 1024;
 
-int fast_gemm_splits(int M, int N, int K, int n_cu) {
-    g_n_cu = n_cu;
+// whole 128-element chunks take both operands through LDS by direct-to-LDS loads
+static bool lds_path(int M, int K) { return gemm_kc(mt_for(M)) == 128 && K % 128 == 0; }
+
+// blocks of NW waves that fit on one CU at once on the direct-to-LDS path (its LDS: the
+// weight ring of DEPTH x NW stages of 4 KiB and the activation double buffer of 2 x MT x 4 KiB)
+static int lds_slots(int MT, int NW) {
+    const int depth = MT <= 4 ? 3 : 2;
+    const int bytes = (depth * NW + 2 * MT) * 4096;
+    return LDS_PER_CU / bytes > 1 ? LDS_PER_CU / bytes : 1;
+}
+
+// Launch cost of NW-wave blocks with S splits on the direct-to-LDS path.  Launches whose
+// blocks are all resident at once (one round) come first, compared by the weight bytes
+// of the busiest CU, then the resident waves (more requests in flight), the split count
+// (partial-tile traffic), and a preference for 4-wave blocks at up to 16 rows (measured
+// faster there) and for 8-wave blocks above.  Launches of several rounds already have
+// blocks enough: fewest splits first, then the block size.  A block streams 16 NW
+// features over its split's 128-element units (splits differ by at most one unit).
+struct LaunchCost {
+    int rounds;
+    long cu_bytes;
+    long waves;
+    int S, pref;
+    bool operator<(const LaunchCost& o) const {
+        if ((rounds == 1) != (o.rounds == 1)) return rounds == 1;
+        if (rounds != 1) {
+            if (S != o.S) return S < o.S;
+            if (pref != o.pref) return pref < o.pref;
+            return cu_bytes < o.cu_bytes;
+        }
+        if (cu_bytes != o.cu_bytes) return cu_bytes < o.cu_bytes;
+        if (waves != o.waves) return waves > o.waves;
+        if (S != o.S) return S < o.S;
+        return pref < o.pref;
+    }
+};
+
+static LaunchCost lds_cost(int M, int N, int K, int S, int NW, int n_cu) {
+    const int MT = mt_for(M), slots = lds_slots(MT, NW);
+    const long nb = (N + 16 * NW * GM_FT - 1) / (16 * NW * GM_FT), blocks = nb * S;
+    const long units = (K + 127) / 128, split_units = (units + S - 1) / S;
+    const long per_cu = (blocks + n_cu - 1) / n_cu;
+    LaunchCost c;
+    c.rounds = (int)((per_cu + slots - 1) / slots);
+    c.cu_bytes = per_cu * split_units * 128 * 16 * NW * GM_FT * 2;
+    c.waves = (blocks < (long)n_cu * slots ? blocks : (long)n_cu * slots) * NW;
+    c.S = S;
+    // several rounds: two 4-wave blocks per CU overlap one block's start with the other's
+    // stream (measured on the 128256-feature LM head); one round: as stated above
+    if (c.rounds != 1) c.pref = (NW == 4) == (lds_slots(MT, 4) >= 2) ? 0 : 1;
+    else c.pref = (NW == 4) == (M <= 16) ? 0 : 1;
+    return c;
+}
+
+// the most splits the partial tiles allow: each split at least 4 chunks, and the partial
+// tiles (S*M*N fp32, written once and read once by the consumer) at most an eighth of
+// the weight bytes (measured at 64 rows: 5.54 ms per fast step against 5.69 with a quarter)
+static int max_splits(int M, int K) {
     const int KC = gemm_kc(mt_for(M));
     const int nchunks = (K + KC - 1) / KC;
-    const int FB = 16 * GM_NW * GM_FT;
-    const int nb = (N + FB - 1) / FB;
-    // enough blocks for about one per CU (two for small batches, whose blocks carry
-    // little MFMA work per weight byte), each with at least 4 chunks, and the
-    // partial tiles (S*M*N fp32, written once and read once by the consumer) at most
-    // an eighth of the weight bytes (measured at 64 rows: 5.54 ms per fast step against
-    // 5.69 with two blocks per CU and a quarter)
-#ifndef MG_GEMM_BLOCKS_PER_CU
-#define MG_GEMM_BLOCKS_PER_CU 1
-#endif
-    const int target = (M <= 16 ? 2 * MG_GEMM_BLOCKS_PER_CU : MG_GEMM_BLOCKS_PER_CU) * n_cu;
-    int S = (target + nb - 1) / nb;
     const int by_chunks = nchunks / 4 > 1 ? nchunks / 4 : 1;
-#ifndef MG_GEMM_TRAFFIC_DIV
-#define MG_GEMM_TRAFFIC_DIV 16
-#endif
-    const long by_traffic = (long)K / ((long)MG_GEMM_TRAFFIC_DIV * (M < 16 ? 16 : M));
-    if (S > by_chunks) S = by_chunks;
+    const long by_traffic = (long)K / (16L * (M < 16 ? 16 : M));
+    int S = by_chunks;
     if (S > by_traffic) S = (int)by_traffic;
     if (S > 32) S = 32;
     return S < 1 ? 1 : S;
 }
 
-template <int MT, int FT, int EPI>
-static void launch_epi(const FastGemmArgs& a, dim3 g, hipStream_t s) {
-    // whole 128-element chunks take both operands through LDS by direct-to-LDS loads
-    if (gemm_kc(MT) == 128 && a.K % 128 == 0)
-        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, true>), g, dim3(GM_THREADS), 0, s, a);
-    else
-        hipLaunchKernelGGL((fast_gemm_kernel<MT, FT, EPI, false>), g, dim3(GM_THREADS), 0, s, a);
+// waves per block for a launch with S splits
+static int fast_gemm_waves(int M, int N, int K, int S, int n_cu) {
+    if (!lds_path(M, K)) return GM_NW;
+    return lds_cost(M, N, K, S, 4, n_cu) < lds_cost(M, N, K, S, 8, n_cu) ? 4 : 8;
 }
 
-template <int MT, int FT>
+int fast_gemm_splits(int M, int N, int K, int n_cu) {
+    const int Smax = max_splits(M, K);
+    if (lds_path(M, K)) {
+        // the cheapest (splits, waves) pair; the launch picks the waves again for its S
+        int best_S = 1;
+        LaunchCost best = lds_cost(M, N, K, 1, 8, n_cu);
+        for (int S = 1; S <= Smax; ++S)
+            for (int NW : {8, 4}) {
+                const LaunchCost c = lds_cost(M, N, K, S, NW, n_cu);
+                if (c < best) { best = c; best_S = S; }
+            }
+        return best_S;
+    }
+    // register operand path: enough 8-wave blocks for about one per CU (two for small
+    // batches, whose blocks carry little MFMA work per weight byte)
+    const int nb = (N + 16 * GM_NW * GM_FT - 1) / (16 * GM_NW * GM_FT);
+    const int target = (M <= 16 ? 2 : 1) * n_cu;
+    const int S = (target + nb - 1) / nb;
+    return S < Smax ? S : Smax;
+}
+
+void fast_gemm_config(int M, int N, int K, int n_cu, int* S, int* waves) {
+    *S = fast_gemm_splits(M, N, K, n_cu);
+    *waves = fast_gemm_waves(M, N, K, *S, n_cu);
+}
+
+template <int MT, int NW, int FT, int EPI>
+static void launch_epi(const FastGemmArgs& a, dim3 g, hipStream_t s) {
+    if constexpr (NW == GM_NW) {
+        if (!(gemm_kc(MT) == 128 && a.K % 128 == 0)) {
+            hipLaunchKernelGGL((fast_gemm_kernel<MT, NW, FT, EPI, false>), g, dim3(64 * NW), 0, s, a);
+            return;
+        }
+    }
+    if constexpr (gemm_kc(MT) == 128)
+        hipLaunchKernelGGL((fast_gemm_kernel<MT, NW, FT, EPI, true>), g, dim3(64 * NW), 0, s, a);
+}
+
+template <int MT, int NW, int FT>
 static void launch_ft(const FastGemmArgs& a, int epi, dim3 g, hipStream_t s) {
     switch (epi) {
-        case FEPI_BF16: launch_epi<MT, FT, FEPI_BF16>(a, g, s); break;
-        case FEPI_PART: launch_epi<MT, FT, FEPI_PART>(a, g, s); break;
-        default: launch_epi<MT, FT, FEPI_F32>(a, g, s); break;
+        case FEPI_BF16: launch_epi<MT, NW, FT, FEPI_BF16>(a, g, s); break;
+        case FEPI_PART: launch_epi<MT, NW, FT, FEPI_PART>(a, g, s); break;
+        default: launch_epi<MT, NW, FT, FEPI_F32>(a, g, s); break;
     }
 }
 
 template <int MT>
-static void launch_mt(const FastGemmArgs& a, int epi, hipStream_t s) {
-    dim3 g((a.N + 16 * GM_NW * GM_FT - 1) / (16 * GM_NW * GM_FT), a.S);
-    launch_ft<MT, GM_FT>(a, epi, g, s);
+static void launch_mt(const FastGemmArgs& a, int epi, int NW, hipStream_t s) {
+    dim3 g((a.N + 16 * NW * GM_FT - 1) / (16 * NW * GM_FT), a.S);
+    if constexpr (gemm_kc(MT) == 128) {
+        if (NW == 4) return launch_ft<MT, 4, GM_FT>(a, epi, g, s);
+    }
+    launch_ft<MT, GM_NW, GM_FT>(a, epi, g, s);
 }
 
 hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s) {
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
     if (a.K < 8 || a.K % 8 || a.N % 16) return hipErrorInvalidValue;
     if (epi != FEPI_PART && a.S != 1) return hipErrorInvalidValue;  // only partial tiles may be split
+    const int NW = fast_gemm_waves(a.M, a.N, a.K, a.S, a.n_cu > 0 ? a.n_cu : 256);
     switch (mt_for(a.M)) {
-        case 1: launch_mt<1>(a, epi, s); break;
-        case 2: launch_mt<2>(a, epi, s); break;
-        case 4: launch_mt<4>(a, epi, s); break;
-        case 8: launch_mt<8>(a, epi, s); break;
-        default: launch_mt<16>(a, epi, s); break;
+        case 1: launch_mt<1>(a, epi, NW, s); break;
+        case 2: launch_mt<2>(a, epi, NW, s); break;
+        case 4: launch_mt<4>(a, epi, NW, s); break;
+        case 8: launch_mt<8>(a, epi, NW, s); break;
+        default: launch_mt<16>(a, epi, NW, s); break;
     }
     return hipGetLastError();
 }

@@ -183,6 +183,7 @@ mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, const uint16_t* 
     a.Y = Y;
     a.part = c->at<float>(c->plan.gemm_part);
     a.S = epi == FEPI_PART ? fast_gemm_splits(split_M ? split_M : M, N, K, c->n_cu) : 1;
+    a.n_cu = c->n_cu;
     if (S_out) *S_out = a.S;
     const double out_bytes = epi == FEPI_PART ? 4.0 * a.S * M * N : (double)M * N * (epi == FEPI_F32 ? 4 : 2);
     const double bytes = 2.0 * N * K + 2.0 * M * K + out_bytes;
@@ -659,11 +660,18 @@ mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const 
     a.Nseg[0] = N;
     a.N = N;
     a.Y = Y;
-    a.S = fast_gemm_splits(n, N, K, device_cu_count());
+    a.n_cu = device_cu_count();
+    a.S = fast_gemm_splits(n, N, K, a.n_cu);
     a.part = static_cast<float*>(workspace);
     if (a.S == 1) return launch_fast_gemm(a, FEPI_F32, s) == hipSuccess ? MG_OK : MG_ERR_HIP;
     if (launch_fast_gemm(a, FEPI_PART, s) != hipSuccess) return MG_ERR_HIP;
     return launch_sum_partials(a.part, a.S, (int64_t)n * N, Y, s) == hipSuccess ? MG_OK : MG_ERR_HIP;
+}
+
+mg_status mg_op_fast_gemm_config(int n, int N, int K, int n_cu, int* S, int* waves) {
+    if (n <= 0 || n > 256 || N <= 0 || K <= 0 || K % 8 || N % 16 || n_cu <= 0 || !S || !waves) return MG_ERR_ARG;
+    fast_gemm_config(n, N, K, n_cu, S, waves);
+    return MG_OK;
 }
 
 mg_status mg_op_rmsnorm(int n, int d, const uint16_t* x, const uint16_t* gamma, float eps, uint16_t* y, void* stream) {

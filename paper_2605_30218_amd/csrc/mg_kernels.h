@@ -64,10 +64,13 @@ struct FastGemmArgs {
     void* Y;                   // FEPI_BF16: bf16 [M][N]; FEPI_F32: fp32 [M][N]
     float* part;               // FEPI_PART: fp32 partial tiles [S][M][N]
     int S;                     // split-K factor (1 unless FEPI_PART)
+    int n_cu;                  // compute units of the device (chooses the waves per block)
 };
 hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s);
 hipError_t launch_sum_partials(const float* part, int S, int64_t n, float* out, hipStream_t s);
 int fast_gemm_splits(int M, int N, int K, int n_cu);
+// the split count and the waves per block a launch of M rows uses
+void fast_gemm_config(int M, int N, int K, int n_cu, int* S, int* waves);
 
 // fast-path consumers of split partial tiles
 // x[r] = bf16(x[r] + bf16(sum_s part[s][r])) (skipped when part == NULL; with embed != NULL,

@@ -64,6 +64,7 @@ SIGNATURES = {
     "mg_op_probe_divsqrt": (I, [I64, P, P, P, P, P]),
     "mg_op_linear_workspace_bytes": (SZ, [I, I, I]),
     "mg_op_linear": (I, [I, I, I, I, P, P, P, P, P, SZ, P]),
+    "mg_op_fast_gemm_config": (I, [I, I, I, I, P, P]),
     "mg_op_rmsnorm": (I, [I, I, P, P, F, P, P]),
 }
 
@@ -255,6 +256,14 @@ def op_linear(canon, X, W):
     _check("mg_op_linear", lib.mg_op_linear(int(canon), n, N, K, X.data_ptr(), W.data_ptr(), None, Y.data_ptr(),
                                             ws.data_ptr(), wsb, _stream()))
     return Y
+
+
+def fast_gemm_config(n, N, K, n_cu=256):
+    """(split-K factor, waves per block) of the fast GEMM launch for n rows of an N x K
+    projection on a device of n_cu compute units (host logic, no device call)."""
+    S, w = C.c_int(0), C.c_int(0)
+    _check("mg_op_fast_gemm_config", load().mg_op_fast_gemm_config(n, N, K, n_cu, C.byref(S), C.byref(w)))
+    return S.value, w.value
 
 
 def op_rmsnorm(x, gamma, eps):

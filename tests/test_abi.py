@@ -93,3 +93,29 @@ def test_load_raises_when_library_missing(monkeypatch, tmp_path):
     monkeypatch.setattr(mg, "LIB_PATH", str(tmp_path / "libmg.so"))
     with pytest.raises(RuntimeError, match="no fallback"):
         mg.load()
+
+
+def test_fast_gemm_launch_rule():
+    """The fast GEMM's (split-K factor, waves per block) choice, host logic only: on the
+    Llama-3.1-8B projections at 64 rows it takes the launches measured fastest per shape
+    (every block resident at once with the least weight per CU, 4-wave blocks for the
+    several-round LM head); splits stay within the partial-tile cap; the register operand
+    path (K % 128 != 0, or more than 128 rows) keeps 8-wave blocks."""
+    llama = {(6144, 4096): (4, 8), (4096, 4096): (4, 4), (28672, 4096): (1, 8), (4096, 14336): (8, 8),
+             (128256, 4096): (1, 4)}
+    for (N, K), want in llama.items():
+        assert mg.fast_gemm_config(64, N, K) == want, (N, K)
+    for n in (1, 9, 16, 20, 33, 64, 100, 128, 129, 256):
+        for (N, K) in [(48, 688), (64, 1032), (256, 4096), (4096, 4096), (6144, 4096), (28672, 4096), (4096, 14336),
+                       (128256, 4096), (3584, 18944), (152064, 5120)]:
+            S, w = mg.fast_gemm_config(n, N, K)
+            assert w in (4, 8) and 1 <= S <= 32
+            assert S == 1 or S * max(n, 16) * 16 <= K  # partial tiles at most an eighth of the weight bytes
+            if K % 128 or n > 128:
+                assert w == 8
+    # the exact-integer GPU cases cover both block sizes at 2, 4 and 8 row tiles
+    assert [mg.fast_gemm_config(n, 16512, 512)[1] for n in (20, 64, 128)] == [8, 8, 8]
+    assert [mg.fast_gemm_config(*c)[1] for c in [(9, 64, 512), (20, 128, 1024), (64, 256, 4096), (128, 96, 2048)]] \
+        == [4, 4, 4, 4]
+    with pytest.raises(Exception):
+        mg.fast_gemm_config(0, 64, 512)

@@ -90,14 +90,16 @@ def test_fast_gemm_within_tolerance(n, N, K):
 
 
 # (64, 256, 4096), (20, 128, 1024), (128, 96, 2048), (9, 64, 512): the direct-to-LDS
-# operand path at 4-, 2-, 8- and 1-tile row counts; the others the register path
+# operand path with 4-wave blocks at 4-, 2-, 8- and 1-tile row counts; (20|64|128, 16512,
+# 512) the same path with 8-wave blocks; the others the register path
 @pytest.mark.parametrize("n,N,K", [(3, 48, 688), (64, 256, 4096), (130, 64, 1032), (20, 128, 1024), (128, 96, 2048),
-                                   (9, 64, 512)])
+                                   (9, 64, 512), (20, 16512, 512), (64, 16512, 512), (128, 16512, 512)])
 def test_fast_gemm_small_integers_exact(n, N, K):
     X = synth.small_int_bf16((n, K), seed=21)
     W = synth.small_int_bf16((N, K), seed=22)
     Y = mg.op_linear(False, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
-    ref = mgo.f32_from_bf16(X).astype(np.int64) @ mgo.f32_from_bf16(W).astype(np.int64).T
+    # integer products summed in float64: exact (every |sum| < 2^53)
+    ref = mgo.f32_from_bf16(X).astype(np.float64) @ mgo.f32_from_bf16(W).astype(np.float64).T
     np.testing.assert_array_equal(Y, ref.astype(np.float32))
     Yc = mg.op_linear(True, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
     np.testing.assert_array_equal(Yc, ref.astype(np.float32))
