@@ -42,11 +42,13 @@ constexpr int KCH = 512;  // K elements per chunk (64 lanes x 8)
 #ifndef MG_GEMV_J_R12
 #define MG_GEMV_J_R12 2  // features per wave of the exact 9..16-row tiles
 #endif
-// exact 9..16-row tiles of a wide output (N >= MG_GEMV_BIG_N: the MLP up projection, the
-// LM head) give each wave 3 features: a third fewer LDS activation reads per fma, and
-// still over a thousand blocks (measured at 12 rows: LM head 239 vs 261 us, gate/up 60 vs
-// 61 us; 4 features drop to 3 waves per SIMD and are slower; narrower outputs keep 2 for
-// the block count)
+// exact 9..16-row tiles give each wave 3 features when the output is wide (N >=
+// MG_GEMV_BIG_N: the MLP up projection, the LM head: a third fewer LDS activation reads
+// per fma, and still over a thousand blocks; measured at 12 rows: LM head 239 vs 261 us,
+// gate/up 60 vs 61 us; 4 features drop to 3 waves per SIMD and are slower); exact
+// 5..16-row tiles of a narrower output take 3 when that leaves the busiest CU fewer
+// features than 2 (6144 features: 256 blocks of 24 instead of 384 of 16, measured at 8
+// and 12 rows 12.8 vs 14.1 and 15.4 vs 18.1 us; 4096 features keep 256 blocks of 16)
 #ifndef MG_GEMV_J_BIG
 #define MG_GEMV_J_BIG 3
 #endif
@@ -264,17 +266,26 @@ static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s)
 }
 
 // A host row count up to 24 gets one tile of exactly ceil(n/4)*4 rows (branch-free rows,
-// at most three of them dead; 9..16 rows of a wide output with 3 features per wave);
+// at most three of them dead; 5..16 rows with 3 features per wave as stated above);
 // larger counts and device-side counts use 16-row tiles (8-row when at most 8 rows can
 // occur) that skip dead rows by a uniform branch.
+// 3 features per wave: on wide outputs for 9..16-row tiles (the 8-row tile measured slower
+// there: LM head at 8 rows 180 vs 178 us), on narrower ones when it balances the CUs
+static bool gemv_three_features(int N, int R, int n_cu) {
+    if (N >= MG_GEMV_BIG_N) return R >= 12;
+    const int b2 = (N + 2 * GV_NW - 1) / (2 * GV_NW), b3 = (N + 3 * GV_NW - 1) / (3 * GV_NW);
+    return (b3 + n_cu - 1) / n_cu * 3 < (b2 + n_cu - 1) / n_cu * 2;
+}
+
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
     if (!a.n_dev && rows <= MG_GEMV_EXACT_MAX) {
         const int nt = (rows + 3) / 4;
-        if (nt == 3 || nt == 4) {
-            if (a.N >= MG_GEMV_BIG_N) return nt == 3 ? launch_jr<MG_GEMV_J_BIG, 12, true>(a, epi, rows, s)
-                                                     : launch_jr<MG_GEMV_J_BIG, 16, true>(a, epi, rows, s);
+        if (nt >= 2 && nt <= 4 && gemv_three_features(a.N, 4 * nt, a.n_cu > 0 ? a.n_cu : 256)) {
+            if (nt == 2) return launch_jr<MG_GEMV_J_BIG, 8, true>(a, epi, rows, s);
+            return nt == 3 ? launch_jr<MG_GEMV_J_BIG, 12, true>(a, epi, rows, s)
+                           : launch_jr<MG_GEMV_J_BIG, 16, true>(a, epi, rows, s);
         }
         switch (nt) {
             case 1: return launch_jr<MG_GEMV_J_R8, 4, true>(a, epi, rows, s);

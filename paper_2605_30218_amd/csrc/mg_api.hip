@@ -210,6 +210,7 @@ mg_status canon_gemv(mg_ctx* c, const uint16_t* X, int n, const int32_t* n_dev, 
     a.n_host = n;
     a.cap = cap;
     a.n_dev = n_dev;
+    a.n_cu = c->n_cu;
     const int rows = n_dev ? cap : n;
     const double bytes = 2.0 * N * K + 2.0 * rows * K + (double)rows * N * (epi == EPI_F32 ? 4 : 2) *
                                                         (epi == EPI_RESID ? 2 : 1);
@@ -646,6 +647,7 @@ mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const 
         a.Y = Y;
         a.n_host = n;
         a.cap = n;
+        a.n_cu = device_cu_count();
         if (bias) return MG_ERR_ARG;  // fp32 output carries no bias; the model path tests the bias
         return launch_canon_gemv(a, EPI_F32, s) == hipSuccess ? MG_OK : MG_ERR_HIP;
     }

@@ -49,6 +49,7 @@ struct GemvArgs {
     void* Y;                   // EPI_BF16: bf16 [n][N]; EPI_F32: fp32 [n][N]; EPI_RESID: bf16 residual [n][N] (in/out)
     int n_host, cap;           // rows
     const int32_t* n_dev;
+    int n_cu;                  // compute units of the device (chooses the features per wave)
 };
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
 

@@ -51,12 +51,14 @@ def test_division_and_sqrt_are_ieee():
 
 # row counts cover every tile the launcher picks: one branch-free tile of 4, 8, 12, 16, 20
 # or 24 rows (9..16 rows of a wide output, N >= 16384, with 3 features per wave and a
-# ragged last feature block), several 16-row tiles (a multiple of 16, and a ragged count with a partial
-# last tile); K covers several 512-element chunks and a partial last chunk
+# ragged last feature block; 5..16 rows of 4608 or 6144 features with 3 features per wave,
+# which balances the CUs), several 16-row tiles (a multiple of 16, and a ragged count with a
+# partial last tile); K covers several 512-element chunks and a partial last chunk
 @pytest.mark.parametrize("n,N,K", [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
                                    (24, 16, 512), (5, 4096, 256), (10, 32, 1032), (12, 48, 4096), (19, 32, 688),
                                    (21, 16, 1544), (25, 32, 1032), (32, 16, 2056), (47, 16, 520),
-                                   (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096)])
+                                   (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096), (7, 6144, 520),
+                                   (12, 4608, 1032), (16, 6144, 264)])
 def test_canonical_gemv_bitexact(n, N, K):
     X = synth.random_bf16((n, K), seed=n * 7 + 1)
     W = synth.random_bf16((N, K), seed=N + K, std=0.05)
