@@ -171,13 +171,24 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
 
     const uint16_t* wrow[J];
     bool valid[J];
+    if constexpr (EPI == EPI_SWIGLU) {
+        // the block's first GV_NW / 2 waves take the gate rows, the others the up rows of the
+        // same J (GV_NW / 2) outputs: wave w's feature jj is output pj0 + jj of its half
+        const int half = wave >= GV_NW / 2, pj0 = fb * (GV_NW / 2 * J) + (wave % (GV_NW / 2)) * J;
 #pragma unroll
-    for (int jj = 0; jj < J; ++jj) {
-        int j = jw + jj;
-        valid[jj] = j < a.N;
-        int seg = 0;
-        while (seg < 2 && j >= a.Nseg[seg]) { j -= a.Nseg[seg]; ++seg; }
-        wrow[jj] = valid[jj] ? a.W[seg] + (size_t)j * K : a.W[0];
+        for (int jj = 0; jj < J; ++jj) {
+            valid[jj] = pj0 + jj < a.N;
+            wrow[jj] = valid[jj] ? a.W[half] + (size_t)(pj0 + jj) * K : a.W[0];
+        }
+    } else {
+#pragma unroll
+        for (int jj = 0; jj < J; ++jj) {
+            int j = jw + jj;
+            valid[jj] = j < a.N;
+            int seg = 0;
+            while (seg < 2 && j >= a.Nseg[seg]) { j -= a.Nseg[seg]; ++seg; }
+            wrow[jj] = valid[jj] ? a.W[seg] + (size_t)j * K : a.W[0];
+        }
     }
 
     float acc[J][R];
@@ -231,6 +242,20 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
     const float v = butterfly_sum_multi<NV>(flat, lane);
     bool writer;
     const int idx = multi_index<NV>(lane, &writer);
+    if constexpr (EPI == EPI_SWIGLU) {
+        // the up waves hand their sums to the gate waves through LDS
+        __shared__ float up_sum[GV_NW / 2 * J][R];
+        const int half = wave >= GV_NW / 2, p = (wave % (GV_NW / 2)) * J + idx / R, rr = idx % R;
+        if (half && writer && idx < J * R) up_sum[p][rr] = v;
+        __syncthreads();
+        if (half || !writer || idx >= J * R || rr >= nr) return;
+        const int pj = fb * (GV_NW / 2 * J) + p;
+        if (pj >= a.N) return;
+        const float g = bf2f(f2bf(v)), up = bf2f(f2bf(up_sum[p][rr]));
+        const float sg = ieee_div(g, 1.0f + canon_exp(-g));
+        reinterpret_cast<uint16_t*>(a.Y)[(size_t)(r0 + rr) * a.N + pj] = (uint16_t)f2bf(sg * up);
+        return;
+    }
     const int jj = idx / R, rr = idx % R;
     bool ok = writer && idx < J * R && rr < nr;
 #pragma unroll
@@ -254,10 +279,12 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
 
 template <int J, int R, bool EXACT>
 static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s) {
-    const int n_fb = (a.N + GV_NW * J - 1) / (GV_NW * J);
+    const int per_block = epi == EPI_SWIGLU ? GV_NW / 2 * J : GV_NW * J;  // outputs (pairs) per block
+    const int n_fb = (a.N + per_block - 1) / per_block;
     const int n_rt = (rows + R - 1) / R;
     const dim3 grid(8 * ((n_fb + 7) / 8) * n_rt);
     switch (epi) {
+        case EPI_SWIGLU: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_SWIGLU, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
         case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
         case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
         default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
@@ -282,7 +309,9 @@ hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     if (rows <= 0 || a.N <= 0) return hipSuccess;
     if (!a.n_dev && rows <= MG_GEMV_EXACT_MAX) {
         const int nt = (rows + 3) / 4;
-        if (nt >= 2 && nt <= 4 && gemv_three_features(a.N, 4 * nt, a.n_cu > 0 ? a.n_cu : 256)) {
+        // (a SwiGLU launch is judged by its 2N features)
+        const int Nf = epi == EPI_SWIGLU ? 2 * a.N : a.N;
+        if (nt >= 2 && nt <= 4 && gemv_three_features(Nf, 4 * nt, a.n_cu > 0 ? a.n_cu : 256)) {
             if (nt == 2) return launch_jr<MG_GEMV_J_BIG, 8, true>(a, epi, rows, s);
             return nt == 3 ? launch_jr<MG_GEMV_J_BIG, 12, true>(a, epi, rows, s)
                            : launch_jr<MG_GEMV_J_BIG, 16, true>(a, epi, rows, s);

@@ -181,31 +181,6 @@ hipError_t launch_rope_kv(const Items& it, const ModelDims& m, int layer, const 
     return hipGetLastError();
 }
 
-// ------------------------------------------------------------------ SwiGLU
-// a = bf16(silu(g) * u), silu(g) = g / (1 + e^-g); gu row = [gate F | up F].
-// canon: the verifier's EXP and IEEE division; otherwise the hardware exp.
-__global__ __launch_bounds__(256) void swiglu_kernel(const uint16_t* __restrict__ gu, RowCount rc, int F, int canon,
-                                                     uint16_t* __restrict__ a) {
-    const int row = blockIdx.y;
-    if (row >= rc.get()) return;
-    const int k = blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= F) return;
-    const float g = bf2f(gu[(size_t)row * 2 * F + k]);
-    const float u = bf2f(gu[(size_t)row * 2 * F + F + k]);
-    const float t = canon ? canon_exp(-g) : __expf(-g);
-    const float sg = ieee_div(g, 1.0f + t);
-    a[(size_t)row * F + k] = (uint16_t)f2bf(sg * u);
-}
-
-hipError_t launch_swiglu(const uint16_t* gu, int n_host, const int32_t* n_dev, int cap, int F, int canon, uint16_t* a,
-                         hipStream_t s) {
-    const int rows = n_dev ? cap : n_host;
-    if (rows <= 0) return hipSuccess;
-    RowCount rc{n_dev, n_host, cap};
-    hipLaunchKernelGGL(swiglu_kernel, dim3((F + 255) / 256, rows), dim3(256), 0, s, gu, rc, F, canon, a);
-    return hipGetLastError();
-}
-
 // ------------------------------------------------------------------ top-1 / top-2
 // Partial state of a top-2 scan: best value/index and the runner-up value of the
 // multiset seen so far.  Merging two states is associative and commutative: the

@@ -26,7 +26,7 @@ constexpr size_t ALIGN = 256;
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 struct Plan {
-    size_t rope, x, h, qkv, qrot, att, gu, act, attn_part, gemm_part, top2_ws, vlog, vrows, total;
+    size_t rope, x, h, qkv, qrot, att, act, attn_part, gemm_part, top2_ws, vlog, vrows, total;
     int rows_cap, max_pos, chunks_canon;
 };
 
@@ -73,7 +73,6 @@ Plan make_plan(const mg_model_cfg* c, int n_cu) {
     p.qkv = o; o += up(R * (Nq + 2 * Nk) * 2);
     p.qrot = o; o += up(R * Nq * 2);
     p.att = o; o += up(R * Nq * 2);
-    p.gu = o; o += up(R * 2 * (size_t)F * 2);
     p.act = o; o += up(R * (size_t)F * 2);
     const size_t ap_canon = R * Hq * (size_t)p.chunks_canon * (hd + 2);
     p.attn_part = o; o += up(ap_canon * sizeof(float));
@@ -205,14 +204,17 @@ mg_status canon_gemv(mg_ctx* c, const uint16_t* X, int n, const int32_t* n_dev, 
         a.Nseg[k] = k < nseg ? Nseg[k] : 0;
         N += a.Nseg[k];
     }
-    a.N = N;
+    // the SwiGLU epilogue writes one output per (gate, up) pair
+    const int Nout = epi == EPI_SWIGLU ? a.Nseg[0] : N;
+    if (epi == EPI_SWIGLU && (nseg != 2 || a.Nseg[1] != a.Nseg[0] || bias)) return MG_ERR_ARG;
+    a.N = Nout;
     a.Y = Y;
     a.n_host = n;
     a.cap = cap;
     a.n_dev = n_dev;
     a.n_cu = c->n_cu;
     const int rows = n_dev ? cap : n;
-    const double bytes = 2.0 * N * K + 2.0 * rows * K + (double)rows * N * (epi == EPI_F32 ? 4 : 2) *
+    const double bytes = 2.0 * N * K + 2.0 * rows * K + (double)rows * Nout * (epi == EPI_F32 ? 4 : 2) *
                                                         (epi == EPI_RESID ? 2 : 1);
     ProfScope ps(c, MG_KIND_CANON_GEMV, s, bytes, 2.0 * rows * N * K);
     HIPCHK(launch_canon_gemv(a, epi, s));
@@ -240,7 +242,6 @@ mg_status canon_forward(mg_ctx* c, const Items& it, uint16_t* own_col, float* lo
     uint16_t* qkv = c->at<uint16_t>(c->plan.qkv);
     uint16_t* qrot = c->at<uint16_t>(c->plan.qrot);
     uint16_t* att = c->at<uint16_t>(c->plan.att);
-    uint16_t* gu = c->at<uint16_t>(c->plan.gu);
     uint16_t* act = c->at<uint16_t>(c->plan.act);
     HIPCHK(launch_embed(it, c->W(0), d, x, s));
     for (int l = 0; l < g.n_layers; ++l) {
@@ -274,11 +275,11 @@ mg_status canon_forward(mg_ctx* c, const Items& it, uint16_t* own_col, float* lo
         }
         HIPCHK(launch_rmsnorm(x, c->LW(l, 8), n, nd, cap, d, g.rms_eps, h, s));
         {
+            // gate/up projection with the SwiGLU in its epilogue: act = bf16(silu(bf16(gate)) * bf16(up))
             const uint16_t* W[2] = {c->LW(l, 9), c->LW(l, 10)};
             const int Ns[2] = {F, F};
-            MGCHK(canon_gemv(c, h, n, nd, cap, d, W, nullptr, Ns, 2, gu, EPI_BF16, s));
+            MGCHK(canon_gemv(c, h, n, nd, cap, d, W, nullptr, Ns, 2, act, EPI_SWIGLU, s));
         }
-        HIPCHK(launch_swiglu(gu, n, nd, cap, F, 1, act, s));
         {
             const uint16_t* W[1] = {c->LW(l, 11)};
             const int Ns[1] = {d};

@@ -38,7 +38,11 @@ struct ModelDims {
 };
 
 // ---------------------------------------------------------------- canonical GEMV
-enum { EPI_BF16 = 0, EPI_RESID = 1, EPI_F32 = 2 };
+enum { EPI_BF16 = 0, EPI_RESID = 1, EPI_F32 = 2, EPI_SWIGLU = 3 };
+// EPI_SWIGLU: W[0] = gate rows, W[1] = up rows (Nseg[0] = Nseg[1] = N); half of a block's
+// waves take gate rows, the other half the up rows of the same outputs, and the block writes
+// Y[r][j] = bf16(silu(bf16(gate)) * bf16(up)) with the verifier's EXP and IEEE division
+// (bf16 [n][N])
 struct GemvArgs {
     const uint16_t* X;         // [n][K] bf16 (compact rows)
     int K;
@@ -89,9 +93,6 @@ hipError_t launch_rmsnorm(const uint16_t* x, const uint16_t* gamma, int n_host, 
 //  kv_col == NULL: the paged cache at the item's position (fast path / prefill)
 hipError_t launch_rope_kv(const Items& it, const ModelDims& m, int layer, const uint16_t* qkv, const float* rope_cs,
                           uint16_t* qrot, uint16_t* kv_pool, uint16_t* kv_col, hipStream_t s);
-hipError_t launch_swiglu(const uint16_t* gu, int n_host, const int32_t* n_dev, int cap, int F, int canon,
-                         uint16_t* a, hipStream_t s);
-
 // ---------------------------------------------------------------- attention
 struct AttnArgs {
     Items it;
