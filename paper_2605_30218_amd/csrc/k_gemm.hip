@@ -245,12 +245,20 @@ __global__ __launch_bounds__(64 * NW) void fast_gemm_kernel(FastGemmArgs a) {
     int nf[FT];
 #pragma unroll
     for (int f = 0; f < FT; ++f) {
-        const int n0 = nb * FB + (wave * FT + f) * 16;
-        nf[f] = n0;
-        wok[f] = n0 < a.N;
-        int seg = 0, nl = n0;
-        while (seg < 2 && nl >= a.Nseg[seg]) { nl -= a.Nseg[seg]; ++seg; }
-        wrow[f] = wok[f] ? a.W[seg] + (size_t)(nl + jl) * K : a.W[0];
+        if constexpr (EPI == FEPI_SWIGLU) {
+            // waves [0, NW/2) take the gate rows, the others the up rows of the same outputs
+            const int n0 = nb * (NW / 2) * 16 + (wave % (NW / 2)) * 16;
+            nf[f] = n0;
+            wok[f] = n0 < a.N;
+            wrow[f] = wok[f] ? a.W[wave >= NW / 2] + (size_t)(n0 + jl) * K : a.W[0];
+        } else {
+            const int n0 = nb * FB + (wave * FT + f) * 16;
+            nf[f] = n0;
+            wok[f] = n0 < a.N;
+            int seg = 0, nl = n0;
+            while (seg < 2 && nl >= a.Nseg[seg]) { nl -= a.Nseg[seg]; ++seg; }
+            wrow[f] = wok[f] ? a.W[seg] + (size_t)(nl + jl) * K : a.W[0];
+        }
     }
 
     // split boundaries in 128-element units whatever the chunk size, so that a row's
@@ -308,6 +316,32 @@ __global__ __launch_bounds__(64 * NW) void fast_gemm_kernel(FastGemmArgs a) {
             mfma_chunk_lds<MT>(wring[c % D][wave], xt[c & 1], jl, q, acc);
             __builtin_amdgcn_sched_barrier(0);
             lds_barrier();
+        }
+        if constexpr (EPI == FEPI_SWIGLU) {
+            // every wave is past its last read of the rings (the loops end on a barrier and
+            // no load is outstanding): the up waves leave their sums in the weight ring
+            float* up_sum = reinterpret_cast<float*>(&wring[0][0][0]) + (wave % (NW / 2)) * MT * 256;
+            static_assert((NW / 2) * MT * 256 * 4 <= (int)sizeof(wring), "up sums fit in the weight ring");
+            if (wave >= NW / 2) {
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) up_sum[mt * 256 + (4 * q + v) * 16 + jl] = acc[mt][0][v];
+            }
+            __syncthreads();
+            if (wave >= NW / 2 || !wok[0]) return;
+            uint16_t* act = reinterpret_cast<uint16_t*>(a.Y);
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int row = 16 * mt + 4 * q + v;
+                    if (row >= M) continue;
+                    const float g = bf2f(f2bf(acc[mt][0][v]));
+                    const float u = bf2f(f2bf(up_sum[mt * 256 + (4 * q + v) * 16 + jl]));
+                    act[(size_t)row * a.N + nf[0] + jl] = (uint16_t)f2bf((g / (1.0f + __expf(-g))) * u);
+                }
+            return;
         }
     } else {
     __shared__ __attribute__((aligned(16))) unsigned char xs[2][S::ROWS * S::STRIDE];
@@ -453,6 +487,8 @@ static int max_splits(int M, int K) {
     return S < 1 ? 1 : S;
 }
 
+bool fast_gemm_lds_path(int M, int K) { return lds_path(M, K); }
+
 // waves per block for a launch with S splits
 static int fast_gemm_waves(int M, int N, int K, int S, int n_cu) {
     if (!lds_path(M, K)) return GM_NW;
@@ -487,6 +523,11 @@ void fast_gemm_config(int M, int N, int K, int n_cu, int* S, int* waves) {
 
 template <int MT, int NW, int FT, int EPI>
 static void launch_epi(const FastGemmArgs& a, dim3 g, hipStream_t s) {
+    if constexpr (EPI == FEPI_SWIGLU) {  // direct-to-LDS path only (checked by the launcher)
+        if constexpr (gemm_kc(MT) == 128)
+            hipLaunchKernelGGL((fast_gemm_kernel<MT, NW, FT, EPI, true>), g, dim3(64 * NW), 0, s, a);
+        return;
+    }
     if constexpr (NW == GM_NW) {
         if (!(gemm_kc(MT) == 128 && a.K % 128 == 0)) {
             hipLaunchKernelGGL((fast_gemm_kernel<MT, NW, FT, EPI, false>), g, dim3(64 * NW), 0, s, a);
@@ -502,13 +543,15 @@ static void launch_ft(const FastGemmArgs& a, int epi, dim3 g, hipStream_t s) {
     switch (epi) {
         case FEPI_BF16: launch_epi<MT, NW, FT, FEPI_BF16>(a, g, s); break;
         case FEPI_PART: launch_epi<MT, NW, FT, FEPI_PART>(a, g, s); break;
+        case FEPI_SWIGLU: launch_epi<MT, NW, FT, FEPI_SWIGLU>(a, g, s); break;
         default: launch_epi<MT, NW, FT, FEPI_F32>(a, g, s); break;
     }
 }
 
 template <int MT>
 static void launch_mt(const FastGemmArgs& a, int epi, int NW, hipStream_t s) {
-    dim3 g((a.N + 16 * NW * GM_FT - 1) / (16 * NW * GM_FT), a.S);
+    const int per_block = epi == FEPI_SWIGLU ? 16 * (NW / 2) : 16 * NW * GM_FT;  // outputs per block
+    dim3 g((a.N + per_block - 1) / per_block, a.S);
     if constexpr (gemm_kc(MT) == 128) {
         if (NW == 4) return launch_ft<MT, 4, GM_FT>(a, epi, g, s);
     }
@@ -519,7 +562,10 @@ hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s) {
     if (a.M <= 0 || a.N <= 0) return hipSuccess;
     if (a.K < 8 || a.K % 8 || a.N % 16) return hipErrorInvalidValue;
     if (epi != FEPI_PART && a.S != 1) return hipErrorInvalidValue;  // only partial tiles may be split
-    const int NW = fast_gemm_waves(a.M, a.N, a.K, a.S, a.n_cu > 0 ? a.n_cu : 256);
+    if (epi == FEPI_SWIGLU && (a.S != 1 || !lds_path(a.M, a.K) || a.Nseg[0] != a.N || a.Nseg[1] != a.N))
+        return hipErrorInvalidValue;
+    // a SwiGLU launch streams the gate and the up rows: 2N weight rows
+    const int NW = fast_gemm_waves(a.M, epi == FEPI_SWIGLU ? 2 * a.N : a.N, a.K, a.S, a.n_cu > 0 ? a.n_cu : 256);
     switch (mt_for(a.M)) {
         case 1: launch_mt<1>(a, epi, NW, s); break;
         case 2: launch_mt<2>(a, epi, NW, s); break;

@@ -178,13 +178,15 @@ mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, const uint16_t* 
         a.Nseg[k] = k < nseg ? Nseg[k] : 0;
         N += a.Nseg[k];
     }
-    a.N = N;
+    // the SwiGLU epilogue writes one output per (gate, up) pair
+    const int Nout = epi == FEPI_SWIGLU ? a.Nseg[0] : N;
+    a.N = Nout;
     a.Y = Y;
     a.part = c->at<float>(c->plan.gemm_part);
     a.S = epi == FEPI_PART ? fast_gemm_splits(split_M ? split_M : M, N, K, c->n_cu) : 1;
     a.n_cu = c->n_cu;
     if (S_out) *S_out = a.S;
-    const double out_bytes = epi == FEPI_PART ? 4.0 * a.S * M * N : (double)M * N * (epi == FEPI_F32 ? 4 : 2);
+    const double out_bytes = epi == FEPI_PART ? 4.0 * a.S * M * N : (double)M * Nout * (epi == FEPI_F32 ? 4 : 2);
     const double bytes = 2.0 * N * K + 2.0 * M * K + out_bytes;
     ProfScope ps(c, MG_KIND_FAST_GEMM, s, bytes, 2.0 * M * N * K);
     HIPCHK(launch_fast_gemm(a, epi, s));
@@ -441,11 +443,17 @@ static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int
         }
         HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, c->LW(l, 8), g.rms_eps, x, h, s));
         {
+            // gate/up: unsplit on the direct-to-LDS path, the SwiGLU runs in the GEMM's epilogue;
+            // otherwise split partial tiles and a separate SwiGLU pass
             const uint16_t* W[2] = {c->LW(l, 9), c->LW(l, 10)};
             const int Ns[2] = {F, F};
-            MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 2, nullptr, FEPI_PART, s, &S, split_M));
+            if (fast_gemm_splits(split_M ? split_M : B, 2 * F, d, c->n_cu) == 1 && fast_gemm_lds_path(B, d)) {
+                MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 2, act, FEPI_SWIGLU, s));
+            } else {
+                MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 2, nullptr, FEPI_PART, s, &S, split_M));
+                HIPCHK(launch_swiglu_part(B, part, S, F, act, s));
+            }
         }
-        HIPCHK(launch_swiglu_part(B, part, S, F, act, s));
         {
             const uint16_t* W[1] = {c->LW(l, 11)};
             const int Ns[1] = {d};

@@ -58,7 +58,10 @@ struct GemvArgs {
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
 
 // ---------------------------------------------------------------- fast MFMA GEMM
-enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2 };
+enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2, FEPI_SWIGLU = 3 };
+// FEPI_SWIGLU (unsplit, direct-to-LDS path only): W[0] = gate rows, W[1] = up rows, N =
+// outputs; half of a block's waves take gate tiles, the other half the up tiles of the same
+// outputs, and Y[r][j] = bf16(silu(bf16(gate)) * bf16(up)) (bf16 [M][N], the fast path's exp)
 struct FastGemmArgs {
     const uint16_t* X;         // [M][K] bf16
     int M, K;
@@ -76,6 +79,8 @@ hipError_t launch_sum_partials(const float* part, int S, int64_t n, float* out, 
 int fast_gemm_splits(int M, int N, int K, int n_cu);
 // the split count and the waves per block a launch of M rows uses
 void fast_gemm_config(int M, int N, int K, int n_cu, int* S, int* waves);
+// whether M rows of a K-long projection take the direct-to-LDS operand path
+bool fast_gemm_lds_path(int M, int K);
 
 // fast-path consumers of split partial tiles
 // x[r] = bf16(x[r] + bf16(sum_s part[s][r])) (skipped when part == NULL; with embed != NULL,
