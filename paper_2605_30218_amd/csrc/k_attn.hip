@@ -75,9 +75,29 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     // the group's rotated queries: one 16-byte load per thread (threads past the group's
     // 8-element pieces re-read the last piece and stage it into an unused part of qs)
     static_assert(GP * HD <= 8 * 256, "one 16-byte load per thread covers the group's queries");
-    const uint16_t* qrow = a.qrot + (size_t)i * m.Hq * HD + (size_t)kh * G * HD;
-    const uint4 qv = *reinterpret_cast<const uint4*>(qrow + 8 * min(t, G * HD / 8 - 1));
-    const uint16_t* own = a.own_col ? a.own_col + ((size_t)i * m.L + a.layer) * 2 * Nk + (size_t)kh * HD : nullptr;
+    // (with qkv: the piece's RoPE partner piece and the cos/sin of its 8 pairs come too)
+    const bool fold = a.qkv != nullptr;
+    const uint16_t* qkv_row = fold ? a.qkv + (size_t)i * (m.Hq * HD + 2 * Nk) : nullptr;
+    const int tq = min(t, G * HD / 8 - 1), e0 = (tq % U4) * 8;
+    const bool qlow = e0 < HD / 2;  // the piece holds first-half elements of its head
+    uint4 qv, qp;
+    float4 cq[4];
+    if (!fold) {
+        qv = *reinterpret_cast<const uint4*>(a.qrot + (size_t)i * m.Hq * HD + (size_t)kh * G * HD + 8 * tq);
+    } else {
+        const uint16_t* qh = qkv_row + (size_t)(kh * G + tq / U4) * HD;
+        qv = *reinterpret_cast<const uint4*>(qh + e0);
+        qp = *reinterpret_cast<const uint4*>(qh + (qlow ? e0 + HD / 2 : e0 - HD / 2));
+        const float* csr = a.cs + (size_t)p * HD + 2 * (qlow ? e0 : e0 - HD / 2);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) cq[k] = *reinterpret_cast<const float4*>(csr + 4 * k);
+    }
+    // the own column: read from own_col, or (fold) rotated here into kown by the block whose
+    // chunk holds position p, which also writes it to own_col for the repair
+    const uint16_t* own = (a.own_col && !fold) ? a.own_col + ((size_t)i * m.L + a.layer) * 2 * Nk + (size_t)kh * HD
+                                               : nullptr;
+    const bool own_here = fold && p < j0 + ATT_MAXC;
+    __shared__ __attribute__((aligned(16))) uint16_t kown[HD];
     // K block of page pg for this KV head
     auto page_k = [&](int pg) -> const uint16_t* {
         return a.kv_pool + ((((size_t)a.layer * m.n_pages + pg) * 2) * m.Hkv + kh) * (size_t)m.page_size * HD;
@@ -114,17 +134,65 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
 #pragma unroll
         for (int q2 = 1; q2 < PGI; ++q2) pg = sub == q2 ? pgs[PGI * k + q2] : pg;
         const uint16_t* vc = page_k(pg) + kv_stride + (size_t)(jj & 15) * HD;
-        const uint16_t* vp = (own && j0 + jj == p) ? own + Nk : vc;
+        const uint16_t* vp = (own && j0 + jj == p)    ? own + Nk
+                             : (fold && j0 + jj == p) ? qkv_row + m.Hq * HD + Nk + (size_t)kh * HD
+                                                      : vc;
         vr[k] = *reinterpret_cast<const u32x4*>(vp + pc * 8);
     }
-    {
+    if (!fold) {
         float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
         qd[0] = make_float4(bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y));
         qd[1] = make_float4(bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w));
+    } else {
+        // rotate-half RoPE of the piece, as the RoPE kernel computes it: pair (x_i, x_(i+hd/2))
+        // -> (bf16(x_i c - x_(i+hd/2) s), bf16(x_(i+hd/2) c + x_i s)), products rounded apart
+        const float pv[8] = {bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y),
+                             bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w)};
+        const float pp[8] = {bf_lo(qp.x), bf_hi(qp.x), bf_lo(qp.y), bf_hi(qp.y),
+                             bf_lo(qp.z), bf_hi(qp.z), bf_lo(qp.w), bf_hi(qp.w)};
+        const float cc[16] = {cq[0].x, cq[0].y, cq[0].z, cq[0].w, cq[1].x, cq[1].y, cq[1].z, cq[1].w,
+                              cq[2].x, cq[2].y, cq[2].z, cq[2].w, cq[3].x, cq[3].y, cq[3].z, cq[3].w};
+        float qf[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const float lo = qlow ? pv[e] : pp[e], hi = qlow ? pp[e] : pv[e];
+            const float c = cc[2 * e], sn = cc[2 * e + 1];
+            const float ac = lo * c, bs = hi * sn, bc = hi * c, as = lo * sn;
+            qf[e] = bf2f(f2bf(qlow ? ac - bs : bc + as));
+        }
+        float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
+        qd[0] = make_float4(qf[0], qf[1], qf[2], qf[3]);
+        qd[1] = make_float4(qf[4], qf[5], qf[6], qf[7]);
+        if (own_here && wave == 0) {
+            const uint16_t* ks = qkv_row + m.Hq * HD + (size_t)kh * HD;
+            const uint16_t* vsrc = ks + Nk;
+            uint16_t* ow = a.own_col ? const_cast<uint16_t*>(a.own_col) + ((size_t)i * m.L + a.layer) * 2 * Nk +
+                                           (size_t)kh * HD
+                                     : nullptr;
+            for (int ii = lane; ii < HD / 2; ii += 64) {
+                const float lo = bf2f(ks[ii]), hi = bf2f(ks[ii + HD / 2]);
+                const float c = a.cs[(size_t)p * HD + 2 * ii], sn = a.cs[(size_t)p * HD + 2 * ii + 1];
+                const float ac = lo * c, bs = hi * sn, bc = hi * c, as = lo * sn;
+                const uint16_t o1 = (uint16_t)f2bf(ac - bs), o2 = (uint16_t)f2bf(bc + as);
+                kown[ii] = o1;
+                kown[ii + HD / 2] = o2;
+                if (ow) {
+                    ow[ii] = o1;
+                    ow[ii + HD / 2] = o2;
+                    ow[Nk + ii] = vsrc[ii];
+                    ow[Nk + ii + HD / 2] = vsrc[ii + HD / 2];
+                }
+            }
+        }
     }
     // the queries staged by other threads are needed from here on; the K and V requests stay
     // in flight across this barrier (loads complete in order: the queries came first)
     __syncthreads();
+    // (fold) the thread of position p takes the rotated own K row
+    if (own_here && t == nj - 1) {
+#pragma unroll
+        for (int k = 0; k < U4; ++k) kr[k] = reinterpret_cast<const uint4*>(kown)[k];
+    }
 
     // ---- scores: position t, all heads of the group at once (K in registers), computed
     // while the V requests are still in flight

@@ -254,7 +254,10 @@ mg_status canon_forward(mg_ctx* c, const Items& it, uint16_t* own_col, float* lo
             const int Ns[3] = {Nq, Nk, Nk};
             MGCHK(canon_gemv(c, h, n, nd, cap, d, W, g.qkv_bias ? B : nullptr, Ns, 3, qkv, EPI_BF16, s));
         }
-        HIPCHK(launch_rope_kv(it, m, l, qkv, c->at<float>(c->plan.rope), qrot, c->kv_pool, own_col, s));
+        // prefill: every item's K/V goes into the cache before any item attends (later
+        // positions read earlier ones); the verifier's rows attend to committed columns and
+        // their own, so its attention rotates the queries and the own column itself
+        if (!own_col) HIPCHK(launch_rope_kv(it, m, l, qkv, c->at<float>(c->plan.rope), qrot, c->kv_pool, nullptr, s));
         {
             AttnArgs a{};
             a.it = it;
@@ -263,6 +266,8 @@ mg_status canon_forward(mg_ctx* c, const Items& it, uint16_t* own_col, float* lo
             a.qrot = qrot;
             a.kv_pool = c->kv_pool;
             a.own_col = own_col;
+            a.qkv = own_col ? qkv : nullptr;
+            a.cs = c->at<float>(c->plan.rope);
             a.part = c->at<float>(c->plan.attn_part);
             a.chunk = CANON_CHUNK;
             a.max_chunks = c->plan.chunks_canon;

@@ -106,6 +106,11 @@ struct AttnArgs {
     const uint16_t* qrot;      // [n][Hq*hd]
     const uint16_t* kv_pool;
     const uint16_t* own_col;   // verifier scratch columns [n][L][2][Hkv][hd], or NULL (read the cache)
+    // qkv != NULL (with own_col): the kernel rotates the queries and the own K column itself
+    // from the QKV output [n][Hq*hd + 2*Hkv*hd] with the cos/sin table cs, and writes the own
+    // column (K', V) to own_col; qrot is then unused
+    const uint16_t* qkv;
+    const float* cs;
     float* part;               // [n][Hq][max_chunks][hd + 2]
     int chunk;                 // positions per chunk (canonical: 256)
     int max_chunks;
