@@ -1,13 +1,15 @@
 // k_gemm.hip -- the fast path's weight-streaming projection on MFMA (gfx950).
 //
 // Y[M][N] = X[M][K] * W[N][K]^T with v_mfma_f32_16x16x32_bf16, M <= 256 (rows
-// padded to 16-row tiles).  A block of NW waves (8, or 4 on the direct-to-LDS path)
-// owns 16 NW output features; a wave owns 16 of them for all rows (the activation
-// chunk staged in LDS serves all of the block's waves).  The block walks its K range in chunks of KC, requesting later chunks while
-// the MFMAs of the current one run.  Two operand paths:
+// padded to 16-row tiles).  A block of NW waves (8, or 4 on the direct-to-LDS path;
+// the host's launch rule picks the waves and the split count per launch) owns 16 NW
+// output features; a wave owns 16 of them for all rows (the activation chunk staged in
+// LDS serves all of the block's waves).  The block walks its K range in chunks of KC,
+// requesting later chunks while the MFMAs of the current one run.  Two operand paths:
 //  * K % 128 == 0 and up to 128 rows (128-element chunks): both operands go through
 //    LDS by direct-to-LDS loads -- each wave's weights through its own ring of DEPTH
-//    stages, two chunks ahead, the activations through a block-wide double buffer --
+//    stages (two chunks ahead up to 64 rows, one above), the activations through a
+//    block-wide double buffer --
 //    in a swizzled layout whose loads read each row's chunk as one contiguous run and
 //    whose MFMA fragment reads are free of bank conflicts (see issue_w_lds).
 //  * otherwise: weights straight from HBM into MFMA B-operand registers (lane (j, q)
@@ -21,8 +23,10 @@
 // The K range may be split over blocks (split-K): each split writes its fp32 partial
 // tile and the kernel that consumes the projection (RoPE and K/V append, SwiGLU, or
 // residual add + RMSNorm) sums the splits in split order, so blocks never wait for each
-// other.  The summation order depends on M (tile and chunk choice), on the split count
-// and on the operand path: this path may be batch-variant.
+// other.  An unsplit gate/up projection on the direct-to-LDS path instead applies the
+// SwiGLU in its epilogue (FEPI_SWIGLU).  The summation order depends on the split count
+// only (split boundaries in 128-element units); the fast path's choice of split count
+// depends on M, so the fast path may be batch-variant.
 #include "mg_device.h"
 #include "mg_kernels.h"
 
