@@ -181,7 +181,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported (rows are independent, so "
-              "the path scales by data parallelism over requests with no exchange; see DESIGN.md)", file=sys.stderr)
+              "the path scales by data parallelism over requests with no exchange)", file=sys.stderr)
         sys.exit(2)
     torch.cuda.set_device(0)
     mg.load()
