@@ -330,89 +330,127 @@ static size_t kv_index(const mgo_cfg* c, int layer, int page, int kv, int kh, in
 
 static size_t col_size(const mgo_cfg* c) { return (size_t)c->n_layers * 2 * c->n_kv_heads * c->head_dim; }
 
-/* One row's forward at position pos.  Earlier positions come from the paged
- * cache; the row's own K/V for `pos` is written to the cache (kvcol == NULL:
- * the fast path's tentative append) or to kvcol (the verifier's scratch column,
- * cache untouched).  logits may be NULL (prefill). */
-static int forward_row(const model_t* m, int mode, int token, int pos, const int32_t* ptab, uint16_t* kv_pool,
-                       const uint16_t* kv_read, uint16_t* kvcol, float* logits) {
+/* Scratch of one row's layer: every intermediate of the layer, sized for the shape. */
+typedef struct {
+    uint16_t *h, *q, *k, *v, *att, *y, *g, *u, *a;
+    const uint16_t **kr, **vr;
+    float* qf;
+} layer_buf_t;
+
+static int layer_buf_init(const mgo_cfg* c, int pos, layer_buf_t* b) {
+    const int d = c->d_model, Hq = c->n_q_heads, Hkv = c->n_kv_heads, hd = c->head_dim, F = c->d_ffn;
+    b->h = (uint16_t*)malloc(2 * (size_t)d);
+    b->q = (uint16_t*)malloc(2 * (size_t)Hq * hd);
+    b->k = (uint16_t*)malloc(2 * (size_t)Hkv * hd);
+    b->v = (uint16_t*)malloc(2 * (size_t)Hkv * hd);
+    b->att = (uint16_t*)malloc(2 * (size_t)Hq * hd);
+    b->y = (uint16_t*)malloc(2 * (size_t)(d > F ? d : F));
+    b->g = (uint16_t*)malloc(2 * (size_t)F);
+    b->u = (uint16_t*)malloc(2 * (size_t)F);
+    b->a = (uint16_t*)malloc(2 * (size_t)F);
+    b->kr = (const uint16_t**)malloc(sizeof(void*) * (size_t)(pos + 1));
+    b->vr = (const uint16_t**)malloc(sizeof(void*) * (size_t)(pos + 1));
+    b->qf = (float*)malloc(sizeof(float) * (size_t)hd);
+    return b->h && b->q && b->k && b->v && b->att && b->y && b->g && b->u && b->a && b->kr && b->vr && b->qf;
+}
+
+static void layer_buf_free(layer_buf_t* b) {
+    free(b->h); free(b->q); free(b->k); free(b->v); free(b->att); free(b->y); free(b->g); free(b->u); free(b->a);
+    free(b->kr); free(b->vr); free(b->qf);
+}
+
+/* Checks a row's token (token < 0: not checked), position and mapped pages 0..pos. */
+static int row_ok(const mgo_cfg* c, int token, int pos, const int32_t* ptab) {
+    const int ps = c->page_size;
+    if ((token >= 0 && token >= c->vocab) || pos < 0 || pos >= c->max_pages_per_row * ps) return 0;
+    for (int p = 0; p <= pos; ++p) {
+        const int pg = ptab[p / ps];
+        if (pg < 0 || pg >= c->n_pages) return 0;
+    }
+    return 1;
+}
+
+/* One decoder layer of one row at position pos, on the residual stream x [d] (in place):
+ * pre-norm attention with the row's own K/V column (after RoPE) placed in the cache
+ * (kvcol == NULL: the fast path's tentative append) or in kvcol (the verifier's scratch
+ * column, cache untouched), earlier positions read from kv_read, then the pre-norm SwiGLU
+ * block; both blocks add into x with one bf16 rounding each. */
+static void layer_row(const model_t* m, int mode, int l, int pos, const int32_t* ptab, uint16_t* kv_pool,
+                      const uint16_t* kv_read, uint16_t* kvcol, uint16_t* x, layer_buf_t* b) {
     const mgo_cfg* c = m->c;
     const int d = c->d_model, Hq = c->n_q_heads, Hkv = c->n_kv_heads, hd = c->head_dim, F = c->d_ffn;
     const int G = Hq / Hkv, ps = c->page_size;
-    if (token < 0 || token >= c->vocab || pos < 0 || pos >= c->max_pages_per_row * ps) return -2;
-    for (int p = 0; p <= pos; ++p) {
-        const int pg = ptab[p / ps];
-        if (pg < 0 || pg >= c->n_pages) return -2;
+    mgo_rmsnorm(mode, d, x, LW(m, l, 0), c->rms_eps, b->h);
+    mgo_linear(mode, Hq * hd, d, b->h, LW(m, l, 1), c->qkv_bias ? LW(m, l, 4) : NULL, b->q, NULL);
+    mgo_linear(mode, Hkv * hd, d, b->h, LW(m, l, 2), c->qkv_bias ? LW(m, l, 5) : NULL, b->k, NULL);
+    mgo_linear(mode, Hkv * hd, d, b->h, LW(m, l, 3), c->qkv_bias ? LW(m, l, 6) : NULL, b->v, NULL);
+    mgo_rope(hd, pos, (double)c->rope_theta, Hq, b->q);
+    mgo_rope(hd, pos, (double)c->rope_theta, Hkv, b->k);
+    /* own column */
+    const uint16_t *ownk[64], *ownv[64];
+    for (int kh = 0; kh < Hkv; ++kh) {
+        uint16_t *dk, *dv;
+        if (kvcol) {
+            dk = kvcol + (((size_t)l * 2 + 0) * Hkv + kh) * hd;
+            dv = kvcol + (((size_t)l * 2 + 1) * Hkv + kh) * hd;
+        } else {
+            const int pg = ptab[pos / ps], sl = pos % ps;
+            dk = kv_pool + kv_index(c, l, pg, 0, kh, sl);
+            dv = kv_pool + kv_index(c, l, pg, 1, kh, sl);
+        }
+        memcpy(dk, b->k + (size_t)kh * hd, 2 * (size_t)hd);
+        memcpy(dv, b->v + (size_t)kh * hd, 2 * (size_t)hd);
+        ownk[kh] = dk;
+        ownv[kh] = dv;
     }
-    uint16_t* x = (uint16_t*)malloc(2 * (size_t)d);
-    uint16_t* h = (uint16_t*)malloc(2 * (size_t)d);
-    uint16_t* q = (uint16_t*)malloc(2 * (size_t)Hq * hd);
-    uint16_t* k = (uint16_t*)malloc(2 * (size_t)Hkv * hd);
-    uint16_t* v = (uint16_t*)malloc(2 * (size_t)Hkv * hd);
-    uint16_t* att = (uint16_t*)malloc(2 * (size_t)Hq * hd);
-    uint16_t* y = (uint16_t*)malloc(2 * (size_t)(d > F ? d : F));
-    uint16_t* g = (uint16_t*)malloc(2 * (size_t)F);
-    uint16_t* u = (uint16_t*)malloc(2 * (size_t)F);
-    uint16_t* a = (uint16_t*)malloc(2 * (size_t)F);
-    const uint16_t** kr = (const uint16_t**)malloc(sizeof(void*) * (size_t)(pos + 1));
-    const uint16_t** vr = (const uint16_t**)malloc(sizeof(void*) * (size_t)(pos + 1));
-    float* qf = (float*)malloc(sizeof(float) * (size_t)hd);
+    for (int hh = 0; hh < Hq; ++hh) {
+        const int kh = hh / G;
+        for (int p = 0; p < pos; ++p) {
+            const int pg = ptab[p / ps], sl = p % ps;
+            b->kr[p] = kv_read + kv_index(c, l, pg, 0, kh, sl);
+            b->vr[p] = kv_read + kv_index(c, l, pg, 1, kh, sl);
+        }
+        b->kr[pos] = ownk[kh];
+        b->vr[pos] = ownv[kh];
+        for (int dd = 0; dd < hd; ++dd) b->qf[dd] = bf(b->q[(size_t)hh * hd + dd]);
+        attend_ptrs(mode, hd, pos + 1, b->qf, b->kr, b->vr, b->att + (size_t)hh * hd);
+    }
+    mgo_linear(mode, d, Hq * hd, b->att, LW(m, l, 7), NULL, b->y, NULL);
+    for (int i = 0; i < d; ++i) x[i] = rb(bf(x[i]) + bf(b->y[i]));
+    mgo_rmsnorm(mode, d, x, LW(m, l, 8), c->rms_eps, b->h);
+    mgo_linear(mode, F, d, b->h, LW(m, l, 9), NULL, b->g, NULL);
+    mgo_linear(mode, F, d, b->h, LW(m, l, 10), NULL, b->u, NULL);
+    mgo_swiglu(mode, F, b->g, b->u, b->a);
+    mgo_linear(mode, d, F, b->a, LW(m, l, 11), NULL, b->y, NULL);
+    for (int i = 0; i < d; ++i) x[i] = rb(bf(x[i]) + bf(b->y[i]));
+}
 
+/* The head of one row: final RMSNorm, then the LM head with fp32 logits (never rounded). */
+static void head_row(const model_t* m, int mode, const uint16_t* x, uint16_t* h, float* logits) {
+    const mgo_cfg* c = m->c;
+    mgo_rmsnorm(mode, c->d_model, x, W(m, 1 + WPL * c->n_layers), c->rms_eps, h);
+    mgo_linear(mode, c->vocab, c->d_model, h, W(m, 2 + WPL * c->n_layers), NULL, NULL, logits);
+}
+
+/* One row's forward at position pos: the embedding row of the token, every layer in
+ * order (layer_row), then the head when logits != NULL (prefill passes NULL). */
+static int forward_row(const model_t* m, int mode, int token, int pos, const int32_t* ptab, uint16_t* kv_pool,
+                       const uint16_t* kv_read, uint16_t* kvcol, float* logits) {
+    const mgo_cfg* c = m->c;
+    const int d = c->d_model;
+    if (token < 0 || !row_ok(c, token, pos, ptab)) return -2;
+    layer_buf_t b = {0};
+    uint16_t* x = (uint16_t*)malloc(2 * (size_t)d);
+    if (!x || !layer_buf_init(c, pos, &b)) {
+        free(x);
+        layer_buf_free(&b);
+        return -3;
+    }
     memcpy(x, W(m, 0) + (size_t)token * d, 2 * (size_t)d);
-    for (int l = 0; l < c->n_layers; ++l) {
-        mgo_rmsnorm(mode, d, x, LW(m, l, 0), c->rms_eps, h);
-        mgo_linear(mode, Hq * hd, d, h, LW(m, l, 1), c->qkv_bias ? LW(m, l, 4) : NULL, q, NULL);
-        mgo_linear(mode, Hkv * hd, d, h, LW(m, l, 2), c->qkv_bias ? LW(m, l, 5) : NULL, k, NULL);
-        mgo_linear(mode, Hkv * hd, d, h, LW(m, l, 3), c->qkv_bias ? LW(m, l, 6) : NULL, v, NULL);
-        mgo_rope(hd, pos, (double)c->rope_theta, Hq, q);
-        mgo_rope(hd, pos, (double)c->rope_theta, Hkv, k);
-        /* own column */
-        const uint16_t *ownk[64], *ownv[64];
-        for (int kh = 0; kh < Hkv; ++kh) {
-            if (kvcol) {
-                uint16_t* dk = kvcol + (((size_t)l * 2 + 0) * Hkv + kh) * hd;
-                uint16_t* dv = kvcol + (((size_t)l * 2 + 1) * Hkv + kh) * hd;
-                memcpy(dk, k + (size_t)kh * hd, 2 * (size_t)hd);
-                memcpy(dv, v + (size_t)kh * hd, 2 * (size_t)hd);
-                ownk[kh] = dk;
-                ownv[kh] = dv;
-            } else {
-                const int pg = ptab[pos / ps], sl = pos % ps;
-                uint16_t* dk = kv_pool + kv_index(c, l, pg, 0, kh, sl);
-                uint16_t* dv = kv_pool + kv_index(c, l, pg, 1, kh, sl);
-                memcpy(dk, k + (size_t)kh * hd, 2 * (size_t)hd);
-                memcpy(dv, v + (size_t)kh * hd, 2 * (size_t)hd);
-                ownk[kh] = dk;
-                ownv[kh] = dv;
-            }
-        }
-        for (int hh = 0; hh < Hq; ++hh) {
-            const int kh = hh / G;
-            for (int p = 0; p < pos; ++p) {
-                const int pg = ptab[p / ps], sl = p % ps;
-                kr[p] = kv_read + kv_index(c, l, pg, 0, kh, sl);
-                vr[p] = kv_read + kv_index(c, l, pg, 1, kh, sl);
-            }
-            kr[pos] = ownk[kh];
-            vr[pos] = ownv[kh];
-            for (int dd = 0; dd < hd; ++dd) qf[dd] = bf(q[(size_t)hh * hd + dd]);
-            attend_ptrs(mode, hd, pos + 1, qf, kr, vr, att + (size_t)hh * hd);
-        }
-        mgo_linear(mode, d, Hq * hd, att, LW(m, l, 7), NULL, y, NULL);
-        for (int i = 0; i < d; ++i) x[i] = rb(bf(x[i]) + bf(y[i]));
-        mgo_rmsnorm(mode, d, x, LW(m, l, 8), c->rms_eps, h);
-        mgo_linear(mode, F, d, h, LW(m, l, 9), NULL, g, NULL);
-        mgo_linear(mode, F, d, h, LW(m, l, 10), NULL, u, NULL);
-        mgo_swiglu(mode, F, g, u, a);
-        mgo_linear(mode, d, F, a, LW(m, l, 11), NULL, y, NULL);
-        for (int i = 0; i < d; ++i) x[i] = rb(bf(x[i]) + bf(y[i]));
-    }
-    if (logits) {
-        mgo_rmsnorm(mode, d, x, W(m, 1 + WPL * c->n_layers), c->rms_eps, h);
-        mgo_linear(mode, c->vocab, d, h, W(m, 2 + WPL * c->n_layers), NULL, NULL, logits);
-    }
-    free(x); free(h); free(q); free(k); free(v); free(att); free(y); free(g); free(u); free(a);
-    free(kr); free(vr); free(qf);
+    for (int l = 0; l < c->n_layers; ++l) layer_row(m, mode, l, pos, ptab, kv_pool, kv_read, kvcol, x, &b);
+    if (logits) head_row(m, mode, x, b.h, logits);
+    free(x);
+    layer_buf_free(&b);
     return 0;
 }
 
@@ -519,5 +557,48 @@ int mgo_prefill(const mgo_cfg* c, const void* const* w, int mode, int n_tok, con
         int rc = forward_row(&m, mode, tokens[t], t, page_table_row, kv_pool, kv_pool, NULL, NULL);
         if (rc) return rc;
     }
+    return 0;
+}
+
+/* ---------------------------------------------------- layer-level entry points */
+
+int mgo_embed(const mgo_cfg* c, const void* const* w, int B, const int32_t* tokens, uint16_t* x) {
+    if (!cfg_ok(c) || !w || B < 0 || (B && (!tokens || !x))) return -1;
+    const uint16_t* E = ((const uint16_t* const*)w)[0];
+    for (int b = 0; b < B; ++b) {
+        if (tokens[b] < 0 || tokens[b] >= c->vocab) return -2;
+        memcpy(x + (size_t)b * c->d_model, E + (size_t)tokens[b] * c->d_model, 2 * (size_t)c->d_model);
+    }
+    return 0;
+}
+
+int mgo_layer(const mgo_cfg* c, const void* const* w, int mode, int layer, int B, const int32_t* positions,
+              const int32_t* page_table, uint16_t* kv_pool, uint16_t* x) {
+    if (!cfg_ok(c) || !w || B < 0 || layer < 0 || layer >= c->n_layers ||
+        (B && (!positions || !page_table || !kv_pool || !x)))
+        return -1;
+    model_t m = {c, (const uint16_t* const*)w};
+    for (int b = 0; b < B; ++b) {
+        const int32_t* ptab = page_table + (size_t)b * c->max_pages_per_row;
+        if (!row_ok(c, -1, positions[b], ptab)) return -2;
+        layer_buf_t lb = {0};
+        if (!layer_buf_init(c, positions[b], &lb)) {
+            layer_buf_free(&lb);
+            return -3;
+        }
+        layer_row(&m, mode, layer, positions[b], ptab, kv_pool, kv_pool, NULL, x + (size_t)b * c->d_model, &lb);
+        layer_buf_free(&lb);
+    }
+    return 0;
+}
+
+int mgo_head(const mgo_cfg* c, const void* const* w, int mode, int B, const uint16_t* x, float* logits) {
+    if (!cfg_ok(c) || !w || B < 0 || (B && (!x || !logits))) return -1;
+    model_t m = {c, (const uint16_t* const*)w};
+    uint16_t* h = (uint16_t*)malloc(2 * (size_t)c->d_model);
+    if (!h) return -3;
+    for (int b = 0; b < B; ++b)
+        head_row(&m, mode, x + (size_t)b * c->d_model, h, logits + (size_t)b * c->vocab);
+    free(h);
     return 0;
 }

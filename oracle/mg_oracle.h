@@ -89,6 +89,18 @@ int mgo_repair_kv_column_action(const mgo_cfg* c, int n, const int32_t* rows, co
                                 const int32_t* page_table, const int32_t* top1, const int32_t* v_tok,
                                 const uint16_t* v_kvcol, uint16_t* kv_pool, int32_t* emitted, int32_t* n_repaired,
                                 int action);
+/* The step cut at layer boundaries, for state-forced per-layer checks.  Composing
+ * mgo_embed, mgo_layer for layers 0..L-1 and mgo_head over the same rows gives exactly
+ * mgo_decode_step (logits and cache).
+ * mgo_embed: x[b] = embedding row of tokens[b], x bf16 [B][d].
+ * mgo_layer: one decoder layer in `mode` on the residual stream x [B][d] (in place): row b
+ *   at positions[b] writes its K/V column of that layer into kv_pool (the tentative
+ *   append) and attends over positions 0..positions[b] of its page-table row.
+ * mgo_head: final RMSNorm and LM head, fp32 logits [B][V] from x [B][d]. */
+int mgo_embed(const mgo_cfg* c, const void* const* w, int B, const int32_t* tokens, uint16_t* x);
+int mgo_layer(const mgo_cfg* c, const void* const* w, int mode, int layer, int B, const int32_t* positions,
+              const int32_t* page_table, uint16_t* kv_pool, uint16_t* x);
+int mgo_head(const mgo_cfg* c, const void* const* w, int mode, int B, const uint16_t* x, float* logits);
 /* prompt prefill of one row, positions [0, n_tok), causal, in `mode` */
 int mgo_prefill(const mgo_cfg* c, const void* const* w, int mode, int n_tok, const int32_t* tokens,
                 const int32_t* page_table_row, uint16_t* kv_pool);

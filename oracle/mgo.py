@@ -73,6 +73,9 @@ def lib():
             ("mgo_repair_kv_column", [P, i32, P, P, P, P, P, P, P, P, P]),
             ("mgo_repair_kv_column_action", [P, i32, P, P, P, P, P, P, P, P, P, i32]),
             ("mgo_prefill", [P, P, i32, i32, P, P, P]),
+            ("mgo_embed", [P, P, i32, P, P]),
+            ("mgo_layer", [P, P, i32, i32, i32, P, P, P, P]),
+            ("mgo_head", [P, P, i32, i32, P, P]),
         ):
             f = getattr(_lib, name)
             f.restype = C.c_int
@@ -210,6 +213,33 @@ class OracleModel:
         logits = np.empty((B, self.shape.vocab), np.float32)
         _chk(lib().mgo_decode_step(C.byref(self.cfg), self._wptr, mode, B, _p(tokens), _p(positions),
                                    _p(page_table), _p(self.kv_pool), _p(logits)), "decode_step")
+        return logits
+
+    # -------------------------------------------------------------- the step cut at layers
+
+    def embed(self, tokens):
+        """Residual stream entering layer 0: the embedding rows, bf16 [B][d]."""
+        tokens = np.ascontiguousarray(tokens, np.int32)
+        x = np.empty((tokens.size, self.shape.d_model), np.uint16)
+        _chk(lib().mgo_embed(C.byref(self.cfg), self._wptr, tokens.size, _p(tokens), _p(x)), "embed")
+        return x
+
+    def layer(self, mode, layer, x, positions, page_table):
+        """One decoder layer on the residual stream x [B][d] (returns the layer's output; the
+        rows' K/V columns of that layer are appended to the cache)."""
+        x = np.array(x, np.uint16, copy=True, order="C")
+        positions = np.ascontiguousarray(positions, np.int32)
+        page_table = np.ascontiguousarray(page_table, np.int32)
+        _chk(lib().mgo_layer(C.byref(self.cfg), self._wptr, mode, layer, positions.size, _p(positions),
+                             _p(page_table), _p(self.kv_pool), _p(x)), "layer")
+        return x
+
+    def head(self, mode, x):
+        """Final RMSNorm and LM head: fp32 logits [B][V] from the residual stream x [B][d]."""
+        x = np.ascontiguousarray(x, np.uint16)
+        B = x.shape[0]
+        logits = np.empty((B, self.shape.vocab), np.float32)
+        _chk(lib().mgo_head(C.byref(self.cfg), self._wptr, mode, B, _p(x), _p(logits)), "head")
         return logits
 
     @staticmethod

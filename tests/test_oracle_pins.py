@@ -564,3 +564,41 @@ def test_gated_loop_canonical_fast_path_never_repairs():
         np.testing.assert_array_equal(emitted, rec["top1"])
         toks, pos = emitted, pos + 1
 
+
+
+@pytest.mark.parametrize("mode", [mgo.PLAIN, mgo.CANON])
+@pytest.mark.parametrize("bias", [False, True])
+def test_step_cut_at_layers_composes_to_decode_step(mode, bias):
+    """mgo_embed, mgo_layer over every layer and mgo_head, called one after another on rows
+    with different positions, give the decode step's logits and cache bit for bit (the
+    entry points the per-layer state-forced GPU checks feed with the GPU's own layer
+    inputs)."""
+    shape = synth.ModelShape("tiny-bias", 2, 256, 8, 2, 32, 344, 1024, True, 1e6, 1e-6) if bias else synth.TINY
+    om, w, pt = _tiny_model(max_batch=3, ctx=48, shape=shape)
+    prompts = synth.make_prompts(3, [12, 31, 5], shape.vocab, seed=2)
+    for r in range(3):
+        om.prefill(mode, prompts[r][:-1], pt[r])
+    snap = om.kv_pool.copy()
+    toks = np.array([p[-1] for p in prompts], np.int32)
+    pos = np.array([len(p) - 1 for p in prompts], np.int32)
+    ref = om.decode_step(mode, toks, pos, pt)
+    ref_kv = om.kv_pool.copy()
+    om.kv_pool[:] = snap
+    x = om.embed(toks)
+    np.testing.assert_array_equal(x, w[0][toks])
+    for l in range(shape.n_layers):
+        y = om.layer(mode, l, x, pos, pt)
+        assert not np.array_equal(y, x)
+        x = y
+    np.testing.assert_array_equal(om.head(mode, x).view(np.uint32), ref.view(np.uint32))
+    np.testing.assert_array_equal(om.kv_pool, ref_kv)
+    # a layer writes only its own layer's column at each row's position
+    om.kv_pool[:] = snap
+    om.layer(mode, 1, om.embed(toks), pos, pt)
+    changed = np.argwhere(om.kv_view() != snap.reshape(om.kv_view().shape))
+    assert changed.size and set(changed[:, 0].tolist()) == {1}
+    for r in range(3):
+        p = int(pos[r])
+        assert ((changed[:, 1] == pt[r, p // 16]) & (changed[:, 4] == p % 16)).any()
+    assert set(zip(changed[:, 1].tolist(), changed[:, 4].tolist())) <= \
+        {(int(pt[r, int(pos[r]) // 16]), int(pos[r]) % 16) for r in range(3)}
