@@ -19,10 +19,34 @@ from . import mg
 from .mg import Engine
 
 
+def check_positions(page_table, positions, page_size: int, n_pages: int):
+    """Host guard of the device-trusted inputs of a step: every row's position must lie inside its
+    page-table row and on a mapped page of the pool (the kernels write the tentative K/V column
+    through that entry and read the RoPE table at that position, unchecked).  Raises ValueError."""
+    pt = np.asarray(page_table)
+    pos = np.asarray(positions).astype(np.int64)
+    if pt.ndim != 2 or pos.shape != (pt.shape[0],):
+        raise ValueError(f"page table {pt.shape} and positions {pos.shape} do not match")
+    cap = pt.shape[1] * page_size
+    bad = np.nonzero((pos < 0) | (pos >= cap))[0]
+    if bad.size:
+        r = int(bad[0])
+        raise ValueError(f"row {r}: position {int(pos[r])} outside its page-table row (capacity {cap})")
+    pages = pt[np.arange(pos.size), pos // page_size]
+    bad = np.nonzero((pages < 0) | (pages >= n_pages))[0]
+    if bad.size:
+        r = int(bad[0])
+        raise ValueError(f"row {r}: position {int(pos[r])} maps to page {int(pages[r])}, not a page of the pool "
+                         f"(0..{n_pages - 1})")
+
+
 class GatedDecoder:
     def __init__(self, engine: Engine, page_table, protected=None, tau: float = 0.5):
         self.e = engine
         dev = engine.device
+        # host mirrors of the page table and the positions, for the capacity guard
+        self._pt_host = np.ascontiguousarray(np.asarray(page_table, np.int32))
+        self._pos_host = None
         self.page_table = torch.as_tensor(page_table, dtype=torch.int32).to(dev).contiguous()
         self.B = self.page_table.shape[0]
         B, V = self.B, engine.shape.vocab
@@ -59,13 +83,19 @@ class GatedDecoder:
         self.hist = []
 
     def set_state(self, tokens, positions):
+        pos = np.array(positions, np.int32, copy=True)
+        check_positions(self._pt_host, pos, self.e.shape.page_size, self.e.cfg.n_pages)
         self.tokens.copy_(torch.as_tensor(np.asarray(tokens, np.int32)))
-        self.positions.copy_(torch.as_tensor(np.asarray(positions, np.int32)))
+        self.positions.copy_(torch.as_tensor(pos))
+        self._pos_host = pos
 
     def step(self, mode: str = "gated", keep=None):
         """One decode step.  keep: optional dict that receives host copies of the step's
         logits / top1 / margin / gate / rows / v_tok (tests)."""
         e, B = self.e, self.B
+        if self._pos_host is None:
+            raise RuntimeError("GatedDecoder.step before set_state")
+        check_positions(self._pt_host, self._pos_host, e.shape.page_size, e.cfg.n_pages)
         e.decode_step(B, self.tokens, self.positions, self.page_table, self.logits)
         gated = mode not in ("off", "always")
         if gated:
@@ -101,6 +131,7 @@ class GatedDecoder:
         elif keep is not None:
             keep.update(rows=np.zeros(0, np.int32), v_tok=np.zeros(0, np.int32))
         e.advance(B, self.top1, self.tokens, self.positions)
+        self._pos_host += 1
         self.steps += 1
         self.protected_row_steps += int(self.always_rows.numel())
         self.verified_row_steps += n
@@ -138,6 +169,13 @@ def prefill_rows(engine: Engine, prompts, page_table, max_items: int = 1024):
     consumed by the first decode step).  Items are issued in increasing position order, so
     every earlier position of a row is in the cache before a later one attends to it."""
     dev = engine.device
+    pts = np.asarray(page_table, np.int32)
+    for r, pr in enumerate(prompts):  # the last prefilled position of each row, and every earlier page
+        if len(pr) > 1:
+            check_positions(pts[r:r + 1], [len(pr) - 2], engine.shape.page_size, engine.cfg.n_pages)
+            n_pg = (len(pr) - 2) // engine.shape.page_size + 1
+            if (pts[r, :n_pg] < 0).any():
+                raise ValueError(f"row {r}: a prompt page is unmapped")
     items = [(t, p, r) for r, pr in enumerate(prompts) for p, t in enumerate(pr[:-1])]
     items.sort(key=lambda x: (x[1], x[2]))
     pt = torch.as_tensor(np.asarray(page_table, np.int32)).to(dev).contiguous()
@@ -161,6 +199,12 @@ def prefill_fast(engine: Engine, prompts, page_table):
     dev = engine.device
     pt = np.asarray(page_table, np.int32)
     lens = np.array([len(p) for p in prompts])
+    for r in range(len(prompts)):
+        if lens[r] > 1:
+            n_pg = (int(lens[r]) - 2) // engine.shape.page_size + 1
+            check_positions(pt[r:r + 1], [int(lens[r]) - 2], engine.shape.page_size, engine.cfg.n_pages)
+            if (pt[r, :n_pg] < 0).any():
+                raise ValueError(f"row {r}: a prompt page is unmapped")
     logits = torch.empty((len(prompts), engine.shape.vocab), dtype=torch.float32, device=dev)
     for t in range(int(lens.max()) - 1):
         act = np.nonzero(lens - 1 > t)[0]

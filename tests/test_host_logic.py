@@ -1,5 +1,6 @@
 """Host-side logic that is neither oracle nor kernel: the calibration recipe's statistics."""
 import numpy as np
+import pytest
 
 
 def test_eps_pert_takes_the_reference_top50():
@@ -110,3 +111,19 @@ def test_divergence_statistics():
     nt = st["near_tie"]
     assert (nt["top2"], nt["top3"], nt["top8"]) == (0.5, 0.5, 1.0)
     assert nt["gate_recall"] == 0.5 and nt["stable_trigger"] == 0.0
+
+
+def test_step_position_guard():
+    """The host guard of a step's device-trusted inputs: positions inside the page-table row,
+    on a mapped page of the pool; everything else raises before any launch."""
+    from paper_2605_30218_amd.runtime import check_positions
+    pt = np.array([[3, 1, -1], [0, 2, 4]], np.int32)
+    check_positions(pt, [0, 47], 16, 5)          # row 1's last slot
+    check_positions(pt, [31, 16], 16, 5)         # row 0's last mapped slot
+    for pos, what in (([32, 0], "maps to page -1"), ([0, 48], "outside"), ([-1, 0], "outside")):
+        with pytest.raises(ValueError, match=what):
+            check_positions(pt, pos, 16, 5)
+    with pytest.raises(ValueError, match="not a page of the pool"):
+        check_positions(pt, [0, 40], 16, 4)      # page id 4 in a pool of 4 pages
+    with pytest.raises(ValueError, match="do not match"):
+        check_positions(pt, [0], 16, 5)
