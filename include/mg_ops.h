@@ -51,6 +51,15 @@ mg_status mg_op_fast_gemm_config(int n, int N, int K, int n_cu, int* S, int* wav
  * row, CDOT order), r < n; d % 8 == 0.  bf16 in, bf16 out. */
 mg_status mg_op_rmsnorm(int n, int d, const uint16_t* x, const uint16_t* gamma, float eps, uint16_t* y, void* stream);
 
+/* mg_decode_step (the BF16 fast path of Sec. 3.1, with its tentative K/V append of
+ * Sec. 3.2) with the same launches, plus a device copy of the residual stream at every
+ * layer boundary: x_taps[0] = the rows' embeddings entering layer 0, x_taps[l + 1] = the
+ * output of layer l, each [B][d_model] bf16 (x_taps holds (n_layers + 1) * B * d_model
+ * values [device]).  For state-forced per-layer checks of the fast path; the logits and
+ * cache writes are those of mg_decode_step.  Errors as mg_decode_step, plus a NULL x_taps. */
+mg_status mg_op_decode_step_taps(mg_ctx* ctx, int B, const int32_t* tokens, const int32_t* positions,
+                                 const int32_t* page_table, float* logits, uint16_t* x_taps, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

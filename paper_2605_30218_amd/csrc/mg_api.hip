@@ -399,9 +399,11 @@ mg_status mg_destroy(mg_ctx* c) {
 // The fast forward of B rows: token / position / page-table row b at index b.  own_out
 // NULL: the step -- the tentative K/V column of every row is appended to the cache.  Else
 // the matrix-core verifier: the K/V columns go to own_out and the cache is only read;
-// split_M fixes every projection's split-K (0: the row count's own split).
+// split_M fixes every projection's split-K (0: the row count's own split).  taps != NULL:
+// the residual stream entering layer 0 and leaving every layer is copied to
+// taps[0..L] ([L+1][B][d] bf16) as the launches run (the per-layer checks of the tests).
 static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int32_t* positions, const int32_t* page_table,
-                       float* logits, uint16_t* own_out, int split_M, hipStream_t s) {
+                       float* logits, uint16_t* own_out, int split_M, hipStream_t s, uint16_t* taps = nullptr) {
     const mg_model_cfg& g = c->cfg;
     const ModelDims& m = c->m;
     const int d = g.d_model, Nq = g.n_q_heads * g.head_dim, Nk = g.n_kv_heads * g.head_dim, F = g.d_ffn;
@@ -412,6 +414,8 @@ static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int
     float* part = c->at<float>(c->plan.gemm_part);
     // layer 0 input: embedding gather fused with the first RMSNorm
     HIPCHK(launch_resid_norm(B, nullptr, 0, c->W(0), tokens, d, c->LW(0, 0), g.rms_eps, x, h, s));
+    const size_t tap_bytes = (size_t)B * d * sizeof(uint16_t);
+    if (taps) HIPCHK(hipMemcpyAsync(taps, x, tap_bytes, hipMemcpyDeviceToDevice, s));
     for (int l = 0; l < g.n_layers; ++l) {
         int S = 1;
         {
@@ -466,6 +470,8 @@ static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int
         }
         const uint16_t* next_gamma = l + 1 < g.n_layers ? c->LW(l + 1, 0) : c->W(1 + WPL * g.n_layers);
         HIPCHK(launch_resid_norm(B, part, S, nullptr, nullptr, d, next_gamma, g.rms_eps, x, h, s));
+        if (taps)
+            HIPCHK(hipMemcpyAsync(taps + (size_t)(l + 1) * B * d, x, tap_bytes, hipMemcpyDeviceToDevice, s));
     }
     const uint16_t* W[1] = {c->W(2 + WPL * g.n_layers)};
     const int Ns[1] = {g.vocab};
@@ -688,6 +694,15 @@ mg_status mg_op_fast_gemm_config(int n, int N, int K, int n_cu, int* S, int* wav
     if (n <= 0 || n > 256 || N <= 0 || K <= 0 || K % 8 || N % 16 || n_cu <= 0 || !S || !waves) return MG_ERR_ARG;
     fast_gemm_config(n, N, K, n_cu, S, waves);
     return MG_OK;
+}
+
+mg_status mg_op_decode_step_taps(mg_ctx* c, int B, const int32_t* tokens, const int32_t* positions,
+                                 const int32_t* page_table, float* logits, uint16_t* x_taps, void* stream) {
+    if (!c || !tokens || !positions || !page_table || !logits || !x_taps) return MG_ERR_ARG;
+    if (B < 0 || B > c->cfg.max_batch) return MG_ERR_ARG;
+    if (B == 0) return MG_OK;
+    return fast_forward(c, B, tokens, positions, page_table, logits, nullptr, 0, static_cast<hipStream_t>(stream),
+                        x_taps);
 }
 
 mg_status mg_op_rmsnorm(int n, int d, const uint16_t* x, const uint16_t* gamma, float eps, uint16_t* y, void* stream) {

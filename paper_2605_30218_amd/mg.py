@@ -50,6 +50,7 @@ SIGNATURES = {
     "mg_destroy": (I, [P]),
     "mg_decode_step": (I, [P, I, P, P, P, P, P]),
     "mg_margin_gate": (I, [P, I, P, P, F, P, P, P, P, P, P, P]),
+    "mg_margin_gate_noalloc": (I, [I, I, P, P, F, P, P, P, P, P, P]),
     "mg_verify_rows": (I, [P, I, P, P, P, P, P, P, P, P, P]),
     "mg_repair_kv_column": (I, [P, I, P, P, P, P, P, P, P, P, P, P]),
     "mg_repair_kv_column_action": (I, [P, I, P, P, P, P, P, P, P, P, P, I, P]),
@@ -66,6 +67,7 @@ SIGNATURES = {
     "mg_op_linear": (I, [I, I, I, I, P, P, P, P, P, SZ, P]),
     "mg_op_fast_gemm_config": (I, [I, I, I, I, P, P]),
     "mg_op_rmsnorm": (I, [I, I, P, P, F, P, P]),
+    "mg_op_decode_step_taps": (I, [P, I, P, P, P, P, P, P]),
 }
 
 _lib = None
@@ -173,6 +175,13 @@ class Engine:
         _check("mg_decode_step", self.lib.mg_decode_step(self.ctx, B, _ptr(tokens), _ptr(positions),
                                                          _ptr(page_table), _ptr(logits), _stream(stream)))
 
+    def decode_step_taps(self, B, tokens, positions, page_table, logits, x_taps, stream=None):
+        """mg_op_decode_step_taps: the fast step plus the residual stream at every layer boundary
+        (x_taps int16 [(n_layers + 1), B, d_model] holding bf16 bits)."""
+        _check("mg_op_decode_step_taps", self.lib.mg_op_decode_step_taps(
+            self.ctx, B, _ptr(tokens), _ptr(positions), _ptr(page_table), _ptr(logits), _ptr(x_taps),
+            _stream(stream)))
+
     def margin_gate(self, B, logits, protected_mask, tau, top1, margin, gate, gated_rows, n_gated,
                     n_gated_host=None, stream=None):
         """n_gated_host: optional pinned CPU int32 tensor that receives the count too."""
@@ -218,6 +227,14 @@ class Engine:
         _check("mg_profile_end", self.lib.mg_profile_end(self.ctx, kind, C.byref(n), C.byref(ms), C.byref(b),
                                                          C.byref(f)))
         return n.value, ms.value, b.value, f.value
+
+
+def margin_gate_noalloc(B, V, logits, protected_mask, tau, top1, margin, gate, gated_rows, n_gated, stream=None):
+    """mg_margin_gate_noalloc: the margin gate with no context and no allocation (its scratch is a
+    static device array of the library)."""
+    _check("mg_margin_gate_noalloc", load().mg_margin_gate_noalloc(
+        int(B), int(V), _ptr(logits), _ptr(protected_mask), float(tau), _ptr(top1), _ptr(margin), _ptr(gate),
+        _ptr(gated_rows), _ptr(n_gated), _stream(stream)))
 
 
 # ---------------------------------------------------------------- op-level calls (tests)

@@ -7,9 +7,12 @@ below tau = 0.5).  Batch 32 with seeded uniform 1024-token prompts (canonical pr
 512 gated greedy decode steps, every row protected.  At sampled steps the oracle is
 state-forced from the GPU cache of sampled rows:
   gate over the batch                bit-exact (top-1, margin bits, gate, ordered rows)
-  fast logits                        within max(1e-2, twice the oracle's own spread between
-                                     the plain and the canonical order on the same state)
-  verifier logits, token, K/V column bit-exact
+  fast step, per layer               each of the 28 layers' output and tentative K/V column,
+                                     and the head's logits, within normwise 1e-2 of the oracle
+                                     run on the GPU's own input to that layer
+  verifier logits, token, K/V column bit-exact, on rows picked from the step's gated list
+                                     (repaired rows first; a step with no repair is run and
+                                     the next one checked)
   commit / single-column repair      the verifier's token and column on gated rows; top-1
                                      with margin >= tau elsewhere
 and the measured trigger rate lies near the perturbation's design point of 1/2."""
@@ -21,7 +24,7 @@ from oracle import mgo  # noqa: F401  (the oracle library is loaded through _gpu
 from paper_2605_30218_amd import mg, synth
 from paper_2605_30218_amd.runtime import GatedDecoder, prefill_rows
 
-from _gpu_common import forced_step_check, oracle_for_rows
+from _gpu_common import assert_forced, assert_layerwise, forced_steps, layerwise_check
 
 pytestmark = pytest.mark.gpu
 S = synth.QWEN7B
@@ -32,7 +35,7 @@ SAMPLE = [0, 13, 31]
 
 @pytest.fixture(scope="module")
 def run():
-    ctx = P + STEPS + 16
+    ctx = P + STEPS + 32
     maxp = -(-ctx // S.page_size)
     pt, n_pages = synth.make_page_table([ctx] * B, S.page_size, maxp, seed=5)
     w = synth.perturb_lm_head_tie_pairs(synth.make_weights(S, seed=0, device="cuda"), S, seed=4, tau=TAU)
@@ -42,31 +45,33 @@ def run():
     wn = synth.weights_to_numpy(w)
     dec = GatedDecoder(eng, pt, None, tau=TAU)
     dec.set_state(last, pos0)
-    checks = []
-    for step in range(STEPS):
+    checks, layers = [], []
+    step = 0
+    while step < STEPS:
         if step in CHECK_STEPS:
-            pre_tok, pre_pos = dec.tokens.cpu().numpy(), dec.positions.cpu().numpy()
-            om, ptl = oracle_for_rows(S, wn, eng, pt, SAMPLE)
-            keep = {}
-            dec.step("gated", keep=keep)
-            emitted = dec.top1.cpu().numpy()
-            c = forced_step_check(S, eng, pt, pre_tok, pre_pos, SAMPLE, om, ptl, keep, emitted, TAU)
-            print(f"step {step}: {c}", flush=True)
-            checks.append(c)
+            tok, pos = dec.tokens.cpu().numpy(), dec.positions.cpu().numpy()
+            res = layerwise_check(S, wn, eng, pt, tok, pos, SAMPLE)
+            print(f"step {step} layerwise: worst x {max(res['x']):.2e} k {max(res['k']):.2e} "
+                  f"v {max(res['v']):.2e} head {res['head']:.2e} e2e {res['e2e']:.4f}", flush=True)
+            layers.append(res)
+            c, ran = forced_steps(S, wn, eng, dec, pt, 1, TAU, want_repair=True)
+            checks += c
+            step += ran
         else:
             dec.step("gated")
+            step += 1
     torch.cuda.synchronize()
-    yield dict(checks=checks, r_verify=dec.r_verify, r_repair=dec.r_repair())
+    yield dict(checks=checks, layers=layers, r_verify=dec.r_verify, r_repair=dec.r_repair())
     eng.close()
 
 
+def test_qwen7b_layerwise_fast_step(run):
+    for res in run["layers"]:
+        assert_layerwise(res)
+
+
 def test_qwen7b_gated_steps_state_forced(run):
-    for c in run["checks"]:
-        assert c["gate"], c
-        assert c["verifier"], c
-        assert c["commit"], c
-        assert c["err"] <= max(1e-2, 2 * c["spread"]), c
-    assert sum(c["gated_in_sample"] for c in run["checks"]) > 0, "no sampled row was gated at the checked steps"
+    assert_forced(run["checks"])
 
 
 def test_qwen7b_trigger_rate_near_design_point(run):

@@ -1,16 +1,18 @@
 """Full-size parity on the Llama-3.1-8B-shaped decoder in the benchmark's launch configuration
 (batch 64, 512-token prompts), on sampled rows the oracle recomputes one by one (GPU).
 
-  fast step logits, full width, 2 and 32 layers
-                                           within max(1e-2, twice the spread between two valid fp32 orders)
-                                           (the verifier's canonical order vs the oracle's plain
-                                           order) measured on the same rows and state: at this
-                                           depth the random-init model amplifies any change of
-                                           summation order to a few percent of the logit scale
-  margin gate over 64 x 128256 logits      bit-exact
-  verifier (sampled rows)                  bit-exact logits, token and K/V column
+  fast step, 32 layers, per layer        each layer's output and tentative K/V column, and the
+                                           head's logits, within normwise 1e-2 of the oracle run
+                                           on the GPU's own input to that layer (state-forced
+                                           per layer); the end-to-end 32-layer error is printed
+  fast step, full width, 2 layers, per layer
+                                           within normwise 1e-2, as at 32 layers
+  margin gate over 64 x 128256 logits      bit-exact, at 8 consecutive gated steps
+  verifier (sampled gated rows)            bit-exact logits, token and K/V column
   verifier batch invariance                a row alone == inside 12 and 64 rows, any place
   single-column repair                     repaired columns == the oracle verifier's columns
+                                           (rows picked from each step's gated list, repaired
+                                           ones first)
 The prompt cache comes from the canonical prefill, then one fast step appends the tentative
 column; the oracle is state-forced from the GPU cache of the sampled rows."""
 import numpy as np
@@ -21,7 +23,7 @@ from oracle import mgo
 from paper_2605_30218_amd import mg, synth
 from paper_2605_30218_amd.runtime import GatedDecoder, prefill_rows
 
-from _gpu_common import dev_i32, normwise, u16
+from _gpu_common import assert_forced, assert_layerwise, dev_i32, forced_steps, layerwise_check, normwise, u16
 
 pytestmark = pytest.mark.gpu
 S = synth.LLAMA8B
@@ -85,59 +87,39 @@ def test_full_verifier_bitexact_and_invariant(full):
         assert np.array_equal(c2[place], vc[2])
 
 
-def test_full_fast_step_gate_and_repair(full):
-    eng, pt = full["eng"], full["pt"]
-    last, pos0 = full["last"], full["pos0"]
+def test_full_layerwise_fast_step(full):
+    """The fast step at full width and depth, one layer at a time: each of the 32 layers'
+    output and tentative K/V column, and the head's logits, within normwise 1e-2 of the
+    oracle's plain order run on the GPU's own input to that layer."""
+    eng = full["eng"]
     snap = eng.kv_pool.clone()
-    # fast-step logits vs the oracle (plain) on sampled rows, from the same pre-step cache
-    om, ptl = oracle_for_rows(full, SAMPLE)
-    ref = om.decode_step(mgo.PLAIN, last[SAMPLE], pos0[SAMPLE], ptl)
+    res = layerwise_check(S, full["wn"], eng, full["pt"], full["last"], full["pos0"], SAMPLE)
+    eng.kv_pool.copy_(snap)
+    assert_layerwise(res)
+
+
+def test_full_gated_steps_state_forced(full):
+    """Eight gated steps at the benchmark's shape and a tau near its trigger rate.  Each step
+    is checked on rows picked after the step from its gated list (repaired rows first) plus
+    one fast-committed row: gate bit-exact over the batch, verifier logits / token / K-V
+    column bit-exact, commit and repaired columns byte for byte."""
+    eng, pt = full["eng"], full["pt"]
+    snap = eng.kv_pool.clone()
     dec = GatedDecoder(eng, pt, None, tau=0.06)
-    dec.set_state(last, pos0)
-    keep = {}
-    dec.step("gated", keep=keep)
-    torch.cuda.synchronize()
-    post = u16(eng.kv_view())
-    emitted = dec.tokens.cpu().numpy()
-    # the spread between two valid orders on the same rows: the verifier (canonical order,
-    # bit-exact with the oracle's canonical mode) against the oracle's plain order
-    vl = torch.empty((len(SAMPLE), S.vocab), dtype=torch.float32, device="cuda")
-    vt = torch.empty(len(SAMPLE), dtype=torch.int32, device="cuda")
-    vc = torch.empty((len(SAMPLE), eng.col_elems), dtype=torch.int16, device="cuda")
+    dec.set_state(full["last"], full["pos0"])
+    checks, _ = forced_steps(S, full["wn"], eng, dec, pt, 8, dec.tau)
     eng.kv_pool.copy_(snap)
-    eng.verify_rows(len(SAMPLE), dev_i32(SAMPLE), None, dev_i32(last), dev_i32(pos0), dev_i32(pt), vl, vt, vc)
-    torch.cuda.synchronize()
-    canon = vl.cpu().numpy()
-    spread = max(normwise(canon[k], ref[k]) for k in range(len(SAMPLE)))
-    errs = [normwise(keep["logits"][r], ref[k]) for k, r in enumerate(SAMPLE)]
-    print(f"32-layer fast-vs-plain {max(errs):.4f}, canonical-vs-plain spread {spread:.4f}")
-    assert max(errs) <= max(1e-2, 2 * spread), (errs, spread)
-    # the gate over the whole batch is bit-exact
-    rt, rm, rg, rr = mgo.OracleModel.margin_gate(keep["logits"], None, dec.tau)
-    np.testing.assert_array_equal(keep["top1"], rt)
-    np.testing.assert_array_equal(keep["gate"], rg)
-    np.testing.assert_array_equal(keep["rows"], rr)
-    # every gated sampled row: verifier token and, on a mismatch, the repaired column
-    eng.kv_pool.copy_(snap)
-    gs = [r for r in SAMPLE if r in set(rr.tolist())]
-    if gs:
-        om2, ptl2 = oracle_for_rows(full, gs)
-        _, vt, vc = om2.verify_rows(np.arange(len(gs), dtype=np.int32), last[gs], pos0[gs], ptl2,
-                                    want_logits=False)
-        for k, r in enumerate(gs):
-            assert emitted[r] == vt[k]
-            if vt[k] != rt[r]:
-                p = pos0[r]
-                col = post[:, pt[r, p // 16], :, :, p % 16, :]
-                np.testing.assert_array_equal(col, vc[k].reshape(col.shape))
-    for r in SAMPLE:
-        if r not in set(rr.tolist()):
-            assert emitted[r] == rt[r] and keep["margin"][r] >= dec.tau
+    assert_forced(checks)
 
 
 def test_full_width_shallow_fast_step():
     """Every fast kernel at the benchmark's widths and launch configuration (d 4096, FFN
-    14336, vocab 128256, 32/8 heads, hd 128, batch 64, context 512), two layers deep."""
+    14336, vocab 128256, 32/8 heads, hd 128, batch 64, context 512), two layers deep: each
+    layer's output and tentative K/V column, and the head's logits, within normwise 1e-2 of
+    the oracle run on the GPU's own input to that layer.  The end-to-end logit error of the
+    two layers is printed beside the oracle's own spread between its plain and canonical
+    orders on the same state (both are about 1.3e-2 on this random-init model, whichever
+    valid fp32 order is used)."""
     shape = synth.ModelShape("llama3.1-8b-width-2l", 2, 4096, 32, 8, 128, 14336, 128256, False, 5e5, 1e-5)
     ctx = P + 8
     maxp = -(-ctx // 16)
@@ -147,21 +129,15 @@ def test_full_width_shallow_fast_step():
     prompts = synth.make_prompts(B, [P] * B, shape.vocab, seed=4)
     last, pos0 = prefill_rows(eng, prompts, pt)
     rows = [0, 21, 63]
-    maxpg = maxp
-    om = mgo.OracleModel(shape, synth.weights_to_numpy(w), len(rows), maxpg, len(rows) * maxpg)
+    wn = synth.weights_to_numpy(w)
+    res = layerwise_check(shape, wn, eng, pt, last, pos0, rows)
+    om = mgo.OracleModel(shape, wn, len(rows), maxp, len(rows) * maxp)
     src = torch.as_tensor(pt[rows].reshape(-1).astype(np.int64)).cuda()
     om.kv_view()[:] = u16(eng.kv_view()[:, src])
-    logits = torch.empty((B, shape.vocab), dtype=torch.float32, device="cuda")
-    eng.decode_step(B, dev_i32(last), dev_i32(pos0), dev_i32(pt), logits)
-    torch.cuda.synchronize()
-    ptl = np.arange(len(rows) * maxpg, dtype=np.int32).reshape(len(rows), maxpg)
+    ptl = np.arange(len(rows) * maxp, dtype=np.int32).reshape(len(rows), maxp)
     ref = om.decode_step(mgo.PLAIN, last[rows], pos0[rows], ptl)
-    got = logits.cpu().numpy()
-    errs = [normwise(got[r], ref[k]) for k, r in enumerate(rows)]
-    # the verifier's canonical order on the same state gives the spread of valid orders
-    om.kv_view()[:] = u16(eng.kv_view()[:, src])
     vl, _, _ = om.verify_rows(np.arange(len(rows), dtype=np.int32), last[rows], pos0[rows], ptl)
     spread = max(normwise(vl[k], ref[k]) for k in range(len(rows)))
     eng.close()
-    print(f"2-layer full-width fast-vs-plain {max(errs):.4f}, canonical-vs-plain spread {spread:.4f}")
-    assert max(errs) <= max(1e-2, 2 * spread), (errs, spread)
+    print(f"2-layer full-width end to end: fast-vs-plain {res['e2e']:.4f}, canonical-vs-plain spread {spread:.4f}")
+    assert_layerwise(res)
