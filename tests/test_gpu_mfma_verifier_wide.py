@@ -5,7 +5,7 @@ A 2-layer decoder at full width (d 4096, 32/8 heads, hd 128, FFN 14336, vocab 12
 256 rows of ragged context (seeded synthetic bf16 caches of 32..300 positions).  With the
 split-K fixed as for 32 rows the QKV projection is split 5 ways and the O and down
 projections 8 ways; the split a list of n rows would choose on its own differs for n in
-{1, 2, 33, 64, 128, 129, 256}.  Checked (deterministic verifier contract, Sec. 3.2):
+{33, 64, 128, 129, 256}.  Checked (deterministic verifier contract, Sec. 3.2):
   batch invariance   a row's logits, token and K/V column are bit-identical for list sizes
                      1, 2, 31, 32, 33, 64, 128, 129, 256, at the first, the last and a
                      middle place, for three different rows
@@ -65,7 +65,7 @@ def test_fixed_split_is_not_one_and_differs_from_the_lists_own():
     assert sum(S > 1 for S in fixed) >= 2
     moved = {n for n in SIZES for (N, K), S in zip(projs, fixed) if mg.fast_gemm_config(n, N, K)[0] != S}
     print("list sizes whose own split would differ:", sorted(moved))
-    assert {1, 64, 128, 256} <= moved
+    assert {64, 128, 256} <= moved
 
 
 def test_mfma_verifier_invariant_where_split_k_is_fixed(wide2):
