@@ -13,7 +13,9 @@
   near_tie  Obs. 3: at each divergence event, the rank of the reference token in the fast
             logits (top-2 / top-3 / top-8 shares) and the fast top-1/top-2 margin, against the
             margins of the stable synchronous steps; the share of events the gate at tau fires
-            on (its recall).
+            on (its recall); and the near-tie count N(Delta) = |{j : l_j >= l_(1) - Delta}| of
+            Sec. 2.4 (its Table 4) at the paper's four scales, as a mean over the token-stable
+            synchronous steps and over the divergent steps, with their ratio.
   oracle    the synthetic analogue of the oracle selective repair (Sec. 2, Table 5): the
             verifier and the repair run exactly at the steps where the fast token differs from
             the reference token; repairs per sequence (all, and those made while the row was
@@ -52,6 +54,17 @@ def _rank_of(logits: torch.Tensor, tok: torch.Tensor) -> torch.Tensor:
     return ((logits > v) | ((logits == v) & (idx < tok.long()[:, None]))).sum(1)
 
 
+NEAR_TIE_DELTAS = (0.25, 0.5, 1.0, 2.0)  # the scales of Sec. 2.4, Table 4 (logit units)
+
+
+def near_tie_count(logits: torch.Tensor, deltas=NEAR_TIE_DELTAS) -> torch.Tensor:
+    """N(Delta) = |{j : l_j >= l_(1) - Delta}| for each row and Delta, [rows][len(deltas)]
+    (int64).  With the inclusive comparison, N(Delta) > 1 exactly when the top-1/top-2 margin
+    is at most Delta (a duplicated maximum, margin 0, counts every copy)."""
+    top = logits.max(1, keepdim=True).values
+    return torch.stack([(logits >= top - float(d)).sum(1) for d in deltas], 1)
+
+
 def flip_study(dec: GatedDecoder, state, kv_snap, steps: int, tau: float, window: int = 16):
     """Obs. 1-3 from one prefilled state (`state` = (tokens, positions) host arrays with all
     rows at one position, `kv_snap` the prefilled pool).  Returns (statistics, the reference
@@ -74,23 +87,26 @@ def flip_study(dec: GatedDecoder, state, kv_snap, steps: int, tau: float, window
     margins = torch.empty((n, steps), dtype=torch.float32, device=dec.tokens.device)
     ranks = torch.empty((n, steps), dtype=torch.int64, device=dec.tokens.device)
     toks = torch.empty((n, steps), dtype=torch.int32, device=dec.tokens.device)
+    ncount = torch.empty((n, steps, len(NEAR_TIE_DELTAS)), dtype=torch.int64, device=dec.tokens.device)
     for s in range(steps):
         dec.step("off")
         margins[:, s] = dec.margin[rows]
         ranks[:, s] = _rank_of(dec.logits[rows], ref_dev[:, s])
+        ncount[:, s] = near_tie_count(dec.logits[rows])
         toks[:, s] = dec.tokens[rows]
     kv_fast = final_layer_kv(dec, p0, steps)
     ek = torch.linalg.vector_norm((kv_fast[:, :, 0] - kv_ref[:, :, 0]).flatten(2), dim=2).cpu().numpy()
     evv = torch.linalg.vector_norm((kv_fast[:, :, 1] - kv_ref[:, :, 1]).flatten(2), dim=2).cpu().numpy()
     stats = divergence_stats(toks.cpu().numpy(), reference, margins.cpu().numpy(), ranks.cpu().numpy(), ek, evv,
-                             tau, window)
+                             tau, window, ncount.cpu().numpy())
     return stats, reference
 
 
-def divergence_stats(toks, reference, margins, ranks, ek, ev_, tau: float, window: int = 16) -> dict:
+def divergence_stats(toks, reference, margins, ranks, ek, ev_, tau: float, window: int = 16, ncount=None) -> dict:
     """The statistics of flip_study from its per-row, per-step arrays: emitted tokens and the
     reference's [rows][steps], the fast margins and the reference token's rank in the fast
-    logits at each step, and the final-layer K and V l2 deviations at each cache step."""
+    logits at each step, the final-layer K and V l2 deviations at each cache step, and
+    (optional) the near-tie counts N(Delta) [rows][steps][len(NEAR_TIE_DELTAS)]."""
     n, steps = reference.shape
     same = toks == reference
     diverged = ~same.all(1)
@@ -125,6 +141,20 @@ def divergence_stats(toks, reference, margins, ranks, ek, ev_, tau: float, windo
     def share(mask):
         return float(np.mean(mask)) if mask.size else None
 
+    # Table 4: mean N(Delta) over the token-stable synchronous steps (s < first) and over the
+    # divergent steps (s = first)
+    cluster = None
+    if ncount is not None:
+        stable_mask = np.arange(steps)[None, :] < first[:, None]
+        cluster = {}
+        for k, dlt in enumerate(NEAR_TIE_DELTAS):
+            ns = ncount[:, :, k][stable_mask]
+            nd = ncount[evr, first[evr], k]
+            ms = float(ns.mean()) if ns.size else None
+            md = float(nd.mean()) if nd.size else None
+            cluster[str(dlt)] = dict(stable=ms, divergent=md,
+                                     ratio=(md / ms) if (ms and md is not None) else None)
+
     return dict(
         steps=steps, rows=n, tau=float(tau),
         flips=dict(events=events, synchronous_samples=samples, rate=events / max(samples, 1),
@@ -133,7 +163,8 @@ def divergence_stats(toks, reference, margins, ranks, ek, ev_, tau: float, windo
                 v_spike=med(spike_v), k_slope_median=med(slope_k), k_slope_abs_median=med(np.abs(slope_k))),
         near_tie=dict(events=int(evr.size), top2=share(ev_rank <= 1), top3=share(ev_rank <= 2),
                       top8=share(ev_rank <= 7), event_margin_median=med(ev_margin), stable_margin_median=med(stable),
-                      gate_recall=share(ev_margin < tau), stable_trigger=share(stable < tau)))
+                      gate_recall=share(ev_margin < tau), stable_trigger=share(stable < tau)),
+        near_tie_count=cluster)
 
 
 def oracle_position_repair(dec: GatedDecoder, state, kv_snap, steps: int, reference):

@@ -60,10 +60,13 @@ def test_forward_bytes_of_the_llama8b_shape():
     from paper_2605_30218_amd import synth
     s = synth.LLAMA8B
     assert abs(bench.streamed_weight_bytes(s) / 2 - 7.505e9) < 0.001e9
-    one = bench.forward_bytes(s, 1, 1000) - bench.forward_bytes(s, 1, 999)
+    one = bench.forward_bytes(s, [1000]) - bench.forward_bytes(s, [999])
     assert one == 128 * 1024
-    assert bench.forward_bytes(s, 2, 10) - bench.forward_bytes(s, 1, 10) == \
-        s.n_layers * bench.attn_bytes(s, 1, 10) + s.vocab * 4
+    assert bench.forward_bytes(s, [10, 10]) - bench.forward_bytes(s, [10]) == \
+        s.n_layers * bench.attn_bytes(s, [10]) + s.vocab * 4
+    # ragged rows: the K/V bytes follow each row's own context
+    assert bench.forward_bytes(s, [100, 300]) == bench.forward_bytes(s, [200, 200])
+    assert bench.forward_bytes(s, []) == 0.0
 
 
 def test_util_summary_means_per_kernel(tmp_path):
@@ -102,7 +105,17 @@ def test_divergence_statistics():
     ek[1, 5:] = 50.0         # cache step 5 holds the first column from a divergent token
     ev = 2 * np.ones((3, steps))
     ev[1, 5:] = 40.0
-    st = diagnostics.divergence_stats(toks, ref, margins, ranks, ek, ev, tau=0.05, window=16)
+    ncount = np.ones((3, steps, len(diagnostics.NEAR_TIE_DELTAS)), np.int64)
+    ncount[1, 4] = [2, 2, 3, 5]  # the divergent steps
+    ncount[2, 0] = [2, 4, 4, 7]
+    ncount[0, 3] = [1, 1, 2, 3]  # one stable step of row 0
+    ncount[1, 6] = 9             # after row 1's divergence: neither stable nor divergent
+    st = diagnostics.divergence_stats(toks, ref, margins, ranks, ek, ev, tau=0.05, window=16, ncount=ncount)
+    nc = st["near_tie_count"]
+    # stable synchronous steps: row 0 all 10, row 1 steps 0..3, row 2 none -> 14 steps
+    assert nc["0.25"] == dict(stable=1.0, divergent=2.0, ratio=2.0)
+    assert nc["1.0"]["stable"] == (13 + 2) / 14 and nc["1.0"]["divergent"] == 3.5
+    assert nc["2.0"]["stable"] == (13 + 3) / 14 and nc["2.0"]["divergent"] == 6.0
     assert st["flips"]["events"] == 2 and st["flips"]["synchronous_samples"] == 10 + 5 + 1
     assert st["kv"]["trials"] == 1
     assert st["kv"]["k_pre"] == 1.0 and st["kv"]["k_spike"] == 50.0
