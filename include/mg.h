@@ -120,6 +120,19 @@ mg_status mg_margin_gate(mg_ctx* ctx, int B, const float* logits, const uint8_t*
                          int32_t* top1, float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated,
                          int32_t* n_gated_host, void* stream);
 
+/* The margin gate of mg_margin_gate for callers that cannot allocate device memory or hold
+ * a context: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same outputs and the same bits as mg_margin_gate over B rows of V logits
+ * (B <= 256, V >= 2, else MG_ERR_ARG), without the host-mirror count.  Its partial states
+ * live in a static device array of 32 KiB per GPU, held until the process ends; the first
+ * call on a device looks up that array's address (no allocation, no context).  Every call
+ * on one GPU shares that array: calls that overlap on one GPU (different streams, or
+ * different host threads) race and must be serialised by the caller.  All pointers
+ * [device], as in mg_margin_gate; stream as everywhere. */
+mg_status mg_margin_gate_noalloc(int B, int V, const float* logits, const uint8_t* protected_mask, float tau,
+                                 int32_t* top1, float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated,
+                                 void* stream);
+
 /* (3) The deterministic verifier (Sec. 3.2, deterministic verifier contract):
  * runs the current step again for rows rows[0..n) of the step batch with
  * the canonical reduction order (fixed per-lane groups + xor butterfly for dot

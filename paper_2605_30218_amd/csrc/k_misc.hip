@@ -318,6 +318,10 @@ int top2_slices(int B, int V) {
     return nsl;
 }
 
+size_t top2_ws_bytes(int B, int V) {
+    return B <= 0 ? 0 : (size_t)top2_slices(B, V) * B * sizeof(Top2);
+}
+
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1, float* margin,
                        uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* n_gated_host, void* part_ws,
                        const int32_t* n_dev, hipStream_t s) {

@@ -140,6 +140,8 @@ hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s);
 // top-1 / top-2 of B <= 256 logit rows in two launches (vocabulary slices, then a
 // per-row merge and the ordered compaction); part_ws holds TOP2_WS_BYTES
 constexpr size_t TOP2_WS_BYTES = 256 * 128 * 16;
+// bytes of part_ws a launch of B rows over V logits uses (at most 2048 slice states of 16 bytes)
+size_t top2_ws_bytes(int B, int V);
 hipError_t launch_top2(int B, int V, const float* logits, const uint8_t* prot, float tau, int32_t* top1,
                        float* margin, uint8_t* gate, int32_t* gated_rows, int32_t* n_gated, int32_t* n_gated_host,
                        void* part_ws, const int32_t* n_dev, hipStream_t s);
