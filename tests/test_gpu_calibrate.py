@@ -117,3 +117,53 @@ def test_divergence_diagnostics(pair, prompts):
     orc = diagnostics.oracle_position_repair(dec, (last, pos0), snap, STEPS, ref)
     print(orc)
     assert orc["verified_row_steps"] >= st["flips"]["events"] and 0.0 <= orc["seq_det"] <= 1.0
+
+
+def test_diagnostics_extraction_matches_the_oracle(pair, prompts):
+    """What the divergence diagnostics read from the GPU, against the oracle on the same state:
+    the final layer's K/V columns after the reference decode (final_layer_kv) equal the oracle's
+    canonical greedy decode cache at those positions bit for bit; on a fast step, the fast
+    margins equal the oracle's top-2 over the same logits, the reference token's rank
+    (_rank_of) equals a brute-force rank under the gate's order, and the near-tie counts
+    N(Delta) equal a brute-force count and satisfy N(Delta) > 1 iff margin <= Delta."""
+    from oracle import mgo
+    last, pos0 = fresh(pair, synth.make_prompts(4, [32] * 4, S.vocab, seed=3))
+    dec = GatedDecoder(pair.eng, pair.pt[:4], None, tau=0.0)
+    dec.set_state(last, pos0)
+    steps = 12
+    ref = calibrate.reference_decode(dec, steps)
+    kv_gpu = diagnostics.final_layer_kv(dec, int(pos0[0]), steps).cpu().numpy()
+    # the oracle's own canonical greedy decode from the same prompts
+    rows = np.arange(4, dtype=np.int32)
+    tok, pos = last.copy(), pos0.copy()
+    never = np.full(4, -1, np.int32)
+    for s in range(steps):
+        _, vt, vc = pair.om.verify_rows(rows, tok, pos, pair.pt[:4], want_logits=False)
+        emitted, _ = pair.om.repair(rows, pos, pair.pt[:4], never, vt, vc, never)
+        assert np.array_equal(emitted, ref[:, s])
+        tok, pos = emitted, pos + 1
+    kv = pair.om.kv_view()
+    L = S.n_layers
+    for b in range(4):
+        for s in range(steps):
+            p = int(pos0[b]) + s
+            col = kv[L - 1, pair.pt[b, p // 16], :, :, p % 16, :]
+            want = (col.astype(np.uint32) << 16).view(np.float32)
+            assert np.array_equal(kv_gpu[b, s], want), (b, s)
+    # a fast step from the post-reference state: margins, ranks and near-tie counts
+    dec.step("off")
+    torch.cuda.synchronize()
+    lg = dec.logits.cpu().numpy()
+    margin = dec.margin.cpu().numpy()
+    probe = torch.as_tensor(ref[:, -1].astype(np.int32), device="cuda")
+    rank = diagnostics._rank_of(dec.logits, probe).cpu().numpy()
+    nt = diagnostics.near_tie_count(dec.logits).cpu().numpy()
+    for b in range(4):
+        t1, g = mgo.top2(lg[b])
+        assert np.float32(g).view(np.uint32) == margin[b].view(np.uint32)
+        v, t = lg[b, ref[b, -1]], int(ref[b, -1])
+        assert rank[b] == int(np.sum((lg[b] > v) | ((lg[b] == v) & (np.arange(lg.shape[1]) < t))))
+        for k, dlt in enumerate(diagnostics.NEAR_TIE_DELTAS):
+            thr = np.float32(lg[b].max()) - np.float32(dlt)   # the threshold in fp32, as the count forms it
+            assert nt[b, k] == int(np.sum(lg[b] >= thr))
+            assert (nt[b, k] > 1) == (margin[b] <= dlt)

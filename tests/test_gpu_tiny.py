@@ -20,9 +20,6 @@ from _gpu_common import Pair, dev_i32, normwise, u16
 pytestmark = pytest.mark.gpu
 S = synth.TINY
 V = S.vocab
-# twice the fast-path logit error bound used for the fast commits (normwise 1e-2 of logits of
-# magnitude ~2 on this model): a split closer than this to a tie is an ambiguous tie, not a bug
-NEAR_TIE = 2 * 1e-2 * 2
 
 
 @pytest.fixture(scope="module")
@@ -244,49 +241,47 @@ def test_state_forced_gated_loop(pair, prompts):
     assert n_fast > 0 and n_gated > 0
 
 
-def _oracle_free_run(om, prompts, pt, steps):
-    """The oracle's own greedy run in canonical mode (its fast path and verifier coincide)."""
-    om.kv_pool[:] = 0
-    for r, p in enumerate(prompts):
-        om.prefill(mgo.CANON, p[:-1], pt[r])
-    toks = np.array([p[-1] for p in prompts], np.int32)
-    pos = np.array([len(p) - 1 for p in prompts], np.int32)
-    out, margins = [], []
-    for _ in range(steps):
-        lg = om.decode_step(mgo.CANON, toks, pos, pt)
-        t1, m, _, _ = om.margin_gate(lg, None, 0.0)
-        out.append(t1.copy())
-        margins.append(m.copy())
-        toks, pos = t1, pos + 1
-    return np.stack(out, 1), np.stack(margins, 1)
-
-
 def test_free_running_matches_oracle_token_for_token(pair, prompts):
-    """tau = 0.5 gates almost every step on this model: the GPU sequence must equal the
-    oracle's canonical greedy sequence; a split is tolerated only at an oracle near-tie
-    (margin <= 2E with E the measured fast-vs-oracle logit gap), then the oracle is
-    teacher-forced and the count reported."""
+    """tau = 0.5 gates almost every step on this model.  The GPU decodes freely; beside it the
+    oracle runs its own canonical greedy decode (its fast path and verifier coincide) on its
+    own cache.  At every step each GPU token must equal the oracle's, except at an ambiguous
+    tie: the oracle's margin there is at most 2E, E the measured l_inf gap at that step between
+    the oracle's logits and the GPU's (the larger of the fast logits' gap and the verifier's,
+    recomputed on the GPU's pre-step state).  At such a split the oracle is teacher-forced onto
+    the GPU's token and the comparison continues, so every split of every row is checked."""
     steps = 24
     last, pos0 = fresh_prefill(pair, prompts)
     B = 4
     dec = pair.decoder(B, protected=None, tau=0.5)
     dec.set_state(last, pos0)
-    gpu = []
-    for _ in range(steps):
-        dec.step("gated")
-        gpu.append(dec.tokens.cpu().numpy().copy())
-    gpu = np.stack(gpu, 1)
-    ref, margins = _oracle_free_run(pair.om, prompts, pair.pt[:B], steps)
-    # the first split of each row must sit at an oracle near-tie; later tokens of that row
-    # follow a different continuation and are not compared
-    splits = 0
-    for b in range(B):
-        diff = np.nonzero(gpu[b] != ref[b])[0]
-        if diff.size:
-            s = diff[0]
-            splits += 1
-            assert margins[b, s] <= NEAR_TIE, (b, s, margins[b, s])
-    print(f"free-running splits at near-ties: {splits} of {B} rows; r_verify {dec.r_verify:.3f}")
+    pt = pair.pt[:B]
+    tok, pos = last.copy(), pos0.copy()
+    splits, ambiguous_steps = [], 0
+    for s in range(steps):
+        keep = {}
+        dec.step("gated", keep=keep)
+        torch.cuda.synchronize()
+        emitted = dec.tokens.cpu().numpy()
+        # the canonical verifier on the GPU's pre-step state (positions < p are untouched by
+        # the step, so it can run after it)
+        vl = torch.empty((B, V), dtype=torch.float32, device="cuda")
+        vt = torch.empty(B, dtype=torch.int32, device="cuda")
+        vc = torch.empty((B, pair.eng.col_elems), dtype=torch.int16, device="cuda")
+        pair.eng.verify_rows(B, dev_i32(np.arange(B)), None, dev_i32(keep["tokens"]), dev_i32(keep["positions"]),
+                             dev_i32(pt), vl, vt, vc)
+        vl = vl.cpu().numpy()
+        ref = pair.om.decode_step(mgo.CANON, tok, pos, pt)
+        t1, m, _, _ = pair.om.margin_gate(ref, None, 0.0)
+        E = np.maximum(np.abs(keep["logits"] - ref).max(1), np.abs(vl - ref).max(1))
+        ambiguous_steps += int(np.sum(m <= 2 * E))
+        for b in range(B):
+            if emitted[b] != t1[b]:
+                splits.append((b, s, float(m[b]), float(E[b])))
+                assert m[b] <= 2 * E[b], (b, s, m[b], E[b])
+        tok, pos = emitted.copy(), pos + 1   # teacher-forced onto the GPU's tokens
+    print(f"free-running splits at ambiguous ties: {splits} (steps with an oracle margin <= 2E: {ambiguous_steps}); "
+          f"r_verify {dec.r_verify:.3f}")
+    assert len(splits) <= ambiguous_steps
 
 
 def test_protected_row_alone_vs_in_batch(pair, prompts):
