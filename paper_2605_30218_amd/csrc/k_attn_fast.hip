@@ -1,7 +1,11 @@
 // k_attn_fast.hip -- the fast path's decode attention, fused with the split-K sum of
 // the QKV projection, the bias, RoPE and the tentative K/V append.
 //
-// One block of 4 waves per (row, KV head).
+// One block of 4 waves per (row, KV head, position split).  With one split (enough rows to
+// fill the device) the block merges everything itself; with several (split-KV, for long
+// contexts at small batch) split k takes an equal share of the pages of positions 0..p-1,
+// split 0 also takes position p, and a second launch merges the splits' (m, l, O) in split
+// order.
 // Prologue: sums the QKV split partials of the block's features (the G query heads of
 // the group, then k, then v) in split order, adds the bias and rounds to bf16 (the
 // projection's rounding point); rotates q and k (rotate-half RoPE from the fp32
@@ -20,8 +24,9 @@
 // K and V of the wave's next step are requested before the current step's
 // arithmetic (register ping-pong); values of positions >= p are zeroed when used.
 // Epilogue: each wave's (m, l, O) goes to LDS; position p contributes its own partial
-// (m = score of q' . k'_p, l = 1, O = v_p); the five partials are merged and
-// out = bf16(O / L).
+// (m = score of q' . k'_p, l = 1, O = v_p) in split 0; the partials are merged and
+// out = bf16(O / L), or the split's merged partial is stored for the split merge.  Every
+// split recomputes the prologue (q' is needed by all); only split 0 writes the column.
 // The summation order depends on the context length and the split of positions over
 // waves: this path is not the verifier's order.
 #include "mg_device.h"
@@ -35,6 +40,9 @@ typedef float f32x4_ft __attribute__((ext_vector_type(4)));
 #ifndef MG_FA_WAVES
 #define MG_FA_WAVES 4
 #endif
+#ifndef MG_FA_MIN_WAVES
+#define MG_FA_MIN_WAVES 2  // waves per SIMD the register budget must allow (up to 4 query heads per KV head: two blocks per CU without spilling; 8 would spill)
+#endif
 constexpr int FA_WAVES = MG_FA_WAVES;
 constexpr int FA_THREADS = 64 * FA_WAVES;
 constexpr int FA_PGCAP = 1024;  // page indices held in LDS (positions < 16384); more are read from memory
@@ -42,14 +50,14 @@ constexpr int FA_PGCAP = 1024;  // page indices held in LDS (positions < 16384);
 __device__ __forceinline__ float fa_scale(int hd) { return hd == 128 ? 0x1.6a09e6p-4f : 0x1.0p-3f; }
 
 template <int HD, int GP>
-__global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArgs a) {
+__global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <= 4 ? MG_FA_MIN_WAVES : 1))) void attn_fast_fused_kernel(FastAttnArgs a) {
     constexpr int DG = HD / 8;    // 16-byte d-groups per row
     constexpr int PPI = 64 / DG;  // positions per V load instruction
     constexpr int VL = 16 / PPI;  // V loads per lane per page step
     constexpr int KST = HD / 32;  // MFMA k-steps over d
     constexpr int H2 = HD / 2;
     const ModelDims& m = a.m;
-    const int kh = blockIdx.x, r = blockIdx.y;
+    const int kh = blockIdx.x, r = blockIdx.y, split = blockIdx.z;
     const int G = m.Hq / m.Hkv, Nq = m.Hq * HD, Nk = m.Hkv * HD, N = Nq + 2 * Nk;
     const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
     const int jl = lane & 15, qg = lane >> 4;
@@ -67,7 +75,11 @@ __global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArg
     const int p = a.positions[r];
     const int32_t* ptab = a.page_table + (size_t)r * m.max_pages_per_row;
     const int npg = (p + 15) / 16;  // pages holding positions 0..p-1
-    const bool pg_lds = npg <= FA_PGCAP;
+    // this split's pages [pg0, pg1)
+    const int per = (npg + a.nsplit - 1) / a.nsplit;
+    const int pg0 = min(npg, split * per), pg1 = min(npg, pg0 + per);
+    const bool pg_lds = pg1 - pg0 <= FA_PGCAP;
+    const bool first = split == 0;
 
     // ---- prologue: split sum + bias + bf16 of this block's q, k, v features
     {
@@ -102,7 +114,7 @@ __global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArg
             y[f + 3] = bf2f(f2bf(v.w));
         }
         if (pg_lds)
-            for (int j = t; j < npg; j += FA_THREADS) pgs[j] = ptab[j];
+            for (int j = t; j < pg1 - pg0; j += FA_THREADS) pgs[j] = ptab[pg0 + j];
         for (int e = G * HD + t; e < GP * HD; e += FA_THREADS) qb[e] = 0;
     }
     __syncthreads();
@@ -130,15 +142,17 @@ __global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArg
                 qb[head * HD + ii] = (uint16_t)o1;
                 qb[head * HD + ii + H2] = (uint16_t)o2;
             } else {
-                kdst[ii] = (uint16_t)o1;
-                kdst[ii + H2] = (uint16_t)o2;
+                if (first) {
+                    kdst[ii] = (uint16_t)o1;
+                    kdst[ii + H2] = (uint16_t)o2;
+                }
                 kps[ii] = bf2f(o1);
                 kps[ii + H2] = bf2f(o2);
             }
         }
         for (int d = t; d < HD; d += FA_THREADS) {
             const float v = y[(G + 1) * HD + d];
-            vdst[d] = (uint16_t)f2bf(v);
+            if (first) vdst[d] = (uint16_t)f2bf(v);
             vps[d] = v;
         }
     }
@@ -177,7 +191,7 @@ __global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArg
     auto fetch = [&](int s, uint4 (&kb)[KST], uint4 (&vb)[VL]) {
         int page;
         if (pg_lds)
-            page = pgs[s];
+            page = pgs[s - pg0];
         else
             page = ptab[s];
         const uint16_t* kp = a.kv_pool + ((((size_t)a.layer * m.n_pages + page) * 2) * m.Hkv + kh) * (size_t)16 * HD;
@@ -231,8 +245,8 @@ __global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArg
             }
         }
     };
-    const int nst = npg;  // page steps over positions 0..p-1
-    int s = wave;
+    const int nst = pg1;  // page steps of this split: pg0 + wave, pg0 + wave + 4, ... < pg1
+    int s = pg0 + wave;
     if (s < nst) {
         uint4 kA[KST], vA[VL], kB[KST], vB[VL];
         fetch(s, kA, vA);
@@ -274,22 +288,57 @@ __global__ __launch_bounds__(FA_THREADS) void attn_fast_fused_kernel(FastAttnArg
     }
     __syncthreads();
 
-    // ---- merge the wave partials and position p
+    // ---- merge the wave partials and (split 0) position p
     for (int oi = t; oi < G * HD; oi += FA_THREADS) {
         const int h = oi / HD, d = oi % HD;
-        float M = sp[h];
+        float M = first ? sp[h] : -__builtin_inff();
 #pragma unroll
         for (int w = 0; w < FA_WAVES; ++w) M = fmaxf(M, wm[w][h]);
-        const float ws = exp2f(sp[h] - M);
-        float L = ws, O = ws * vps[d];
-#pragma unroll
-        for (int w = 0; w < FA_WAVES; ++w) {
-            const float ww = exp2f(wm[w][h] - M);
-            L += ww * wl[w][h];
-            O += ww * wo[w][h * HD + d];
+        float L = 0.0f, O = 0.0f;
+        if (first) {
+            const float ws = exp2f(sp[h] - M);
+            L = ws;
+            O = ws * vps[d];
         }
-        a.out[(size_t)r * Nq + (size_t)(kh * G + h) * HD + d] = (uint16_t)f2bf(O / L);
+        if (M != -__builtin_inff()) {  // (a split with no position keeps L = O = 0)
+#pragma unroll
+            for (int w = 0; w < FA_WAVES; ++w) {
+                const float ww = exp2f(wm[w][h] - M);
+                L += ww * wl[w][h];
+                O += ww * wo[w][h * HD + d];
+            }
+        }
+        if (a.nsplit == 1) {
+            a.out[(size_t)r * Nq + (size_t)(kh * G + h) * HD + d] = (uint16_t)f2bf(O / L);
+        } else {
+            float* dst = a.split_part + (((size_t)r * m.Hq + kh * G + h) * a.nsplit + split) * (HD + 2);
+            if (d == 0) {
+                dst[0] = M;
+                dst[1] = L;
+            }
+            dst[2 + d] = O;
+        }
     }
+}
+
+// The split merge of split-KV: for each (row, query head), the splits' (m, l, O) combined in
+// split order (exp2 domain, as the partials), out = bf16(O / L).
+__global__ void attn_fast_split_merge_kernel(FastAttnArgs a) {
+    const int h = blockIdx.x, r = blockIdx.y, d = threadIdx.x;
+    const int hd = a.m.hd, ns = a.nsplit;
+    if (d >= hd) return;
+    const float* base = a.split_part + ((size_t)r * a.m.Hq + h) * ns * (hd + 2);
+    float M = -__builtin_inff();
+    for (int k = 0; k < ns; ++k) M = fmaxf(M, base[(size_t)k * (hd + 2)]);
+    float L = 0.0f, O = 0.0f;
+    for (int k = 0; k < ns; ++k) {
+        const float* pk = base + (size_t)k * (hd + 2);
+        if (pk[0] == -__builtin_inff()) continue;  // a split with no position
+        const float w = exp2f(pk[0] - M);
+        L += w * pk[1];
+        O += w * pk[2 + d];
+    }
+    a.out[(size_t)r * a.m.Hq * hd + (size_t)h * hd + d] = (uint16_t)f2bf(O / L);
 }
 
 template <int HD>
@@ -306,13 +355,24 @@ hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s) {
     if (a.B <= 0) return hipSuccess;
     const int G = a.m.Hq / a.m.Hkv;
     if (G < 1 || G > 8 || a.m.page_size != 16 || (a.m.hd != 64 && a.m.hd != 128)) return hipErrorInvalidValue;
+    if (a.nsplit < 1 || (a.nsplit > 1 && !a.split_part)) return hipErrorInvalidValue;
     const int gp = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
-    const dim3 grid(a.m.Hkv, a.B);
+    const dim3 grid(a.m.Hkv, a.B, a.nsplit);
     if (a.m.hd == 128)
         launch_hd<128>(a, gp, grid, s);
     else
         launch_hd<64>(a, gp, grid, s);
+    if (a.nsplit > 1) hipLaunchKernelGGL(attn_fast_split_merge_kernel, dim3(a.m.Hq, a.B), dim3(a.m.hd), 0, s, a);
     return hipGetLastError();
+}
+
+int fast_attn_splits(int rows, int n_kv_heads, int max_pages_per_row, int n_cu, int cap) {
+    const int blocks = rows * n_kv_heads;
+    if (blocks <= 0 || blocks >= 2 * n_cu) return 1;
+    int ns = (2 * n_cu + blocks - 1) / blocks;
+    ns = ns < max_pages_per_row / 16 ? ns : max_pages_per_row / 16;
+    ns = ns < cap ? ns : cap;
+    return ns < 1 ? 1 : ns;
 }
 
 }  // namespace mg

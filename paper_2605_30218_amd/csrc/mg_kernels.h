@@ -133,8 +133,13 @@ struct FastAttnArgs {
     uint16_t* kv_pool;
     uint16_t* out;              // [B][Hq * hd] bf16
     uint16_t* own_out;          // NULL: append K'/V at p to the cache; else [B][L][2][Hkv][hd] (the cache is not written)
+    int nsplit;                 // position splits per (row, KV head): 1 = one block merges everything
+    float* split_part;          // nsplit > 1: partials [B][Hq][nsplit][hd + 2] (m, l, O), merged by a second launch
 };
 hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s);
+// position splits of the fast attention for `rows` rows (split-KV when the (row, KV head)
+// blocks alone cannot fill the device: at least 16 pages of capacity per split)
+int fast_attn_splits(int rows, int n_kv_heads, int max_pages_per_row, int n_cu, int cap);
 
 // ---------------------------------------------------------------- gate / repair / misc
 // top-1 / top-2 of B <= 256 logit rows in two launches (vocabulary slices, then a

@@ -141,3 +141,42 @@ def test_full_width_shallow_fast_step():
     eng.close()
     print(f"2-layer full-width end to end: fast-vs-plain {res['e2e']:.4f}, canonical-vs-plain spread {spread:.4f}")
     assert_layerwise(res)
+
+
+def test_full_width_split_kv_fast_step():
+    """Split-KV: at full width with 4 rows of long, ragged context the fast attention splits each
+    (row, KV head) over several blocks (8 here) and merges them in a second launch.  Each layer's
+    output and tentative K/V column, and the head's logits, within normwise 1e-2 of the oracle
+    run on the GPU's own input to that layer; and the matrix-core verifier, whose split is fixed
+    as for 32 rows, gives a row the same bits alone and inside the 4 rows."""
+    shape = synth.ModelShape("llama3.1-8b-width-2l", 2, 4096, 32, 8, 128, 14336, 128256, False, 5e5, 1e-5)
+    lens = np.array([3000, 1500, 700, 17], np.int32)
+    ctx = int(lens.max()) + 16
+    maxp = -(-ctx // 16)
+    pt, n_pages = synth.make_page_table([ctx] * 4, 16, maxp, seed=5)
+    w = synth.make_weights(shape, seed=3, device="cuda")
+    eng = mg.Engine(shape, w, 4, maxp, n_pages)
+    cached = np.concatenate([pt[r, :-(-(int(lens[r]) - 1) // 16)] for r in range(4)])
+    synth.fill_synthetic_kv(eng.kv_view(), cached, seed=13)
+    tok = synth.make_prompts(1, [4], shape.vocab, seed=14)[0]
+    pos = (lens - 1).astype(np.int32)
+    wn = synth.weights_to_numpy(w)
+    snap = eng.kv_pool.clone()
+    res = layerwise_check(shape, wn, eng, pt, tok, pos, [0, 1, 2, 3])
+    eng.kv_pool.copy_(snap)
+    assert_layerwise(res)
+
+    def mfma(rows):
+        n = len(rows)
+        vl = torch.empty((n, shape.vocab), dtype=torch.float32, device="cuda")
+        vt = torch.empty(n, dtype=torch.int32, device="cuda")
+        vc = torch.empty((n, eng.col_elems), dtype=torch.int16, device="cuda")
+        eng.verify_rows_mfma(n, dev_i32(rows), dev_i32(tok), dev_i32(pos), dev_i32(pt), vl, vt, vc)
+        torch.cuda.synchronize()
+        return vl.cpu().numpy().view(np.uint32), vt.cpu().numpy(), u16(vc)
+
+    alone = mfma([0])
+    inside = mfma([3, 1, 0, 2])
+    eng.close()
+    assert np.array_equal(inside[0][2], alone[0][0]) and inside[1][2] == alone[1][0]
+    assert np.array_equal(inside[2][2], alone[2][0])
