@@ -11,9 +11,9 @@
 // A wave owns J features (2, or 3 for wide outputs); a block of 8 waves owns 8J
 // features and a tile of R rows (so the tile's activations, staged once per block,
 // serve 8J features).  K is walked in chunks of 512 elements (one group per lane).
-// While the fma work of chunk c runs, the weights of chunk c+1 are in flight (register
-// double buffer: one 16-byte group per feature and lane, 1 KiB coalesced per feature,
-// in a ping-pong register pair) and the rows' activations of chunk c+1 are loaded into
+// While the fma work of chunk c runs, the weights of chunk c+1 (or c+1 and c+2 on the
+// narrow, short-K launches) are in flight (registers: one 16-byte group per feature and
+// lane, 1 KiB coalesced per feature, in a ping-pong pair or a ring of three) and the rows' activations of chunk c+1 are loaded into
 // registers, then staged into the fp32 LDS tile: tiles up to 16 rows have two buffers
 // and one barrier per chunk; larger tiles restage one buffer between two barriers,
 // which keeps their LDS footprint at R * 2 KiB.  No split-K, no atomics: a row's
@@ -146,7 +146,8 @@ __device__ __forceinline__ void gemv_fma_chunk(const float4 (*xb)[2][64], int la
     }
 }
 
-template <int J, int R, int EPI, bool EXACT>
+// PF: chunks of weights requested ahead (1 or 2)
+template <int J, int R, int EPI, bool EXACT, int PF>
 __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int n_fb, int n_rt) {
     const int b = blockIdx.x;
     const int xcd = b & 7, slot = b >> 3;
@@ -198,38 +199,66 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
         for (int rr = 0; rr < R; ++rr) acc[jj][rr] = 0.0f;
 
     const int nch = (K + KCH - 1) / KCH;
-    uint4 wA[J], wB[J];
     uint4 xr[GemvShape<R>::XLD];
-    gemv_load_x<R>(a, r0, nr, 0, wave, lane, xr);
-    gemv_load_w<J>(wrow, lane, G, wA);
-    gemv_store_x<R>(xs[0], wave, lane, xr);
-    __syncthreads();
-    // one chunk with a successor: request chunk c+1 (activations first, then weights
-    // into `nxt`), run chunk c, then stage chunk c+1's activations.  Loads complete in
-    // order, so the staging waits for the activations only and the weights of chunk c+1
-    // stay in flight.  With two LDS buffers chunk c+1 goes to the other buffer and one
-    // barrier per chunk suffices (the buffer it overwrites was last read by chunk c-1,
-    // which every wave finished before the previous barrier); with one buffer the
-    // restaging sits between two barriers.
-    auto step = [&](int c, const uint4 (&cur)[J], uint4 (&nxt)[J]) {
-        gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, wave, lane, xr);
-        gemv_load_w<J>(wrow, (c + 1) * 64 + lane, G, nxt);
-        __builtin_amdgcn_sched_barrier(0);
-        if (c * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs[c % XB], lane, nr, cur, acc);
-        if (XB == 1) __syncthreads();
-        gemv_store_x<R>(xs[(c + 1) % XB], wave, lane, xr);
+    if constexpr (PF == 2) {
+        // weights requested two chunks ahead (a ring of three register buffers, the loop
+        // unrolled by three so every buffer is named statically); loads past the last chunk
+        // re-read the last group (clamped) and are never used
+        uint4 wA[J], wB[J], wC[J];
+        gemv_load_x<R>(a, r0, nr, 0, wave, lane, xr);
+        gemv_load_w<J>(wrow, lane, G, wA);
+        gemv_load_w<J>(wrow, 64 + lane, G, wB);
+        gemv_store_x<R>(xs[0], wave, lane, xr);
         __syncthreads();
-    };
-    int c = 0;
-    for (; c + 2 < nch; c += 2) {
-        step(c, wA, wB);
-        step(c + 1, wB, wA);
-    }
-    if (c + 1 < nch) {
-        step(c, wA, wB);
-        if ((c + 1) * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs[(c + 1) % XB], lane, nr, wB, acc);
-    } else if (c * 64 + lane < G) {
-        gemv_fma_chunk<J, R, EXACT>(xs[c % XB], lane, nr, wA, acc);
+        auto step = [&](int c, const uint4 (&cur)[J], uint4 (&nxt)[J]) {
+            gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, wave, lane, xr);
+            gemv_load_w<J>(wrow, (c + 2) * 64 + lane, G, nxt);
+            __builtin_amdgcn_sched_barrier(0);
+            if (c * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs[c % XB], lane, nr, cur, acc);
+            if (XB == 1) __syncthreads();
+            gemv_store_x<R>(xs[(c + 1) % XB], wave, lane, xr);
+            __syncthreads();
+        };
+        for (int c = 0; c < nch; c += 3) {
+            step(c, wA, wC);
+            if (c + 1 >= nch) break;
+            step(c + 1, wB, wA);
+            if (c + 2 >= nch) break;
+            step(c + 2, wC, wB);
+        }
+    } else {
+        uint4 wA[J], wB[J];
+        gemv_load_x<R>(a, r0, nr, 0, wave, lane, xr);
+        gemv_load_w<J>(wrow, lane, G, wA);
+        gemv_store_x<R>(xs[0], wave, lane, xr);
+        __syncthreads();
+        // one chunk with a successor: request chunk c+1 (activations first, then weights
+        // into `nxt`), run chunk c, then stage chunk c+1's activations.  Loads complete in
+        // order, so the staging waits for the activations only and the weights of chunk c+1
+        // stay in flight.  With two LDS buffers chunk c+1 goes to the other buffer and one
+        // barrier per chunk suffices (the buffer it overwrites was last read by chunk c-1,
+        // which every wave finished before the previous barrier); with one buffer the
+        // restaging sits between two barriers.
+        auto step = [&](int c, const uint4 (&cur)[J], uint4 (&nxt)[J]) {
+            gemv_load_x<R>(a, r0, nr, (c + 1) * KCH, wave, lane, xr);
+            gemv_load_w<J>(wrow, (c + 1) * 64 + lane, G, nxt);
+            __builtin_amdgcn_sched_barrier(0);
+            if (c * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs[c % XB], lane, nr, cur, acc);
+            if (XB == 1) __syncthreads();
+            gemv_store_x<R>(xs[(c + 1) % XB], wave, lane, xr);
+            __syncthreads();
+        };
+        int c = 0;
+        for (; c + 2 < nch; c += 2) {
+            step(c, wA, wB);
+            step(c + 1, wB, wA);
+        }
+        if (c + 1 < nch) {
+            step(c, wA, wB);
+            if ((c + 1) * 64 + lane < G) gemv_fma_chunk<J, R, EXACT>(xs[(c + 1) % XB], lane, nr, wB, acc);
+        } else if (c * 64 + lane < G) {
+            gemv_fma_chunk<J, R, EXACT>(xs[c % XB], lane, nr, wA, acc);
+        }
     }
 
     // all J*R butterflies at once (padded to a power of two; each value is summed over the
@@ -277,17 +306,17 @@ __global__ __launch_bounds__(GV_THREADS) void canon_gemv_kernel(GemvArgs a, int 
     }
 }
 
-template <int J, int R, bool EXACT>
+template <int J, int R, bool EXACT, int PF = 1>
 static hipError_t launch_jr(const GemvArgs& a, int epi, int rows, hipStream_t s) {
     const int per_block = epi == EPI_SWIGLU ? GV_NW / 2 * J : GV_NW * J;  // outputs (pairs) per block
     const int n_fb = (a.N + per_block - 1) / per_block;
     const int n_rt = (rows + R - 1) / R;
     const dim3 grid(8 * ((n_fb + 7) / 8) * n_rt);
     switch (epi) {
-        case EPI_SWIGLU: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_SWIGLU, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
-        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
-        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
-        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32, EXACT>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        case EPI_SWIGLU: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_SWIGLU, EXACT, PF>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_BF16, EXACT, PF>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_RESID, EXACT, PF>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
+        default: hipLaunchKernelGGL((canon_gemv_kernel<J, R, EPI_F32, EXACT, PF>), grid, dim3(GV_THREADS), 0, s, a, n_fb, n_rt); break;
     }
     return hipGetLastError();
 }
@@ -311,16 +340,27 @@ hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
         const int nt = (rows + 3) / 4;
         // (a SwiGLU launch is judged by its 2N features)
         const int Nf = epi == EPI_SWIGLU ? 2 * a.N : a.N;
+        // narrow outputs over a short K (the QKV and O projections) request their weights two
+        // chunks ahead from 5 rows on: those launches have one block per CU and wait on
+        // memory (measured at 12 rows: QKV 20.0 vs 23.4 us, O 15.9 vs 17.8; the wide and the
+        // long-K projections were not faster)
+        const bool pf2 = nt >= 2 && a.K <= 4096 && Nf <= 8192;
         if (nt >= 2 && nt <= 4 && gemv_three_features(Nf, 4 * nt, a.n_cu > 0 ? a.n_cu : 256)) {
-            if (nt == 2) return launch_jr<MG_GEMV_J_BIG, 8, true>(a, epi, rows, s);
-            return nt == 3 ? launch_jr<MG_GEMV_J_BIG, 12, true>(a, epi, rows, s)
-                           : launch_jr<MG_GEMV_J_BIG, 16, true>(a, epi, rows, s);
+            if (nt == 2) return pf2 ? launch_jr<MG_GEMV_J_BIG, 8, true, 2>(a, epi, rows, s)
+                                    : launch_jr<MG_GEMV_J_BIG, 8, true>(a, epi, rows, s);
+            if (nt == 3) return pf2 ? launch_jr<MG_GEMV_J_BIG, 12, true, 2>(a, epi, rows, s)
+                                    : launch_jr<MG_GEMV_J_BIG, 12, true>(a, epi, rows, s);
+            return pf2 ? launch_jr<MG_GEMV_J_BIG, 16, true, 2>(a, epi, rows, s)
+                       : launch_jr<MG_GEMV_J_BIG, 16, true>(a, epi, rows, s);
         }
         switch (nt) {
             case 1: return launch_jr<MG_GEMV_J_R8, 4, true>(a, epi, rows, s);
-            case 2: return launch_jr<MG_GEMV_J_R8, 8, true>(a, epi, rows, s);
-            case 3: return launch_jr<MG_GEMV_J_R12, 12, true>(a, epi, rows, s);
-            case 4: return launch_jr<MG_GEMV_J_R12, 16, true>(a, epi, rows, s);
+            case 2: return pf2 ? launch_jr<MG_GEMV_J_R8, 8, true, 2>(a, epi, rows, s)
+                               : launch_jr<MG_GEMV_J_R8, 8, true>(a, epi, rows, s);
+            case 3: return pf2 ? launch_jr<MG_GEMV_J_R12, 12, true, 2>(a, epi, rows, s)
+                               : launch_jr<MG_GEMV_J_R12, 12, true>(a, epi, rows, s);
+            case 4: return pf2 ? launch_jr<MG_GEMV_J_R12, 16, true, 2>(a, epi, rows, s)
+                               : launch_jr<MG_GEMV_J_R12, 16, true>(a, epi, rows, s);
             case 5: return launch_jr<MG_GEMV_J_R16, 20, true>(a, epi, rows, s);
             default: return launch_jr<MG_GEMV_J_R16, 24, true>(a, epi, rows, s);
         }
