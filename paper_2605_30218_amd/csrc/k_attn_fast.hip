@@ -75,11 +75,13 @@ __global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <
     const int p = a.positions[r];
     const int32_t* ptab = a.page_table + (size_t)r * m.max_pages_per_row;
     const int npg = (p + 15) / 16;  // pages holding positions 0..p-1
-    // this split's pages [pg0, pg1)
-    const int per = (npg + a.nsplit - 1) / a.nsplit;
-    const int pg0 = min(npg, split * per), pg1 = min(npg, pg0 + per);
-    const bool pg_lds = pg1 - pg0 <= FA_PGCAP;
+    // this split's pages [pg0, pg1): a fixed share of the capacity, so a block's work is
+    // bounded whatever the row's length; a split past the row's pages has nothing to do (the
+    // merge reads only the row's live splits)
+    const int pg0 = split * a.split_pages, pg1 = min(npg, pg0 + a.split_pages);
     const bool first = split == 0;
+    if (!first && pg0 >= npg) return;
+    const bool pg_lds = pg1 - pg0 <= FA_PGCAP;
 
     // ---- prologue: split sum + bias + bf16 of this block's q, k, v features
     {
@@ -327,11 +329,14 @@ __global__ void attn_fast_split_merge_kernel(FastAttnArgs a) {
     const int h = blockIdx.x, r = blockIdx.y, d = threadIdx.x;
     const int hd = a.m.hd, ns = a.nsplit;
     if (d >= hd) return;
+    // the row's live splits: split 0 (position p) and those holding pages of positions < p
+    const int npg = (a.positions[r] + 15) / 16;
+    const int live = max(1, min(ns, (npg + a.split_pages - 1) / a.split_pages));
     const float* base = a.split_part + ((size_t)r * a.m.Hq + h) * ns * (hd + 2);
     float M = -__builtin_inff();
-    for (int k = 0; k < ns; ++k) M = fmaxf(M, base[(size_t)k * (hd + 2)]);
+    for (int k = 0; k < live; ++k) M = fmaxf(M, base[(size_t)k * (hd + 2)]);
     float L = 0.0f, O = 0.0f;
-    for (int k = 0; k < ns; ++k) {
+    for (int k = 0; k < live; ++k) {
         const float* pk = base + (size_t)k * (hd + 2);
         if (pk[0] == -__builtin_inff()) continue;  // a split with no position
         const float w = exp2f(pk[0] - M);
@@ -355,7 +360,9 @@ hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s) {
     if (a.B <= 0) return hipSuccess;
     const int G = a.m.Hq / a.m.Hkv;
     if (G < 1 || G > 8 || a.m.page_size != 16 || (a.m.hd != 64 && a.m.hd != 128)) return hipErrorInvalidValue;
-    if (a.nsplit < 1 || (a.nsplit > 1 && !a.split_part)) return hipErrorInvalidValue;
+    if (a.nsplit < 1 || a.split_pages < 1 || (long)a.nsplit * a.split_pages < a.m.max_pages_per_row ||
+        (a.nsplit > 1 && !a.split_part))
+        return hipErrorInvalidValue;
     const int gp = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
     const dim3 grid(a.m.Hkv, a.B, a.nsplit);
     if (a.m.hd == 128)
@@ -368,9 +375,13 @@ hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s) {
 
 int fast_attn_splits(int rows, int n_kv_heads, int max_pages_per_row, int n_cu, int cap) {
     const int blocks = rows * n_kv_heads;
-    if (blocks <= 0 || blocks >= 2 * n_cu) return 1;
+    if (blocks <= 0 || blocks >= 2 * n_cu) return 1;  // enough blocks: one per (row, KV head)
     int ns = (2 * n_cu + blocks - 1) / blocks;
     ns = ns < max_pages_per_row / 16 ? ns : max_pages_per_row / 16;
+    // small batches: also shares of at most 64 pages, so that a long row does not leave
+    // its one block working after the short rows' blocks are done
+    const int by_length = (max_pages_per_row + 63) / 64;
+    ns = ns > by_length ? ns : by_length;
     ns = ns < cap ? ns : cap;
     return ns < 1 ? 1 : ns;
 }

@@ -134,11 +134,14 @@ struct FastAttnArgs {
     uint16_t* out;              // [B][Hq * hd] bf16
     uint16_t* own_out;          // NULL: append K'/V at p to the cache; else [B][L][2][Hkv][hd] (the cache is not written)
     int nsplit;                 // position splits per (row, KV head): 1 = one block merges everything
+    int split_pages;            // pages per split (split k covers pages [k, k+1) * split_pages of a row)
     float* split_part;          // nsplit > 1: partials [B][Hq][nsplit][hd + 2] (m, l, O), merged by a second launch
 };
 hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s);
-// position splits of the fast attention for `rows` rows (split-KV when the (row, KV head)
-// blocks alone cannot fill the device: at least 16 pages of capacity per split)
+// position splits of the fast attention for `rows` rows: 1 when the (row, KV head) blocks
+// fill the device; else enough (row, KV head, split) blocks to fill it (at least 16 pages of
+// capacity per split) and no split longer than 64 pages of capacity, so that rows of ragged
+// lengths give blocks of bounded work
 int fast_attn_splits(int rows, int n_kv_heads, int max_pages_per_row, int n_cu, int cap);
 
 // ---------------------------------------------------------------- gate / repair / misc
