@@ -155,8 +155,9 @@ mg_status mg_verify_rows(mg_ctx* ctx, int n, const int32_t* rows, const int32_t*
  * list -- deterministic and batch-invariant by fixed tiling, which is what the
  * deterministic verifier contract of Sec. 3.2 asks for.  Its order is not the canonical
  * one of mg_verify_rows: its results match the oracle within the fast path's tolerance,
- * not bit for bit.  Outputs as mg_verify_rows: v_logits [n][vocab] fp32 (may be NULL),
- * v_tok[i] = argmax (lowest index on ties), v_kvcol[i] the row's K/V column [L][2][Hkv][hd]
+ * not bit for bit.  Outputs as mg_verify_rows: v_logits [n][vocab] fp32 (may be NULL: then
+ * the LM head runs with a fused top-2 epilogue that writes no logits, and v_tok is the same
+ * index), v_tok[i] = argmax (lowest index on ties), v_kvcol[i] the row's K/V column [L][2][Hkv][hd]
  * bf16; the cache is read (positions < positions[rows[i]]) and not written.  Shares the
  * context's workspace with the other calls (one call at a time per context). */
 mg_status mg_verify_rows_mfma(mg_ctx* ctx, int n, const int32_t* rows, const int32_t* tokens,

@@ -385,6 +385,31 @@ __global__ __launch_bounds__(64 * NW) void fast_gemm_kernel(FastGemmArgs a) {
     }
 
     // D[i][j] of a 16x16 tile sits in lane j + 16*(i/4), element i%4
+    if constexpr (EPI == FEPI_TOP2) {
+        // per row: the top-2 of the wave's 16 features (xor shuffles inside the lane group of
+        // the row), then of the block's waves (LDS), stored as the block's state of the row
+        static_assert(FT == 1, "one 16-feature tile per wave");
+        __shared__ Top2 wst[NW][16 * MT];
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                Top2 st{-__builtin_inff(), -__builtin_inff(), -1, 0};
+                if (wok[0]) top2_push(st, acc[mt][0][v], nf[0] + jl);
+#pragma unroll
+                for (int o = 1; o < 16; o <<= 1) st = top2_merge(st, top2_shfl(st, o));
+                if (jl == 0) wst[wave][16 * mt + 4 * q + v] = st;
+            }
+        __syncthreads();
+        Top2* states = reinterpret_cast<Top2*>(a.part);
+        for (int row = threadIdx.x; row < 16 * MT && row < M; row += 64 * NW) {
+            Top2 st = wst[0][row];
+#pragma unroll
+            for (int w = 1; w < NW; ++w) st = top2_merge(st, wst[w][row]);
+            states[(size_t)row * gridDim.x + nb] = st;
+        }
+        return;
+    } else {
 #pragma unroll
     for (int f = 0; f < FT; ++f) {
         if (!wok[f]) continue;
@@ -396,6 +421,32 @@ __global__ __launch_bounds__(64 * NW) void fast_gemm_kernel(FastGemmArgs a) {
                 if (row < M) fast_epilogue<EPI>(a, split, row, nf[f] + jl, acc[mt][f][v]);
             }
     }
+    }
+}
+
+// one block per row: merges the row's nblk block states (top2_merge is associative and
+// commutative, so the grouping does not change the result) and writes the top-1 index
+__global__ __launch_bounds__(256) void top1_rows_kernel(const Top2* __restrict__ states, int nblk,
+                                                        int32_t* __restrict__ top1) {
+    const int r = blockIdx.x, t = threadIdx.x;
+    Top2 st{-__builtin_inff(), -__builtin_inff(), -1, 0};
+    for (int k = t; k < nblk; k += 256) st = top2_merge(st, states[(size_t)r * nblk + k]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) st = top2_merge(st, top2_shfl(st, o));
+    __shared__ Top2 ws[4];
+    if ((t & 63) == 0) ws[t >> 6] = st;
+    __syncthreads();
+    if (t == 0) {
+        const Top2 m = top2_merge(top2_merge(ws[0], ws[1]), top2_merge(ws[2], ws[3]));
+        top1[r] = m.i1 < 0 ? 0 : m.i1;
+    }
+}
+
+hipError_t launch_top1_rows(int M, const void* states, int nblk, int32_t* top1, hipStream_t s) {
+    if (M <= 0) return hipSuccess;
+    if (nblk <= 0) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(top1_rows_kernel, dim3(M), dim3(256), 0, s, static_cast<const Top2*>(states), nblk, top1);
+    return hipGetLastError();
 }
 
 // out[i] = sum over s of part[s][i] in split order (the op-level entry point)
@@ -520,6 +571,11 @@ int fast_gemm_splits(int M, int N, int K, int n_cu) {
     return S < Smax ? S : Smax;
 }
 
+int fast_gemm_blocks(int M, int N, int K, int n_cu) {
+    const int NW = fast_gemm_waves(M, N, K, 1, n_cu);
+    return (N + 16 * NW * GM_FT - 1) / (16 * NW * GM_FT);
+}
+
 void fast_gemm_config(int M, int N, int K, int n_cu, int* S, int* waves) {
     *S = fast_gemm_splits(M, N, K, n_cu);
     *waves = fast_gemm_waves(M, N, K, *S, n_cu);
@@ -548,6 +604,7 @@ static void launch_ft(const FastGemmArgs& a, int epi, dim3 g, hipStream_t s) {
         case FEPI_BF16: launch_epi<MT, NW, FT, FEPI_BF16>(a, g, s); break;
         case FEPI_PART: launch_epi<MT, NW, FT, FEPI_PART>(a, g, s); break;
         case FEPI_SWIGLU: launch_epi<MT, NW, FT, FEPI_SWIGLU>(a, g, s); break;
+        case FEPI_TOP2: launch_epi<MT, NW, FT, FEPI_TOP2>(a, g, s); break;
         default: launch_epi<MT, NW, FT, FEPI_F32>(a, g, s); break;
     }
 }

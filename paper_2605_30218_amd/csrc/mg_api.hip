@@ -182,11 +182,15 @@ mg_status fast_gemm(mg_ctx* c, const uint16_t* X, int M, int K, const uint16_t* 
     const int Nout = epi == FEPI_SWIGLU ? a.Nseg[0] : N;
     a.N = Nout;
     a.Y = Y;
-    a.part = c->at<float>(c->plan.gemm_part);
+    // the top-2 states of the fused LM-head epilogue go where the verifier's logits would
+    // (M x blocks x 16 bytes, at most M x N x 4)
+    a.part = epi == FEPI_TOP2 ? c->at<float>(c->plan.vlog) : c->at<float>(c->plan.gemm_part);
     a.S = epi == FEPI_PART ? fast_gemm_splits(split_M ? split_M : M, N, K, c->n_cu) : 1;
     a.n_cu = c->n_cu;
     if (S_out) *S_out = a.S;
-    const double out_bytes = epi == FEPI_PART ? 4.0 * a.S * M * N : (double)M * Nout * (epi == FEPI_F32 ? 4 : 2);
+    const double out_bytes = epi == FEPI_PART   ? 4.0 * a.S * M * N
+                             : epi == FEPI_TOP2 ? 16.0 * M * fast_gemm_blocks(M, N, K, c->n_cu)
+                                                : (double)M * Nout * (epi == FEPI_F32 ? 4 : 2);
     const double bytes = 2.0 * N * K + 2.0 * M * K + out_bytes;
     ProfScope ps(c, MG_KIND_FAST_GEMM, s, bytes, 2.0 * M * N * K);
     HIPCHK(launch_fast_gemm(a, epi, s));
@@ -402,8 +406,11 @@ mg_status mg_destroy(mg_ctx* c) {
 // split_M fixes every projection's split-K (0: the row count's own split).  taps != NULL:
 // the residual stream entering layer 0 and leaving every layer is copied to
 // taps[0..L] ([L+1][B][d] bf16) as the launches run (the per-layer checks of the tests).
+// top1_out != NULL (with logits NULL): the LM head runs with the fused top-2 epilogue and
+// only each row's top-1 index is written (no logits).
 static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int32_t* positions, const int32_t* page_table,
-                       float* logits, uint16_t* own_out, int split_M, hipStream_t s, uint16_t* taps = nullptr) {
+                       float* logits, uint16_t* own_out, int split_M, hipStream_t s, uint16_t* taps = nullptr,
+                       int32_t* top1_out = nullptr) {
     const mg_model_cfg& g = c->cfg;
     const ModelDims& m = c->m;
     const int d = g.d_model, Nq = g.n_q_heads * g.head_dim, Nk = g.n_kv_heads * g.head_dim, F = g.d_ffn;
@@ -481,6 +488,11 @@ static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int
     }
     const uint16_t* W[1] = {c->W(2 + WPL * g.n_layers)};
     const int Ns[1] = {g.vocab};
+    if (top1_out) {
+        MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 1, nullptr, FEPI_TOP2, s));
+        HIPCHK(launch_top1_rows(B, c->at<void>(c->plan.vlog), fast_gemm_blocks(B, g.vocab, d, c->n_cu), top1_out, s));
+        return MG_OK;
+    }
     MGCHK(fast_gemm(c, h, B, d, W, nullptr, Ns, 1, logits, FEPI_F32, s));
     return MG_OK;
 }
@@ -509,8 +521,12 @@ mg_status mg_verify_rows_mfma(mg_ctx* c, int n, const int32_t* rows, const int32
     int32_t* vpt = vn + 4;
     float* vmargin = reinterpret_cast<float*>(vpt + (size_t)B * maxp);
     uint8_t* vgate = reinterpret_cast<uint8_t*>(vmargin + B);
-    float* logits = v_logits ? v_logits : c->at<float>(c->plan.vlog);
     HIPCHK(launch_gather_rows(n, rows, tokens, positions, page_table, maxp, vtok, vpos, vpt, s));
+    if (!v_logits) {
+        // no logits wanted: the LM head's fused top-2 epilogue gives v_tok directly
+        return fast_forward(c, n, vtok, vpos, vpt, nullptr, v_kvcol, MFMA_VERIFIER_SPLIT_M, s, nullptr, v_tok);
+    }
+    float* logits = v_logits;
     MGCHK(fast_forward(c, n, vtok, vpos, vpt, logits, v_kvcol, MFMA_VERIFIER_SPLIT_M, s));
     // v_tok = top-1 of each row (lowest index on ties); the gate outputs are scratch
     HIPCHK(launch_top2(n, c->cfg.vocab, logits, nullptr, 0.0f, v_tok, vmargin, vgate, vrowlist, vn, nullptr,

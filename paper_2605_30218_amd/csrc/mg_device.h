@@ -114,6 +114,48 @@ __device__ __forceinline__ float wave_sum_fast(float v) {
     return v;
 }
 
+// ---- top-1 / top-2 states (the margin gate and the matrix-core verifier's fused LM-head epilogue)
+// Partial state of a top-2 scan: best value/index and the runner-up value of the
+// multiset seen so far.  Merging two states is associative and commutative: the
+// winner is the larger value, the lower index on equal values; the runner-up is
+// the larger of the winner's runner-up and the loser's best.  NaN entries are
+// skipped and only flagged.
+struct Top2 {
+    float v1, v2;
+    int i1;
+    int nan;
+};
+
+__device__ __forceinline__ Top2 top2_merge(const Top2& a, const Top2& b) {
+    if (a.i1 < 0) return Top2{b.v1, b.v2, b.i1, b.nan | a.nan};
+    if (b.i1 < 0) return Top2{a.v1, a.v2, a.i1, a.nan | b.nan};
+    const bool aw = (a.v1 > b.v1) || (a.v1 == b.v1 && a.i1 < b.i1);
+    Top2 o;
+    if (aw) {
+        o.v1 = a.v1; o.i1 = a.i1; o.v2 = fmaxf(a.v2, b.v1);
+    } else {
+        o.v1 = b.v1; o.i1 = b.i1; o.v2 = fmaxf(b.v2, a.v1);
+    }
+    o.nan = a.nan | b.nan;
+    return o;
+}
+
+__device__ __forceinline__ void top2_push(Top2& s, float v, int j) {
+    if (v != v) { s.nan = 1; return; }
+    if (s.i1 < 0) { s.v1 = v; s.i1 = j; return; }
+    if (v > s.v1) { s.v2 = s.v1; s.v1 = v; s.i1 = j; }   // j increases within a thread: ties keep the old index
+    else if (v > s.v2) s.v2 = v;
+}
+
+__device__ __forceinline__ Top2 top2_shfl(const Top2& s, int o) {
+    Top2 t;
+    t.v1 = __shfl_xor(s.v1, o, MG_WAVE);
+    t.v2 = __shfl_xor(s.v2, o, MG_WAVE);
+    t.i1 = __shfl_xor(s.i1, o, MG_WAVE);
+    t.nan = __shfl_xor(s.nan, o, MG_WAVE);
+    return t;
+}
+
 // Row set of a launch: `n` rows, or the count read on the device (capped).
 struct RowCount {
     const int32_t* dev;

@@ -58,7 +58,10 @@ struct GemvArgs {
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
 
 // ---------------------------------------------------------------- fast MFMA GEMM
-enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2, FEPI_SWIGLU = 3 };
+enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2, FEPI_SWIGLU = 3, FEPI_TOP2 = 4 };
+// FEPI_TOP2 (unsplit): no output tile; each block writes, per row, the top-2 state of its
+// features (struct Top2, 16 bytes) to part[row * gridDim.x + block] (M x fast_gemm_blocks(...)
+// states), for launch_top1_rows to merge into the row's top-1 index
 // FEPI_SWIGLU (unsplit, direct-to-LDS path only): W[0] = gate rows, W[1] = up rows, N =
 // outputs; half of a block's waves take gate tiles, the other half the up tiles of the same
 // outputs, and Y[r][j] = bf16(silu(bf16(gate)) * bf16(up)) (bf16 [M][N], the fast path's exp)
@@ -76,6 +79,11 @@ struct FastGemmArgs {
 };
 hipError_t launch_fast_gemm(const FastGemmArgs& a, int epi, hipStream_t s);
 hipError_t launch_sum_partials(const float* part, int S, int64_t n, float* out, hipStream_t s);
+// blocks of an unsplit fast GEMM launch of M rows over N features (the FEPI_TOP2 states per row)
+int fast_gemm_blocks(int M, int N, int K, int n_cu);
+// top1[r] = the lowest index of the largest non-NaN value of row r, merged from the nblk
+// top-2 states per row a FEPI_TOP2 launch wrote (0 when the row has no number), r < M
+hipError_t launch_top1_rows(int M, const void* states, int nblk, int32_t* top1, hipStream_t s);
 int fast_gemm_splits(int M, int N, int K, int n_cu);
 // the split count and the waves per block a launch of M rows uses
 void fast_gemm_config(int M, int N, int K, int n_cu, int* S, int* waves);

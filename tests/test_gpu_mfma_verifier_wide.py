@@ -104,3 +104,27 @@ def test_mfma_verifier_within_tolerance_of_the_oracle_at_full_width(wide2):
         if gt[i] != rt[i]:
             srt = np.sort(rl[i])[::-1]
             assert srt[0] - srt[1] <= 2 * np.abs(gl[i] - rl[i]).max(), rows[i]
+
+
+def test_mfma_verifier_fused_top2_epilogue(wide2):
+    """Without a logits buffer the matrix-core verifier's LM head runs with the fused top-2
+    epilogue (per-block states merged per row): the same tokens and K/V columns as with the
+    logits written, and batch-invariant the same way."""
+    f = wide2
+    eng = f["eng"]
+
+    def run_nologits(rows):
+        n = len(rows)
+        vt = torch.empty(n, dtype=torch.int32, device="cuda")
+        vc = torch.empty((n, eng.col_elems), dtype=torch.int16, device="cuda")
+        eng.verify_rows_mfma(n, dev_i32(rows), dev_i32(f["tok"]), dev_i32(f["pos"]), dev_i32(f["pt"]), None, vt, vc)
+        torch.cuda.synchronize()
+        return vt.cpu().numpy(), u16(vc)
+
+    rng = np.random.default_rng(31)
+    for n in (1, 12, 33, 129, 256):
+        rows = [int(r) for r in rng.choice(NB, n, replace=False)]
+        _, t_ref, c_ref = run(f, rows)
+        t, c = run_nologits(rows)
+        np.testing.assert_array_equal(t, t_ref)
+        np.testing.assert_array_equal(c, c_ref)

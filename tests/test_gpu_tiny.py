@@ -378,6 +378,30 @@ def test_mfma_verifier_batch_invariance_1_to_256(wide):
     np.testing.assert_array_equal(u16(e.kv_pool), before)  # the cache is only read
 
 
+def test_mfma_verifier_fused_top2_matches_logits_path(wide):
+    """The matrix-core verifier without a logits buffer (fused top-2 LM-head epilogue) gives the
+    tokens and K/V columns of the path that writes the logits, for list sizes across the
+    16-row tiles and the register-operand path (129 rows and more)."""
+    p, last, pos0 = wide
+    e = p.eng
+    pt, toks, poss = dev_i32(p.pt), dev_i32(last), dev_i32(pos0)
+    rng = np.random.default_rng(41)
+    for n in (1, 5, 16, 17, 64, 128, 129, 256):
+        rows = dev_i32(rng.choice(256, n, replace=False))
+        vl = torch.empty((n, V), dtype=torch.float32, device="cuda")
+        vt = torch.empty(n, dtype=torch.int32, device="cuda")
+        vc = torch.empty((n, e.col_elems), dtype=torch.int16, device="cuda")
+        e.verify_rows_mfma(n, rows, toks, poss, pt, vl, vt, vc)
+        vt2 = torch.empty(n, dtype=torch.int32, device="cuda")
+        vc2 = torch.empty((n, e.col_elems), dtype=torch.int16, device="cuda")
+        e.verify_rows_mfma(n, rows, toks, poss, pt, None, vt2, vc2)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(vt2.cpu().numpy(), vt.cpu().numpy(), err_msg=str(n))
+        np.testing.assert_array_equal(u16(vc2), u16(vc), err_msg=str(n))
+        # and the token is the argmax of the written logits (lowest index on ties)
+        np.testing.assert_array_equal(vt.cpu().numpy(), vl.cpu().numpy().argmax(1))
+
+
 def test_mfma_verifier_within_tolerance_of_the_oracle(wide):
     """Against the oracle's canonical verifier on the same cache: logits within the fast
     path's tolerance (normwise 1e-2), the K/V column within bf16 rounding of the canonical
