@@ -470,6 +470,8 @@ def main():
     ap.add_argument("--no-extras", action="store_true", help="skip the bs=1 leg and the small-batch sweep")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run the plain copy kernel on MIB MiB five times (HBM counter scaling) and exit")
+    ap.add_argument("--read-calibration", type=int, default=0, metavar="MIB",
+                    help="only run the streaming-read kernel over MIB MiB five times (the HBM read rate) and exit")
     ap.add_argument("--prefill", choices=("canonical", "fast"), default="canonical",
                     help="prompt prefill before the timed steps (llama8b; not timed)")
     args = ap.parse_args()
@@ -491,6 +493,19 @@ def main():
         torch.cuda.synchronize()
         ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(5)]
         print(json.dumps(dict(copy_bytes=nb, launches=5, ms=ms, gbps_read_plus_write=2 * nb / (min(ms) * 1e-3) / 1e9)))
+        return
+    if args.read_calibration:
+        nb = args.read_calibration << 20
+        src = torch.ones(nb // 4, dtype=torch.int32, device="cuda")
+        sink = torch.zeros(mg.read_stream_sink_words(), dtype=torch.int32, device="cuda")
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(6)]
+        ev[0].record()
+        for i in range(5):
+            mg.op_read_stream(src, sink)
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        ms = [ev[i].elapsed_time(ev[i + 1]) for i in range(5)]
+        print(json.dumps(dict(read_bytes=nb, launches=5, ms=ms, gbps_read=nb / (min(ms) * 1e-3) / 1e9)))
         return
     cfg = args.config
     wl = WORKLOADS[cfg](args)

@@ -22,6 +22,13 @@ extern "C" {
  * n_bytes % 16 == 0; src and dst 16-byte aligned [device]. */
 mg_status mg_op_copy(int64_t n_bytes, const void* src, void* dst, void* stream);
 
+/* Reads src[0..n_bytes) once with a grid-stride streaming kernel (eight 16-byte loads in
+ * flight per thread) and stores one xor word per block into sink (mg_op_read_stream_sink_words()
+ * words): the reference for the HBM read rate of the streaming kernels.  n_bytes % 16 == 0;
+ * src 16-byte aligned, sink [device]. */
+int mg_op_read_stream_sink_words(void);
+mg_status mg_op_read_stream(int64_t n_bytes, const void* src, uint32_t* sink, void* stream);
+
 /* out[i] = bf16 round-to-nearest-even of in[i] (NaN -> quiet NaN), the device
  * conversion used at every bf16 rounding point.  in fp32 [n], out uint16 [n]. */
 mg_status mg_op_probe_bf16(int64_t n, const float* in, uint16_t* out, void* stream);

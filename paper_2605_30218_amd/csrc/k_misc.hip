@@ -430,6 +430,43 @@ hipError_t launch_copy16(int64_t n16, const void* src, void* dst, hipStream_t s)
     return hipGetLastError();
 }
 
+// Streaming read of n16 16-byte words (eight loads in flight per thread, grid-stride): the
+// reference for the HBM read rate the weight- and K/V-streaming kernels could reach.  Each
+// block stores the xor of its words to sink[block], which keeps every load.
+constexpr int READ_STREAM_BLOCKS = 16384;
+__global__ __launch_bounds__(256) void read_stream_kernel(int64_t n16, const uint4* __restrict__ src,
+                                                          uint32_t* __restrict__ sink) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+    uint32_t acc = 0;
+    for (; i + 7 * stride < n16; i += 8 * stride) {
+        uint4 v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = src[i + u * stride];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    for (; i < n16; i += stride) {
+        const uint4 v = src[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    __shared__ uint32_t red[4];
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) acc ^= __shfl_xor(acc, o, MG_WAVE);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) sink[blockIdx.x] = red[0] ^ red[1] ^ red[2] ^ red[3];
+}
+
+int read_stream_blocks() { return READ_STREAM_BLOCKS; }
+
+hipError_t launch_read_stream(int64_t n16, const void* src, uint32_t* sink, hipStream_t s) {
+    if (n16 <= 0) return hipSuccess;
+    hipLaunchKernelGGL(read_stream_kernel, dim3(READ_STREAM_BLOCKS), dim3(256), 0, s, n16,
+                       static_cast<const uint4*>(src), sink);
+    return hipGetLastError();
+}
+
 static int probe_grid(int64_t n) { return (int)((n + 255) / 256 < 4096 ? (n + 255) / 256 : 4096); }
 
 hipError_t launch_probe_bf16(int64_t n, const float* in, uint16_t* out, hipStream_t s) {

@@ -654,6 +654,14 @@ mg_status mg_op_copy(int64_t n_bytes, const void* src, void* dst, void* stream) 
     return launch_copy16(n_bytes / 16, src, dst, static_cast<hipStream_t>(stream)) == hipSuccess ? MG_OK : MG_ERR_HIP;
 }
 
+int mg_op_read_stream_sink_words(void) { return read_stream_blocks(); }
+
+mg_status mg_op_read_stream(int64_t n_bytes, const void* src, uint32_t* sink, void* stream) {
+    if (n_bytes < 0 || n_bytes % 16 || (n_bytes && (!src || !sink))) return MG_ERR_ARG;
+    return launch_read_stream(n_bytes / 16, src, sink, static_cast<hipStream_t>(stream)) == hipSuccess ? MG_OK
+                                                                                                        : MG_ERR_HIP;
+}
+
 mg_status mg_op_probe_bf16(int64_t n, const float* in, uint16_t* out, void* stream) {
     if (n < 0 || (n && (!in || !out))) return MG_ERR_ARG;
     return launch_probe_bf16(n, in, out, static_cast<hipStream_t>(stream)) == hipSuccess ? MG_OK : MG_ERR_HIP;

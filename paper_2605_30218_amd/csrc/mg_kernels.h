@@ -173,6 +173,9 @@ hipError_t launch_advance(int B, const int32_t* emitted, int32_t* tokens, int32_
 
 // element-wise numerics probes used by the tests
 hipError_t launch_copy16(int64_t n16, const void* src, void* dst, hipStream_t s);
+// streaming read of n16 16-byte words; sink receives read_stream_blocks() words
+int read_stream_blocks();
+hipError_t launch_read_stream(int64_t n16, const void* src, uint32_t* sink, hipStream_t s);
 hipError_t launch_probe_bf16(int64_t n, const float* in, uint16_t* out, hipStream_t s);
 hipError_t launch_probe_exp(int64_t n, const float* in, float* out, hipStream_t s);
 hipError_t launch_probe_divsqrt(int64_t n, const float* a, const float* b, float* q, float* r, hipStream_t s);

@@ -60,6 +60,8 @@ SIGNATURES = {
     "mg_profile_begin": (I, [P, I, I]),
     "mg_profile_end": (I, [P, I, P, P, P, P]),
     "mg_op_copy": (I, [I64, P, P, P]),
+    "mg_op_read_stream_sink_words": (I, []),
+    "mg_op_read_stream": (I, [I64, P, P, P]),
     "mg_op_probe_bf16": (I, [I64, P, P, P]),
     "mg_op_probe_exp": (I, [I64, P, P, P]),
     "mg_op_probe_divsqrt": (I, [I64, P, P, P, P, P]),
@@ -242,6 +244,16 @@ def margin_gate_noalloc(B, V, logits, protected_mask, tau, top1, margin, gate, g
 def op_copy(src, dst):
     _check("mg_op_copy", load().mg_op_copy(src.numel() * src.element_size(), src.data_ptr(), dst.data_ptr(),
                                            _stream()))
+
+
+def op_read_stream(src, sink):
+    """mg_op_read_stream: read every byte of src once (the HBM read-rate reference)."""
+    _check("mg_op_read_stream", load().mg_op_read_stream(src.numel() * src.element_size(), src.data_ptr(),
+                                                         sink.data_ptr(), _stream()))
+
+
+def read_stream_sink_words():
+    return int(load().mg_op_read_stream_sink_words())
 
 
 def op_probe_bf16(x):

@@ -114,3 +114,20 @@ def test_rmsnorm_bitexact(d, eps):
     y = mg.op_rmsnorm(to_dev_bf16(x), to_dev_bf16(g), eps).cpu().numpy().view(np.uint16)
     for r in range(9):
         np.testing.assert_array_equal(y[r], mgo.rmsnorm(mgo.CANON, x[r], g, eps))
+
+
+@pytest.mark.parametrize("n_words", [0, 4, 1 << 20, (1 << 22) + 12])
+def test_bandwidth_references_touch_every_word(n_words):
+    """The copy and streaming-read kernels behind the bandwidth calibrations: the copy is
+    exact, and the read's per-block xor words fold to the xor of the whole buffer (every
+    word read once), including a tail shorter than one grid-wide batch of loads."""
+    src_np = np.random.default_rng(n_words).integers(-(1 << 31), 1 << 31, n_words, dtype=np.int64).astype(np.int32)
+    src = torch.from_numpy(src_np).to(DEV)
+    dst = torch.zeros_like(src)
+    mg.op_copy(src, dst)
+    np.testing.assert_array_equal(dst.cpu().numpy(), src_np)
+    sink = torch.zeros(mg.read_stream_sink_words(), dtype=torch.int32, device=DEV)
+    mg.op_read_stream(src, sink)
+    folded = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    expect = np.bitwise_xor.reduce(src_np.view(np.uint32)) if n_words else np.uint32(0)
+    assert folded == expect
