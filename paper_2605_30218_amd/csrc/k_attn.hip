@@ -25,10 +25,12 @@ constexpr int ATT_MAXC = 256;   // positions per canonical chunk
 __device__ __forceinline__ float attn_scale(int hd) { return hd == 128 ? 0x1.6a09e6p-4f : 0x1.0p-3f; }
 
 // Canonical attention: one block of 256 threads per (item, KV head, chunk of 256
-// positions).  Thread j loads the K row of position j into registers and the block's
-// V rows are staged into LDS; every K and V load of the chunk is issued at once, so
-// the block waits for memory once.  The sequential chains below read LDS in unrolled
-// batches, so their loads are in flight together.
+// positions).  Every K and V load of the chunk is issued at once (coalesced: a wave reads
+// 4 whole rows per instruction), so the block waits for memory once.  K goes through LDS,
+// where the 16-byte pieces of row j sit in xor-swizzled slots (piece k at slot k ^ (j mod
+// U4)) so that thread j reads its own row without bank conflicts; V then takes the same
+// LDS space.  The sequential chains below read LDS in unrolled batches, so their loads are
+// in flight together.
 //   scores  thread j: s_j for each query head of the group, sequential fma over d, * scale
 //   chunk   wave w: heads w, w + 4: m = max_j s_j, e_j = EXP(s_j - m) in place
 //   values  thread t: d pair (2 dp, 2 dp + 1) of the heads hg, hg + 256 / (hd/2), ...:
@@ -102,30 +104,18 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     auto page_k = [&](int pg) -> const uint16_t* {
         return a.kv_pool + ((((size_t)a.layer * m.n_pages + pg) * 2) * m.Hkv + kh) * (size_t)m.page_size * HD;
     };
-    // K row of position t and the V pieces.  Every load is unconditional, so the waits
-    // below count requests exactly and the queries can be staged while K and V are in
-    // flight: positions past the chunk's last live one (nj - 1) re-read that position (a
-    // cache hit; those values are never used).  The verifier's own column stands in for
-    // the cache's tentative column p.
-    // (V pieces as a native vector type: a struct copy held across the scores stays in memory)
+    // K and V pieces: iteration k covers positions PPI*k .. PPI*k + PPI-1 (PPI/16 pages), thread t
+    // piece t mod U4 of position t / U4 of those.  Every load is unconditional, so the waits
+    // below count requests exactly and the queries can be staged while K and V are in flight:
+    // positions past the chunk's last live one (nj - 1) re-read that position (a cache hit;
+    // those values are never used).  The verifier's own column stands in for the cache's
+    // tentative column p (the fold path's rotated own K row is taken from kown below).
+    // (pieces as a native vector type: a struct copy held across the scores stays in memory)
     using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
-    uint4 kr[U4];
-    u32x4 vr[NLD];
-    // (the page is taken from the unclamped position: pgs is clamped to the current
-    // position's page, which is also the page of the clamped position nj - 1)
-    {
-        const int jt = min(t, nj - 1);
-        int pg = pgs[0];
-#pragma unroll
-        for (int k = 1; k < NPG; ++k) pg = (t >> 4) == k ? pgs[k] : pg;
-        const uint16_t* kc = page_k(pg) + (size_t)(jt & 15) * HD;
-        const uint4* kp = reinterpret_cast<const uint4*>((own && j0 + jt == p) ? own : kc);
-#pragma unroll
-        for (int k = 0; k < U4; ++k) kr[k] = kp[k];
-    }
-    // V: iteration k covers positions PPI*k .. PPI*k + PPI-1, i.e. PPI/16 pages
     constexpr int PPI = 256 / U4, PGI = PPI / 16;
     const int sub = (t / U4) >> 4;
+    u32x4 kq[NLD], vr[NLD];
+    const uint16_t* vps[NLD];
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
         const int e = t + 256 * k;
@@ -133,12 +123,15 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
         int pg = pgs[PGI * k];
 #pragma unroll
         for (int q2 = 1; q2 < PGI; ++q2) pg = sub == q2 ? pgs[PGI * k + q2] : pg;
-        const uint16_t* vc = page_k(pg) + kv_stride + (size_t)(jj & 15) * HD;
-        const uint16_t* vp = (own && j0 + jj == p)    ? own + Nk
-                             : (fold && j0 + jj == p) ? qkv_row + m.Hq * HD + Nk + (size_t)kh * HD
-                                                      : vc;
-        vr[k] = *reinterpret_cast<const u32x4*>(vp + pc * 8);
+        const uint16_t* kc = page_k(pg) + (size_t)(jj & 15) * HD + pc * 8;
+        const bool at_p = j0 + jj == p;
+        kq[k] = *reinterpret_cast<const u32x4*>((own && at_p) ? own + pc * 8 : kc);
+        vps[k] = (own && at_p)    ? own + Nk + pc * 8
+                 : (fold && at_p) ? qkv_row + m.Hq * HD + Nk + (size_t)kh * HD + pc * 8
+                                  : kc + kv_stride;
     }
+#pragma unroll
+    for (int k = 0; k < NLD; ++k) vr[k] = *reinterpret_cast<const u32x4*>(vps[k]);
     if (!fold) {
         float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
         qd[0] = make_float4(bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y));
@@ -185,10 +178,19 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
             }
         }
     }
-    // the queries staged by other threads are needed from here on; the K and V requests stay
-    // in flight across this barrier (loads complete in order: the queries came first)
+    // K into LDS, swizzled (the V requests stay in flight: loads complete in order)
+#pragma unroll
+    for (int k = 0; k < NLD; ++k) {
+        const int e = t + 256 * k;
+        const int jj = e / U4, pc = e % U4;
+        *reinterpret_cast<u32x4*>(vs + (jj * U4 + (pc ^ (jj % U4))) * 4) = kq[k];
+    }
+    // the queries and K rows staged by other threads are needed from here on
     __syncthreads();
-    // (fold) the thread of position p takes the rotated own K row
+    // thread t's K row (the fold path's thread of position p takes the rotated own K row)
+    uint4 kr[U4];
+#pragma unroll
+    for (int k = 0; k < U4; ++k) kr[k] = *reinterpret_cast<const uint4*>(vs + (t * U4 + (k ^ (t % U4))) * 4);
     if (own_here && t == nj - 1) {
 #pragma unroll
         for (int k = 0; k < U4; ++k) kr[k] = reinterpret_cast<const uint4*>(kown)[k];
@@ -227,14 +229,15 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
 #pragma unroll
         for (int h = 0; h < GP; ++h) ps[h * ATT_MAXC + t] = sc[h] * scale;
     }
+    // every K read is done before V takes the LDS space
+    __syncthreads();
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
         const int e = t + 256 * k;
         *reinterpret_cast<u32x4*>(vs + (e / U4) * HP + (e % U4) * 4) = vr[k];
     }
-    __syncthreads();
 
-    // ---- chunk max and exponentials
+    // ---- chunk max and exponentials (scores only: no barrier needed after the V stores)
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
         const int h = wave + 4 * hh;
