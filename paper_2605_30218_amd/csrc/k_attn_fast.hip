@@ -50,15 +50,28 @@ constexpr int FA_PGCAP = 1024;  // page indices held in LDS (positions < 16384);
 __device__ __forceinline__ float fa_scale(int hd) { return hd == 128 ? 0x1.6a09e6p-4f : 0x1.0p-3f; }
 
 template <int HD, int GP>
-__global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <= 4 ? MG_FA_MIN_WAVES : 1))) void attn_fast_fused_kernel(FastAttnArgs a) {
+__global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(MG_FA_MIN_WAVES))) void attn_fast_fused_kernel(FastAttnArgs a) {
     constexpr int DG = HD / 8;    // 16-byte d-groups per row
     constexpr int PPI = 64 / DG;  // positions per V load instruction
     constexpr int VL = 16 / PPI;  // V loads per lane per page step
     constexpr int KST = HD / 32;  // MFMA k-steps over d
     constexpr int H2 = HD / 2;
     const ModelDims& m = a.m;
-    const int kh = blockIdx.x, r = blockIdx.y, split = blockIdx.z;
-    const int G = m.Hq / m.Hkv, Nq = m.Hq * HD, Nk = m.Hkv * HD, N = Nq + 2 * Nk;
+    const int Gall = m.Hq / m.Hkv, Nq = m.Hq * HD, Nk = m.Hkv * HD, N = Nq + 2 * Nk;
+    // block -> (row, KV head, head group of up to GP query heads).  With several head groups
+    // the blocks of one (row, KV head) are 8 block ids apart: blocks are dealt to the 8 XCDs
+    // round-robin, so they run on the same XCD at about the same time and all but the first
+    // read the pages from that XCD's L2
+    const int HG = (Gall + GP - 1) / GP;
+    int u = blockIdx.x, hg = 0;
+    if (HG > 1) {
+        const int w = blockIdx.x % (8 * HG);
+        u = blockIdx.x / (8 * HG) * 8 + w % 8;
+        hg = w / 8;
+    }
+    if (u >= a.B * m.Hkv) return;
+    const int kh = u % m.Hkv, r = u / m.Hkv, split = blockIdx.z;
+    const int hoff = hg * GP, G = min(GP, Gall - hoff);  // this block's query heads: hoff .. hoff + G - 1 of the group
     const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
     const int jl = lane & 15, qg = lane >> 4;
     const int dg = lane % DG, po = lane / DG;
@@ -80,6 +93,7 @@ __global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <
     // merge reads only the row's live splits)
     const int pg0 = split * a.split_pages, pg1 = min(npg, pg0 + a.split_pages);
     const bool first = split == 0;
+    const bool writer = first && hg == 0;  // the block that appends the tentative column
     if (!first && pg0 >= npg) return;
     const bool pg_lds = pg1 - pg0 <= FA_PGCAP;
 
@@ -92,7 +106,7 @@ __global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <
             const int f = 4 * q4;
             int n, nb;
             const uint16_t* b;
-            if (f < G * HD) { n = kh * G * HD + f; b = a.bq; nb = n; }
+            if (f < G * HD) { n = (kh * Gall + hoff) * HD + f; b = a.bq; nb = n; }
             else if (f < (G + 1) * HD) { nb = kh * HD + f - G * HD; n = Nq + nb; b = a.bk; }
             else { nb = kh * HD + f - (G + 1) * HD; n = Nq + Nk + nb; b = a.bv; }
             // splits summed in split order; loads issued in batches of 8
@@ -144,7 +158,7 @@ __global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <
                 qb[head * HD + ii] = (uint16_t)o1;
                 qb[head * HD + ii + H2] = (uint16_t)o2;
             } else {
-                if (first) {
+                if (writer) {
                     kdst[ii] = (uint16_t)o1;
                     kdst[ii + H2] = (uint16_t)o2;
                 }
@@ -154,7 +168,7 @@ __global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <
         }
         for (int d = t; d < HD; d += FA_THREADS) {
             const float v = y[(G + 1) * HD + d];
-            if (first) vdst[d] = (uint16_t)f2bf(v);
+            if (writer) vdst[d] = (uint16_t)f2bf(v);
             vps[d] = v;
         }
     }
@@ -311,9 +325,9 @@ __global__ __launch_bounds__(FA_THREADS) __attribute__((amdgpu_waves_per_eu(GP <
             }
         }
         if (a.nsplit == 1) {
-            a.out[(size_t)r * Nq + (size_t)(kh * G + h) * HD + d] = (uint16_t)f2bf(O / L);
+            a.out[(size_t)r * Nq + (size_t)(kh * Gall + hoff + h) * HD + d] = (uint16_t)f2bf(O / L);
         } else {
-            float* dst = a.split_part + (((size_t)r * m.Hq + kh * G + h) * a.nsplit + split) * (HD + 2);
+            float* dst = a.split_part + (((size_t)r * m.Hq + kh * Gall + hoff + h) * a.nsplit + split) * (HD + 2);
             if (d == 0) {
                 dst[0] = M;
                 dst[1] = L;
@@ -351,8 +365,7 @@ static void launch_hd(const FastAttnArgs& a, int gp, dim3 grid, hipStream_t s) {
     switch (gp) {
         case 1: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 1>), grid, dim3(FA_THREADS), 0, s, a); break;
         case 2: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 2>), grid, dim3(FA_THREADS), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 4>), grid, dim3(FA_THREADS), 0, s, a); break;
-        default: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 8>), grid, dim3(FA_THREADS), 0, s, a); break;
+        default: hipLaunchKernelGGL((attn_fast_fused_kernel<HD, 4>), grid, dim3(FA_THREADS), 0, s, a); break;
     }
 }
 
@@ -363,14 +376,20 @@ hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s) {
     if (a.nsplit < 1 || a.split_pages < 1 || (long)a.nsplit * a.split_pages < a.m.max_pages_per_row ||
         (a.nsplit > 1 && !a.split_part))
         return hipErrorInvalidValue;
-    const int gp = G <= 1 ? 1 : G <= 2 ? 2 : G <= 4 ? 4 : 8;
-    const dim3 grid(a.m.Hkv, a.B, a.nsplit);
+    const int gp = G <= 1 ? 1 : G <= 2 ? 2 : 4;
+    const int HG = fast_attn_head_groups(a.m.Hq, a.m.Hkv), units = a.B * a.m.Hkv;
+    const dim3 grid(HG == 1 ? units : (units + 7) / 8 * 8 * HG, 1, a.nsplit);
     if (a.m.hd == 128)
         launch_hd<128>(a, gp, grid, s);
     else
         launch_hd<64>(a, gp, grid, s);
     if (a.nsplit > 1) hipLaunchKernelGGL(attn_fast_split_merge_kernel, dim3(a.m.Hq, a.B), dim3(a.m.hd), 0, s, a);
     return hipGetLastError();
+}
+
+int fast_attn_head_groups(int n_q_heads, int n_kv_heads) {
+    const int G = n_q_heads / n_kv_heads;
+    return G <= 4 ? 1 : (G + 3) / 4;
 }
 
 int fast_attn_splits(int rows, int n_kv_heads, int max_pages_per_row, int n_cu, int cap) {

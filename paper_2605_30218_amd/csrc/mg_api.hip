@@ -451,8 +451,8 @@ static mg_status fast_forward(mg_ctx* c, int B, const int32_t* tokens, const int
             a.own_out = own_out;
             // split-KV when the (row, KV head) blocks cannot fill the device; the matrix-core
             // verifier fixes the split as for split_M rows, whatever its own row count
-            a.nsplit = fast_attn_splits(split_M ? split_M : B, g.n_kv_heads, g.max_pages_per_row, c->n_cu,
-                                        c->plan.chunks_canon);
+            a.nsplit = fast_attn_splits(split_M ? split_M : B, g.n_kv_heads * fast_attn_head_groups(g.n_q_heads, g.n_kv_heads),
+                                        g.max_pages_per_row, c->n_cu, c->plan.chunks_canon);
             a.split_pages = (g.max_pages_per_row + a.nsplit - 1) / a.nsplit;
             a.split_part = c->at<float>(c->plan.attn_part);
             ProfScope ps(c, MG_KIND_FAST_ATTN, s, 0.0);

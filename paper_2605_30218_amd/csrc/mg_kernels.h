@@ -150,7 +150,11 @@ hipError_t launch_fast_attention(const FastAttnArgs& a, hipStream_t s);
 // fill the device; else enough (row, KV head, split) blocks to fill it (at least 16 pages of
 // capacity per split) and no split longer than 64 pages of capacity, so that rows of ragged
 // lengths give blocks of bounded work
+// (row, KV head) units: `n_kv_heads` is the KV-head count times the head groups
 int fast_attn_splits(int rows, int n_kv_heads, int max_pages_per_row, int n_cu, int cap);
+// blocks per (row, KV head, split): query-head groups of at most 4 (more than 4 heads per
+// block do not fit two blocks per CU in registers)
+int fast_attn_head_groups(int n_q_heads, int n_kv_heads);
 
 // ---------------------------------------------------------------- gate / repair / misc
 // top-1 / top-2 of B <= 256 logit rows in two launches (vocabulary slices, then a
