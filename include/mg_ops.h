@@ -41,9 +41,12 @@ mg_status mg_op_probe_divsqrt(int64_t n, const float* a, const float* b, float* 
 
 /* Y[r][j] = sum_k X[r][k] * W[j][k] in fp32 (no bias, no rounding to bf16), for
  * r < n <= 256, N % 16 == 0, K % 8 == 0.  canon = 1: the verifier's canonical
- * GEMV (CDOT order, bit-reproducible); canon = 0: the fast path's MFMA GEMM with
- * its split-K choice for this shape, which needs a workspace of
- * mg_op_linear_workspace_bytes(n, N, K) bytes (ignored when canon = 1).
+ * GEMV (CDOT order, bit-reproducible) with the kernel the verifier would pick for n
+ * rows; canon = 2 / 3: the same GEMV forced onto its vector-fma kernel / its
+ * matrix-core kernel (the two give identical bits; tests compare both with the
+ * oracle at every shape); canon = 0: the fast path's MFMA GEMM with its split-K
+ * choice for this shape, which needs a workspace of
+ * mg_op_linear_workspace_bytes(n, N, K) bytes (ignored when canon != 0).
  * bias must be NULL.  X bf16 [n][K], W bf16 [N][K], Y fp32 [n][N]. */
 size_t mg_op_linear_workspace_bytes(int n, int N, int K);
 mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const uint16_t* W, const uint16_t* bias,

@@ -333,7 +333,7 @@ static bool gemv_three_features(int N, int R, int n_cu) {
     return (b3 + n_cu - 1) / n_cu * 3 < (b2 + n_cu - 1) / n_cu * 2;
 }
 
-hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
+hipError_t launch_canon_gemv_valu(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
     if (!a.n_dev && rows <= MG_GEMV_EXACT_MAX) {
@@ -368,6 +368,19 @@ hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     if (!a.n_dev && rows % 16 == 0) return launch_jr<MG_GEMV_J_R16, 16, true>(a, epi, rows, s);
     if (rows > 8) return launch_jr<MG_GEMV_J_R16, 16, false>(a, epi, rows, s);
     return launch_jr<MG_GEMV_J_R8, 8, false>(a, epi, rows, s);
+}
+
+// Which of the two bit-identical kernels runs: the matrix-core one (k_gemv_mfma.hip) where it
+// was measured faster -- a host count of 12..16 rows (one 16-row tile with few dead rows) or
+// more than 24 (32-row tiles), and device counts that may exceed 24 -- the fma kernel above
+// otherwise (its exact 4..24-row tiles waste fewer lanes on small and mid counts).  Measured
+// per projection shape at 1, 8, 12, 16, 20, 32 and 64 rows (Llama-8B shapes): e.g. gate/up at
+// 16 rows 47.6 vs 63.2 us, LM head at 64 rows 825 vs 1167 us; at 8 rows 46.8 vs 40.9 and 241.5
+// vs 182.9.
+hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
+    const int rows = a.n_dev ? a.cap : a.n_host;
+    const bool mfma = a.n_dev ? rows > MG_GEMV_EXACT_MAX : (rows >= 12 && rows <= 16) || rows > MG_GEMV_EXACT_MAX;
+    return mfma ? launch_canon_gemv_mfma(a, epi, s) : launch_canon_gemv_valu(a, epi, s);
 }
 
 }  // namespace mg

@@ -1,0 +1,334 @@
+// k_gemv_mfma.hip -- the verifier's canonical GEMV on the matrix cores.
+//
+// Same arithmetic as canon_gemv_kernel (k_gemv.hip), bit for bit: y[r][j] = CDOT(x[r], W[j])
+// with CDOT's 64 chains (chain l owns the 8-element groups g = l mod 64 and fma-accumulates
+// them in increasing g, element order inside a group, from +0) combined by the xor butterfly
+// over chain offsets 32, 16, 8, 4, 2, 1.
+//
+// The fma steps run on v_mfma_f32_16x16x1_4b_f32.  With K = 1 every output element of that
+// instruction is one fused multiply-add, d = fma(a, b, c) with a single IEEE rounding (a
+// probe over 8.4M cases with subnormals, signed zeros, infinities and cancellation found it
+// equal to fmaf bit for bit), and its four blocks are four independent 16 x 16 outer
+// products.  So one instruction advances 4 chains (the blocks) x 16 features (A rows) x 16
+// rows (B columns) by one element: block bk of lane 16 bk + i takes feature i's weight and
+// row i's activation of its chain's element, and D holds (block bk, feature i, row j) in
+// register 4 bk + i % 4 of lane 16 (i / 4) + j.
+//
+// Work split.  A block owns FG groups of 16 features (a SwiGLU group is 8 gate rows and the
+// 8 matching up rows) and a tile of 16 rows; NWB waves serve each feature group.  K is walked
+// in stages of 256 elements (32 groups: the chains of one half, l = 32 p + ..., p = stage
+// parity).  Every stage, weights and activations go through LDS by direct-to-LDS loads: one
+// load moves two 512-byte runs (two rows of the stage), and group g of stage row r sits at
+// slot 32 r + (g xor (r mod 16)), so each run is one contiguous read and each MFMA operand
+// read (16 rows, one group) hits 16 distinct bank groups.  The stages form a ring of D
+// buffers (stage s + D is requested into the buffer of stage s once every wave holds stage
+// s's operands in registers; the operands of stage s + 1 are read while the MFMAs of stage s
+// run); the loads of a stage are shared by all waves, so each stage starts on a block barrier.  The compiler does not count
+// direct-to-LDS loads when it places waits, so the operand reads, their waits, the barrier and
+// every wait for the loads are explicit.
+// Chain bits of wave w of its feature group (NWB = 4: l = 32 p + 16 qq + 4 w + bk; NWB = 8:
+// l = 32 p + 4 w + bk): the bits above the wave bits are the wave's own, then come the wave
+// bits, then the instruction's blocks.  Butterfly, in the order of the offsets: the wave's
+// own bits by register adds, the wave bits through LDS, the block bits by register adds of
+// the four block registers of a lane.  IEEE addition is commutative, so pairing operands in
+// either order gives the same bits as the single-lane butterfly.
+// Groups past K read a group of -0 weights and +0 activations: fma(-0, +0, c) = c + (-0) = c
+// for every c, so those chains are left unchanged.  Rows past the count compute on a copy of
+// the last live row and are not written; features past N on a copy of the last feature.
+#include <type_traits>
+
+#include "mg_device.h"
+#include "mg_kernels.h"
+
+namespace mg {
+
+typedef float mg_v16f __attribute__((ext_vector_type(16)));
+typedef uint32_t mg_u32x4 __attribute__((ext_vector_type(4)));
+
+// one 8-element group of bf16 -0 (weights) and of +0 (activations) for groups past K
+__device__ __align__(16) const uint16_t k_neg_zero_group[8] = {0x8000, 0x8000, 0x8000, 0x8000,
+                                                              0x8000, 0x8000, 0x8000, 0x8000};
+__device__ __align__(16) const uint16_t k_pos_zero_group[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+
+__device__ __forceinline__ float bfe(const mg_u32x4& v, int e) {
+    const uint32_t w = v[e >> 1];
+    return (e & 1) ? bf_hi(w) : bf_lo(w);
+}
+
+template <int N>
+__device__ __forceinline__ void gv_wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+__device__ __forceinline__ void gv_barrier() { asm volatile("s_barrier" ::: "memory"); }
+__device__ __forceinline__ void gv_lds_read(mg_u32x4& v, const uint4* p) {
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"((uint32_t)(uintptr_t)p));
+}
+// waits for the operand reads and names every operand as read and written by the wait, so
+// no use of one can be scheduled before it
+template <int NQ, int T>
+__device__ __forceinline__ void gv_lds_wait(mg_u32x4 (&av)[NQ], mg_u32x4 (&bv)[T][NQ]) {
+    if constexpr (NQ == 1 && T == 1) {
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(av[0]), "+v"(bv[0][0]) : : "memory");
+    } else if constexpr (NQ == 2 && T == 1) {
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(av[0]), "+v"(av[1]), "+v"(bv[0][0]), "+v"(bv[0][1]) : : "memory");
+    } else {
+        static_assert(NQ == 1 && T == 2, "quads per stage x row tiles");
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(av[0]), "+v"(bv[0][0]), "+v"(bv[1][0]) : : "memory");
+    }
+}
+
+template <int FG, int NWB, int T, int EPI, int D, bool RAGGED>
+__global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4)) void canon_gemv_mfma_kernel(GemvArgs a, int n_fg, int n_rt) {
+    constexpr int NW = FG * NWB;
+    constexpr int NQ = 8 / NWB;                 // quads of a wave per stage
+    constexpr int SROWS = 16 * FG + 16 * T;     // rows of a stage: weights, then activations
+    constexpr int NLD = SROWS / 2;              // direct-to-LDS loads per stage
+    constexpr int IPW = NLD / NW;               // loads per wave per stage
+    static_assert(NWB == 4 || NWB == 8, "waves per feature group");
+    static_assert(2 * NQ * T <= 4, "accumulators");
+    static_assert(NLD % NW == 0, "every wave issues the same loads (exact waits)");
+    const int b = blockIdx.x;
+    const int xcd = b & 7, slot = b >> 3;
+    const int fb = (slot / n_rt) * 8 + xcd;     // feature block (FG groups)
+    const int rt = slot % n_rt;
+    if (fb * FG >= n_fg) return;
+    RowCount rc{a.n_dev, a.n_host, a.cap};
+    const int n = rc.get();
+    const int r0 = rt * 16 * T;
+    if (r0 >= n) return;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+    const int fgw = wave / NWB, wb = wave % NWB;
+    const int bk = lane >> 4, ii = lane & 15;
+    const int K = a.K, G = K >> 3;
+    const int nst = (G + 31) >> 5;
+
+    __shared__ __attribute__((aligned(16))) uint4 ring[D][SROWS * 32];
+
+    // the rows this lane loads: load m = wave + NW t of a stage covers stage rows 2m, 2m+1;
+    // this lane's half is row 2m + (lane >> 5), its slot lane & 31
+    const uint16_t* src_row[IPW];
+    int sw[IPW];
+    bool is_w[IPW];
+#pragma unroll
+    for (int t = 0; t < IPW; ++t) {
+        const int m = wave + NW * t;
+        const int r = 2 * m + (lane >> 5);
+        is_w[t] = r < 16 * FG;
+        if (r < 16 * FG) {
+            const int fgl = fb * FG + r / 16, i = r % 16;
+            if constexpr (EPI == EPI_SWIGLU) {
+                const int pj = min(fgl * 8 + (i & 7), a.N - 1);
+                src_row[t] = a.W[i >> 3] + (size_t)pj * K;
+            } else {
+                int j = min(fgl * 16 + i, a.N - 1), seg = 0;
+                while (seg < 2 && j >= a.Nseg[seg]) { j -= a.Nseg[seg]; ++seg; }
+                src_row[t] = a.W[seg] + (size_t)j * K;
+            }
+        } else {
+            src_row[t] = a.X + (size_t)min(r0 + r - 16 * FG, n - 1) * K;
+        }
+        sw[t] = (lane & 31) ^ (r & 15);  // the group this lane's slot holds
+    }
+    // the loads of stage s into buffer s % D (clamped to the last stage)
+    auto issue = [&](int s) {
+        const int sc = min(s, nst - 1);
+        uint4* buf = ring[s % D];
+#pragma unroll
+        for (int t = 0; t < IPW; ++t) {
+            const int g = sc * 32 + sw[t];
+            const uint16_t* src = src_row[t] + (size_t)g * 8;
+            if constexpr (RAGGED) src = g < G ? src : (is_w[t] ? k_neg_zero_group : k_pos_zero_group);
+            __builtin_amdgcn_global_load_lds(src, buf + 64 * (wave + NW * t), 16, 0, 0);
+        }
+    };
+
+    mg_v16f acc[T][2 * NQ];  // [row tile][2 qi + p] (qi: the wave's quad of a stage, p: stage parity)
+#pragma unroll
+    for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int k = 0; k < 2 * NQ; ++k)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[t][k][r] = 0.0f;
+
+    // operand slots of quad qi (group of the stage: NWB = 4: 16 qi + 4 wb + bk; NWB = 8: 4 wb + bk)
+    int aslot[NQ], bslot[T][NQ];
+#pragma unroll
+    for (int qi = 0; qi < NQ; ++qi) {
+        const int lg = (NWB == 4 ? 16 * qi : 0) + 4 * wb + bk;
+        aslot[qi] = 32 * (16 * fgw + ii) + (lg ^ ii);
+#pragma unroll
+        for (int t = 0; t < T; ++t) bslot[t][qi] = 32 * (16 * FG + 16 * t + ii) + (lg ^ ii);
+    }
+    // operand reads of stage s (raw bf16 groups), waited for one stage later
+    struct Ops {
+        mg_u32x4 a[NQ], b[T][NQ];
+    };
+    auto read_ops = [&](int s, Ops& o) {
+        const uint4* buf = ring[s % D];
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi) {
+            gv_lds_read(o.a[qi], buf + aslot[qi]);
+#pragma unroll
+            for (int t = 0; t < T; ++t) gv_lds_read(o.b[t][qi], buf + bslot[t][qi]);
+        }
+    };
+    // the MFMAs of one stage into the accumulators of parity P (a compile-time index, so the
+    // accumulators stay in registers)
+    auto mfmas = [&](const Ops& o, auto P) {
+        constexpr int p = decltype(P)::value;
+        // a quad's operands converted into their own registers before its MFMAs, so no
+        // conversion waits on an MFMA still reading the register it would overwrite
+#pragma unroll
+        for (int qi = 0; qi < NQ; ++qi) {
+            float fa[8], fx[T][8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                fa[e] = bfe(o.a[qi], e);
+#pragma unroll
+                for (int t = 0; t < T; ++t) fx[t][e] = bfe(o.b[t][qi], e);
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+#pragma unroll
+                for (int t = 0; t < T; ++t)
+                    acc[t][2 * qi + p] = __builtin_amdgcn_mfma_f32_16x16x1f32(fa[e], fx[t][e], acc[t][2 * qi + p], 0, 0, 0);
+        }
+    };
+    // One stage: its operands (read one stage earlier) are waited for; then, if a stage
+    // follows, this wave's loads of stage s + 1 are waited for (stages s + 1 .. s + D - 1 are
+    // requested while s + D - 1 < nst, so D - 2 stages of loads may remain; near the end
+    // none), the barrier makes every wave's loads of s + 1 visible and every read of stage
+    // s finished, the loads of stage s + D go to the buffer of s, and the operands of s + 1 are
+    // requested; then the MFMAs of stage s run from registers.
+    auto step = [&](int s, Ops& cur, Ops& nxt, auto P) {
+        gv_lds_wait<NQ, T>(cur.a, cur.b);
+        if (s + 1 < nst) {
+            if (s + D - 1 < nst) gv_wait_vmcnt<IPW * (D - 2)>();
+            else gv_wait_vmcnt<0>();
+            gv_barrier();
+            if (s + D < nst) issue(s + D);
+            read_ops(s + 1, nxt);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(cur, P);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // ring: stages 0 .. D - 1 requested up front, one per buffer (clamped past the last
+    // stage: a clamped stage is never read)
+#pragma unroll
+    for (int s = 0; s < D; ++s) issue(s);
+    gv_wait_vmcnt<IPW * (D - 1)>();
+    gv_barrier();
+    Ops oa, ob;
+    read_ops(0, oa);
+    for (int s = 0; s < nst; s += 2) {
+        step(s, oa, ob, std::integral_constant<int, 0>{});
+        if (s + 1 < nst) step(s + 1, ob, oa, std::integral_constant<int, 1>{});
+    }
+    gv_wait_vmcnt<0>();  // (clamped prologue loads of a short K)
+
+    // butterfly, the wave's own bits: stage parity (offset 32), then for NWB = 4 the quad (16);
+    // then the wave bits through LDS (the ring is free once every wave is past its last read),
+    // one row tile at a time; then the block bits
+    float* red = reinterpret_cast<float*>(&ring[0][0]);  // [NW][16][64]
+    static_assert(NW * 16 * 64 * 4 <= D * SROWS * 32 * 16, "the reduction fits in the ring");
+    const int col = wb & 3;  // register column i % 4 that waves wb < 4 finish
+    float vt[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        mg_v16f tot;
+        if constexpr (NQ == 2) {
+            tot = (acc[t][0] + acc[t][1]) + (acc[t][2] + acc[t][3]);
+        } else {
+            tot = acc[t][0] + acc[t][1];
+        }
+        gv_barrier();  // every wave is past its last read of the ring (or of the previous tile)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[(wave * 16 + r) * 64 + lane] = tot[r];
+        __syncthreads();
+        float s4[4];
+#pragma unroll
+        for (int bb = 0; bb < 4; ++bb) {
+            float v[NWB];
+#pragma unroll
+            for (int w = 0; w < NWB; ++w) v[w] = red[((fgw * NWB + w) * 16 + 4 * bb + col) * 64 + lane];
+#pragma unroll
+            for (int h = NWB / 2; h >= 1; h >>= 1)
+#pragma unroll
+                for (int w = 0; w < h; ++w) v[w] = v[w] + v[w + h];
+            s4[bb] = v[0];
+        }
+        vt[t] = (s4[0] + s4[2]) + (s4[1] + s4[3]);  // block bits: offsets 2 then 1
+    }
+    if (wb >= 4) return;
+
+    // epilogue: lane 16 (i / 4) + j holds feature i = 4 (lane / 16) + col, row j = lane % 16
+    const int fgl = fb * FG + fgw;
+    const int i = 4 * (lane >> 4) + col;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+        const float v = vt[t];
+        const int row = r0 + 16 * t + (lane & 15);
+        if constexpr (EPI == EPI_SWIGLU) {
+            // gate outputs sit in lanes 0..31 (i < 8), their up rows 32 lanes higher
+            const float upv = __shfl_xor(v, 32, MG_WAVE);
+            const int pj = fgl * 8 + i;
+            if (lane >= 32 || row >= n || pj >= a.N) continue;
+            const float g = bf2f(f2bf(v)), up = bf2f(f2bf(upv));
+            const float sg = ieee_div(g, 1.0f + canon_exp(-g));
+            reinterpret_cast<uint16_t*>(a.Y)[(size_t)row * a.N + pj] = (uint16_t)f2bf(sg * up);
+        } else {
+            const int j = fgl * 16 + i;
+            if (row >= n || j >= a.N) continue;
+            if (EPI == EPI_F32) {
+                reinterpret_cast<float*>(a.Y)[(size_t)row * a.N + j] = v;
+            } else if (EPI == EPI_BF16) {
+                int jl = j, seg = 0;
+                while (seg < 2 && jl >= a.Nseg[seg]) { jl -= a.Nseg[seg]; ++seg; }
+                const float y = a.bias[seg] ? v + bf2f(a.bias[seg][jl]) : v;
+                reinterpret_cast<uint16_t*>(a.Y)[(size_t)row * a.N + j] = (uint16_t)f2bf(y);
+            } else {  // residual: x = bf16(x + bf16(y))
+                uint16_t* xp = reinterpret_cast<uint16_t*>(a.Y) + (size_t)row * a.N + j;
+                *xp = (uint16_t)f2bf(bf2f(*xp) + bf2f(f2bf(v)));
+            }
+        }
+    }
+}
+
+template <int FG, int NWB, int T, int D, bool RG>
+static hipError_t launch_mfma_cfg(const GemvArgs& a, int epi, int rows, hipStream_t s) {
+    const int n_fg = epi == EPI_SWIGLU ? (a.N + 7) / 8 : (a.N + 15) / 16;
+    const int n_fb = (n_fg + FG - 1) / FG;
+    const int n_rt = (rows + 16 * T - 1) / (16 * T);
+    const dim3 grid(8 * ((n_fb + 7) / 8) * n_rt), block(64 * FG * NWB);
+    switch (epi) {
+        case EPI_SWIGLU: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_SWIGLU, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_BF16, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_RESID, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+        default: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_F32, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+    }
+    return hipGetLastError();
+}
+
+template <bool RG>
+static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool wide, hipStream_t s) {
+    if (rows > 16) return wide ? launch_mfma_cfg<2, 8, 2, 2, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 3, RG>(a, epi, rows, s);
+    return wide ? launch_mfma_cfg<2, 4, 1, 3, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 1, 2, RG>(a, epi, rows, s);
+}
+
+// Launch rule: one 16-row tile per block up to 16 rows, two above (their MFMAs share the
+// weight operand); two feature groups per block where that leaves every CU at least four
+// blocks, else one group served by 8 waves, so the narrow outputs still fill the chip.
+hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s) {
+    const int rows = a.n_dev ? a.cap : a.n_host;
+    if (rows <= 0 || a.N <= 0) return hipSuccess;
+    const int n_fg = epi == EPI_SWIGLU ? (a.N + 7) / 8 : (a.N + 15) / 16;
+    const int n_cu = a.n_cu > 0 ? a.n_cu : 256;
+    const int n_rt = rows > 16 ? (rows + 31) / 32 : 1;
+    const bool wide = (long)(n_fg / 2) * n_rt >= 4L * n_cu;
+    return a.K % 256 ? launch_mfma_rg<true>(a, epi, rows, wide, s) : launch_mfma_rg<false>(a, epi, rows, wide, s);
+}
+
+}  // namespace mg

@@ -685,7 +685,7 @@ size_t mg_op_linear_workspace_bytes(int n, int N, int K) {
 
 mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const uint16_t* W, const uint16_t* bias,
                        float* Y, void* workspace, size_t workspace_bytes, void* stream) {
-    if (n <= 0 || n > 256 || N <= 0 || K <= 0 || K % 8 || N % 16 || !X || !W || !Y) return MG_ERR_ARG;
+    if (n <= 0 || n > 256 || N <= 0 || K <= 0 || K % 8 || N % 16 || !X || !W || !Y || canon < 0 || canon > 3) return MG_ERR_ARG;
     hipStream_t s = static_cast<hipStream_t>(stream);
     if (canon) {
         GemvArgs a{};
@@ -699,7 +699,10 @@ mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const 
         a.cap = n;
         a.n_cu = device_cu_count();
         if (bias) return MG_ERR_ARG;  // fp32 output carries no bias; the model path tests the bias
-        return launch_canon_gemv(a, EPI_F32, s) == hipSuccess ? MG_OK : MG_ERR_HIP;
+        const hipError_t e = canon == 2   ? launch_canon_gemv_valu(a, EPI_F32, s)
+                             : canon == 3 ? launch_canon_gemv_mfma(a, EPI_F32, s)
+                                          : launch_canon_gemv(a, EPI_F32, s);
+        return e == hipSuccess ? MG_OK : MG_ERR_HIP;
     }
     const size_t need = mg_op_linear_workspace_bytes(n, N, K);
     if (!workspace || workspace_bytes < need) return MG_ERR_WORKSPACE;

@@ -55,7 +55,11 @@ struct GemvArgs {
     const int32_t* n_dev;
     int n_cu;                  // compute units of the device (chooses the features per wave)
 };
+// two kernels with bit-identical results: fma on the vector ALUs, and the same fma steps on
+// the matrix cores (v_mfma_f32_16x16x1_4b_f32); launch_canon_gemv picks one by row count
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
+hipError_t launch_canon_gemv_valu(const GemvArgs& a, int epi, hipStream_t s);
+hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s);
 
 // ---------------------------------------------------------------- fast MFMA GEMM
 enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2, FEPI_SWIGLU = 3, FEPI_TOP2 = 4 };

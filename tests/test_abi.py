@@ -71,6 +71,8 @@ def test_null_arguments_are_rejected_before_any_work():
     assert lib.mg_op_linear(1, 0, 16, 8, None, None, None, None, None, 0, None) == -1
     assert lib.mg_op_linear(1, 4, 15, 8, 1, 1, None, 1, None, 0, None) == -1   # N % 16
     assert lib.mg_op_linear(1, 4, 16, 12, 1, 1, None, 1, None, 0, None) == -1  # K % 8
+    assert lib.mg_op_linear(4, 4, 16, 8, 1, 1, None, 1, None, 0, None) == -1   # no such kernel
+    assert lib.mg_op_linear(-1, 4, 16, 8, 1, 1, None, 1, None, 0, None) == -1
     assert lib.mg_op_probe_exp(-1, None, None, None) == -1
 
 

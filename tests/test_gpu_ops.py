@@ -49,20 +49,29 @@ def test_division_and_sqrt_are_ieee():
         np.testing.assert_array_equal(r.cpu().numpy().view(np.uint32), np.sqrt(a).view(np.uint32))
 
 
-# row counts cover every tile the launcher picks: one branch-free tile of 4, 8, 12, 16, 20
-# or 24 rows (9..16 rows of a wide output, N >= 16384, with 3 features per wave and a
+# row counts cover every tile the vector-fma kernel picks: one branch-free tile of 4, 8, 12,
+# 16, 20 or 24 rows (9..16 rows of a wide output, N >= 16384, with 3 features per wave and a
 # ragged last feature block; 5..16 rows of 4608 or 6144 features with 3 features per wave,
 # which balances the CUs), several 16-row tiles (a multiple of 16, and a ragged count with a
-# partial last tile); K covers several 512-element chunks and a partial last chunk
-@pytest.mark.parametrize("n,N,K", [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
-                                   (24, 16, 512), (5, 4096, 256), (10, 32, 1032), (12, 48, 4096), (19, 32, 688),
-                                   (21, 16, 1544), (25, 32, 1032), (32, 16, 2056), (47, 16, 520),
-                                   (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096), (7, 6144, 520),
-                                   (12, 4608, 1032), (16, 6144, 264)])
-def test_canonical_gemv_bitexact(n, N, K):
+# partial last tile); and every launch of the matrix-core kernel: one or two 16-row tiles per
+# block, one or two feature groups per block (two from 32768 features at one 32-row tile),
+# K a multiple of 256 or not (groups past K), several blocks of row tiles.  K covers several
+# 512-element chunks and a partial last chunk.  kernel: 1 = the verifier's choice for n rows,
+# 2 = the vector-fma kernel, 3 = the matrix-core kernel.
+GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
+              (24, 16, 512), (5, 4096, 256), (10, 32, 1032), (12, 48, 4096), (19, 32, 688),
+              (21, 16, 1544), (25, 32, 1032), (32, 16, 2056), (47, 16, 520),
+              (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096), (7, 6144, 520),
+              (12, 4608, 1032), (16, 6144, 264), (14, 32784, 264), (15, 32768, 512),
+              (40, 32784, 520), (29, 32768, 256), (64, 96, 4096), (100, 48, 264)]
+
+
+@pytest.mark.parametrize("kernel", [1, 2, 3])
+@pytest.mark.parametrize("n,N,K", GEMV_CASES)
+def test_canonical_gemv_bitexact(n, N, K, kernel):
     X = synth.random_bf16((n, K), seed=n * 7 + 1)
     W = synth.random_bf16((N, K), seed=N + K, std=0.05)
-    Y = mg.op_linear(True, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
+    Y = mg.op_linear(kernel, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
     for r in range(n):
         ref = mgo.linear(mgo.CANON, X[r], W, fp32=True)
         np.testing.assert_array_equal(Y[r].view(np.uint32), ref.view(np.uint32), err_msg=f"row {r}")
@@ -103,8 +112,9 @@ def test_fast_gemm_small_integers_exact(n, N, K):
     # integer products summed in float64: exact (every |sum| < 2^53)
     ref = mgo.f32_from_bf16(X).astype(np.float64) @ mgo.f32_from_bf16(W).astype(np.float64).T
     np.testing.assert_array_equal(Y, ref.astype(np.float32))
-    Yc = mg.op_linear(True, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
-    np.testing.assert_array_equal(Yc, ref.astype(np.float32))
+    for kernel in (1, 2, 3):
+        Yc = mg.op_linear(kernel, to_dev_bf16(X), to_dev_bf16(W)).cpu().numpy()
+        np.testing.assert_array_equal(Yc, ref.astype(np.float32))
 
 
 @pytest.mark.parametrize("d,eps", [(256, 1e-5), (4096, 1e-5), (3584, 1e-6), (5120, 1e-6), (688, 1e-5)])
