@@ -24,62 +24,74 @@ constexpr int ATT_MAXC = 256;   // positions per canonical chunk
 
 __device__ __forceinline__ float attn_scale(int hd) { return hd == 128 ? 0x1.6a09e6p-4f : 0x1.0p-3f; }
 
-// Canonical attention: one block of 256 threads per (item, KV head, chunk of 256
-// positions).  Every K and V load of the chunk is issued at once (coalesced: a wave reads
-// 4 whole rows per instruction), so the block waits for memory once.  K goes through LDS,
-// where the 16-byte pieces of row j sit in xor-swizzled slots (piece k at slot k ^ (j mod
-// U4)) so that thread j reads its own row without bank conflicts; V then takes the same
-// LDS space.  The sequential chains below read LDS in unrolled batches, so their loads are
-// in flight together.
-//   scores  thread j: s_j for each query head of the group, sequential fma over d, * scale
-//   chunk   wave w: heads w, w + 4: m = max_j s_j, e_j = EXP(s_j - m) in place
-//   values  thread t: d pair (2 dp, 2 dp + 1) of the heads hg, hg + 256 / (hd/2), ...:
-//           a[d] = sequential fma over j of e_j v_jd, and in the same loop
-//           l = sequential sum of e_j in position order
-template <int HD, int GP>  // GP: query heads per KV head, 1..8
-__global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
-    constexpr int U4 = HD / 8;                // 16-byte pieces per K/V row
-    constexpr int NLD = ATT_MAXC * U4 / 256;  // V pieces per thread
-    constexpr int HP = HD / 2;                // d pairs (words per V row)
-    constexpr int HPT = 256 / HP;             // head groups over the block's threads
-    constexpr int NPG = ATT_MAXC / 16;        // pages per chunk
-#ifndef MG_ATT_UB
-#define MG_ATT_UB 16
-#endif
-    constexpr int UB = MG_ATT_UB;             // positions per batch of LDS reads
-    static_assert(UB % 4 == 0 && ATT_MAXC % UB == 0, "whole float4 batches");
-    static_assert(NLD * 256 == ATT_MAXC * U4, "pieces must divide evenly");
+// Canonical attention: one block of NT threads (NT = 512 or 1024) per (item, KV head, chunk
+// of 256 positions).  Every K and V load of the chunk is issued at once (coalesced: a wave
+// reads whole rows), so the block waits for memory once, and the V loads stay in flight
+// while the scores run.  K goes through LDS, where the 16-byte pieces of row j sit in
+// xor-swizzled slots (piece k at slot k ^ (j mod U4)) so that the threads of one position
+// read its row without bank conflicts; V then takes the same LDS space.  Every chain below
+// is one thread's sequential loop, in the order of the definition:
+//   scores  thread (j, group hg): s_j of heads hg, hg + NT/256, ...: sequential fma over d,
+//           then * scale (K row and query read from LDS piece by piece)
+//   chunk   m = max_j s_j (wave max, then across the waves of a head group through LDS),
+//           e_j = EXP(s_j - m) by the thread that holds s_j
+//   values  thread (h, d): a[d] = sequential fma over j of e_j v_jd; l = sequential sum of
+//           e_j in position order by a thread of its own (or by the d = 0 thread when every
+//           thread has a value chain)
+template <int HD, int GP, int NT>  // GP: query heads per KV head, 1..8
+__global__ __launch_bounds__(NT) void attn_canon_kernel(AttnArgs a) {
+    constexpr int U4 = HD / 8;                  // 16-byte pieces per K/V row
+    constexpr int NLD = ATT_MAXC * U4 / NT;     // K (and V) pieces per thread
+    constexpr int HP = HD / 2;                  // d pairs (words per V row)
+    constexpr int NPG = ATT_MAXC / 16;          // pages per chunk
+    constexpr int HGN = NT / ATT_MAXC;          // head groups of the score phase
+    constexpr int HG = (GP + HGN - 1) / HGN;    // heads per score thread
+    constexpr int PPK = NT / (16 * U4);         // pages per load iteration
+    constexpr bool LS_SPARE = GP * HD + GP <= NT;  // l chains on threads of their own
+    constexpr int UB = 16;                      // positions per batch of LDS reads (values)
+    static_assert(NLD * NT == ATT_MAXC * U4, "pieces must divide evenly");
+    static_assert(GP * HD <= NT, "one value chain per thread");
+    static_assert(HGN >= 1 && PPK >= 1, "block shape");
 
     __shared__ __attribute__((aligned(16))) uint32_t vs[ATT_MAXC * HP];
-    __shared__ __attribute__((aligned(16))) float qs[8 * 256];  // the group's queries, then padding
+    __shared__ __attribute__((aligned(16))) float qs[GP * HD];
     __shared__ __attribute__((aligned(16))) float ps[GP * ATT_MAXC];
-    __shared__ float red[GP][1];
+    __shared__ float wmx[GP][4];
+    __shared__ float red[GP];
+    __shared__ __attribute__((aligned(16))) uint16_t kown[HD];
 
     const int i = blockIdx.z;
     if (i >= items_n(a.it)) return;
     const int kh = blockIdx.y, c = blockIdx.x;
-    const int r = items_row(a.it, i), p = items_pos(a.it, i);
+    const ModelDims& m = a.m;
     const int j0 = c * ATT_MAXC;
+    // position and page indices of the chunk (uniform, read through the scalar cache); entries
+    // past the current position's page are clamped to it (always mapped).  From the item table
+    // when there is one (one round trip), else from the item's row, position and page table.
+    int p, pgs[NPG];
+    if (a.itab) {
+        const int32_t* tb = a.itab + (size_t)i * (1 + m.max_pages_per_row);
+        p = tb[0];
+#pragma unroll
+        for (int k = 0; k < NPG; ++k) pgs[k] = tb[1 + min(j0 / 16 + k, m.max_pages_per_row - 1)];
+    } else {
+        const int r = items_row(a.it, i);
+        p = items_pos(a.it, i);
+        const int32_t* ptab = a.it.page_table + (size_t)r * m.max_pages_per_row;
+#pragma unroll
+        for (int k = 0; k < NPG; ++k) pgs[k] = ptab[min(j0 / 16 + k, p >> 4)];
+    }
     if (j0 > p) return;
     const int nj = min(ATT_MAXC, p + 1 - j0);
-    const ModelDims& m = a.m;
-    constexpr int G = GP;  // query heads per KV head (a template parameter, so the head loops have no branch)
+    constexpr int G = GP;
     const int Nk = m.Hkv * HD;
     const int t = threadIdx.x, wave = t >> 6, lane = t & 63;
     const size_t kv_stride = (size_t)m.Hkv * m.page_size * HD;  // K -> V of the same page
-
-    // page indices of the chunk (uniform, so read through the scalar cache together with the
-    // queries); entries past the current position's page are clamped to it (always mapped)
-    const int32_t* ptab = a.it.page_table + (size_t)r * m.max_pages_per_row;
-    int pgs[NPG];
-#pragma unroll
-    for (int k = 0; k < NPG; ++k) pgs[k] = ptab[min(j0 / 16 + k, p >> 4)];
-    // the group's rotated queries: one 16-byte load per thread (threads past the group's
-    // 8-element pieces re-read the last piece and stage it into an unused part of qs)
-    static_assert(GP * HD <= 8 * 256, "one 16-byte load per thread covers the group's queries");
+    // the group's queries: one 16-byte piece per thread for the first G * HD / 8 threads
     // (with qkv: the piece's RoPE partner piece and the cos/sin of its 8 pairs come too)
     const bool fold = a.qkv != nullptr;
     const uint16_t* qkv_row = fold ? a.qkv + (size_t)i * (m.Hq * HD + 2 * Nk) : nullptr;
+    const bool qthr = t < G * HD / 8;
     const int tq = min(t, G * HD / 8 - 1), e0 = (tq % U4) * 8;
     const bool qlow = e0 < HD / 2;  // the piece holds first-half elements of its head
     uint4 qv, qp;
@@ -99,30 +111,25 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     const uint16_t* own = (a.own_col && !fold) ? a.own_col + ((size_t)i * m.L + a.layer) * 2 * Nk + (size_t)kh * HD
                                                : nullptr;
     const bool own_here = fold && p < j0 + ATT_MAXC;
-    __shared__ __attribute__((aligned(16))) uint16_t kown[HD];
-    // K block of page pg for this KV head
     auto page_k = [&](int pg) -> const uint16_t* {
         return a.kv_pool + ((((size_t)a.layer * m.n_pages + pg) * 2) * m.Hkv + kh) * (size_t)m.page_size * HD;
     };
-    // K and V pieces: iteration k covers positions PPI*k .. PPI*k + PPI-1 (PPI/16 pages), thread t
-    // piece t mod U4 of position t / U4 of those.  Every load is unconditional, so the waits
-    // below count requests exactly and the queries can be staged while K and V are in flight:
+    // K and V pieces: iteration k covers positions (NT / U4) k .. + NT / U4 - 1 (PPK pages),
+    // thread t piece t mod U4 of position t / U4 of those.  Every load is unconditional:
     // positions past the chunk's last live one (nj - 1) re-read that position (a cache hit;
     // those values are never used).  The verifier's own column stands in for the cache's
     // tentative column p (the fold path's rotated own K row is taken from kown below).
-    // (pieces as a native vector type: a struct copy held across the scores stays in memory)
     using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
-    constexpr int PPI = 256 / U4, PGI = PPI / 16;
     const int sub = (t / U4) >> 4;
     u32x4 kq[NLD], vr[NLD];
     const uint16_t* vps[NLD];
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
-        const int e = t + 256 * k;
+        const int e = t + NT * k;
         const int jj = min(e / U4, nj - 1), pc = e % U4;
-        int pg = pgs[PGI * k];
+        int pg = pgs[PPK * k];
 #pragma unroll
-        for (int q2 = 1; q2 < PGI; ++q2) pg = sub == q2 ? pgs[PGI * k + q2] : pg;
+        for (int q2 = 1; q2 < PPK; ++q2) pg = sub == q2 ? pgs[PPK * k + q2] : pg;
         const uint16_t* kc = page_k(pg) + (size_t)(jj & 15) * HD + pc * 8;
         const bool at_p = j0 + jj == p;
         kq[k] = *reinterpret_cast<const u32x4*>((own && at_p) ? own + pc * 8 : kc);
@@ -132,88 +139,86 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
     }
 #pragma unroll
     for (int k = 0; k < NLD; ++k) vr[k] = *reinterpret_cast<const u32x4*>(vps[k]);
-    if (!fold) {
+    if (qthr) {
         float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
-        qd[0] = make_float4(bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y));
-        qd[1] = make_float4(bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w));
-    } else {
-        // rotate-half RoPE of the piece, as the RoPE kernel computes it: pair (x_i, x_(i+hd/2))
-        // -> (bf16(x_i c - x_(i+hd/2) s), bf16(x_(i+hd/2) c + x_i s)), products rounded apart
-        const float pv[8] = {bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y),
-                             bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w)};
-        const float pp[8] = {bf_lo(qp.x), bf_hi(qp.x), bf_lo(qp.y), bf_hi(qp.y),
-                             bf_lo(qp.z), bf_hi(qp.z), bf_lo(qp.w), bf_hi(qp.w)};
-        const float cc[16] = {cq[0].x, cq[0].y, cq[0].z, cq[0].w, cq[1].x, cq[1].y, cq[1].z, cq[1].w,
-                              cq[2].x, cq[2].y, cq[2].z, cq[2].w, cq[3].x, cq[3].y, cq[3].z, cq[3].w};
-        float qf[8];
+        if (!fold) {
+            qd[0] = make_float4(bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y));
+            qd[1] = make_float4(bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w));
+        } else {
+            // rotate-half RoPE of the piece, as the RoPE kernel computes it: pair (x_i, x_(i+hd/2))
+            // -> (bf16(x_i c - x_(i+hd/2) s), bf16(x_(i+hd/2) c + x_i s)), products rounded apart
+            const float pv[8] = {bf_lo(qv.x), bf_hi(qv.x), bf_lo(qv.y), bf_hi(qv.y),
+                                 bf_lo(qv.z), bf_hi(qv.z), bf_lo(qv.w), bf_hi(qv.w)};
+            const float pp[8] = {bf_lo(qp.x), bf_hi(qp.x), bf_lo(qp.y), bf_hi(qp.y),
+                                 bf_lo(qp.z), bf_hi(qp.z), bf_lo(qp.w), bf_hi(qp.w)};
+            const float cc[16] = {cq[0].x, cq[0].y, cq[0].z, cq[0].w, cq[1].x, cq[1].y, cq[1].z, cq[1].w,
+                                  cq[2].x, cq[2].y, cq[2].z, cq[2].w, cq[3].x, cq[3].y, cq[3].z, cq[3].w};
+            float qf[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const float lo = qlow ? pv[e] : pp[e], hi = qlow ? pp[e] : pv[e];
-            const float c = cc[2 * e], sn = cc[2 * e + 1];
-            const float ac = lo * c, bs = hi * sn, bc = hi * c, as = lo * sn;
-            qf[e] = bf2f(f2bf(qlow ? ac - bs : bc + as));
+            for (int e = 0; e < 8; ++e) {
+                const float lo = qlow ? pv[e] : pp[e], hi = qlow ? pp[e] : pv[e];
+                const float cs_ = cc[2 * e], sn = cc[2 * e + 1];
+                const float ac = lo * cs_, bs = hi * sn, bc = hi * cs_, as = lo * sn;
+                qf[e] = bf2f(f2bf(qlow ? ac - bs : bc + as));
+            }
+            qd[0] = make_float4(qf[0], qf[1], qf[2], qf[3]);
+            qd[1] = make_float4(qf[4], qf[5], qf[6], qf[7]);
         }
-        float4* qd = reinterpret_cast<float4*>(qs + 8 * t);
-        qd[0] = make_float4(qf[0], qf[1], qf[2], qf[3]);
-        qd[1] = make_float4(qf[4], qf[5], qf[6], qf[7]);
-        if (own_here && wave == 0) {
-            const uint16_t* ks = qkv_row + m.Hq * HD + (size_t)kh * HD;
-            const uint16_t* vsrc = ks + Nk;
-            uint16_t* ow = a.own_col ? const_cast<uint16_t*>(a.own_col) + ((size_t)i * m.L + a.layer) * 2 * Nk +
-                                           (size_t)kh * HD
-                                     : nullptr;
-            for (int ii = lane; ii < HD / 2; ii += 64) {
-                const float lo = bf2f(ks[ii]), hi = bf2f(ks[ii + HD / 2]);
-                const float c = a.cs[(size_t)p * HD + 2 * ii], sn = a.cs[(size_t)p * HD + 2 * ii + 1];
-                const float ac = lo * c, bs = hi * sn, bc = hi * c, as = lo * sn;
-                const uint16_t o1 = (uint16_t)f2bf(ac - bs), o2 = (uint16_t)f2bf(bc + as);
-                kown[ii] = o1;
-                kown[ii + HD / 2] = o2;
-                if (ow) {
-                    ow[ii] = o1;
-                    ow[ii + HD / 2] = o2;
-                    ow[Nk + ii] = vsrc[ii];
-                    ow[Nk + ii + HD / 2] = vsrc[ii + HD / 2];
-                }
+    }
+    if (own_here && wave == 0) {
+        const uint16_t* ks = qkv_row + m.Hq * HD + (size_t)kh * HD;
+        const uint16_t* vsrc = ks + Nk;
+        uint16_t* ow = a.own_col ? const_cast<uint16_t*>(a.own_col) + ((size_t)i * m.L + a.layer) * 2 * Nk +
+                                       (size_t)kh * HD
+                                 : nullptr;
+        for (int ii = lane; ii < HD / 2; ii += 64) {
+            const float lo = bf2f(ks[ii]), hi = bf2f(ks[ii + HD / 2]);
+            const float cs_ = a.cs[(size_t)p * HD + 2 * ii], sn = a.cs[(size_t)p * HD + 2 * ii + 1];
+            const float ac = lo * cs_, bs = hi * sn, bc = hi * cs_, as = lo * sn;
+            const uint16_t o1 = (uint16_t)f2bf(ac - bs), o2 = (uint16_t)f2bf(bc + as);
+            kown[ii] = o1;
+            kown[ii + HD / 2] = o2;
+            if (ow) {
+                ow[ii] = o1;
+                ow[ii + HD / 2] = o2;
+                ow[Nk + ii] = vsrc[ii];
+                ow[Nk + ii + HD / 2] = vsrc[ii + HD / 2];
             }
         }
     }
     // K into LDS, swizzled (the V requests stay in flight: loads complete in order)
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
-        const int e = t + 256 * k;
+        const int e = t + NT * k;
         const int jj = e / U4, pc = e % U4;
         *reinterpret_cast<u32x4*>(vs + (jj * U4 + (pc ^ (jj % U4))) * 4) = kq[k];
     }
     // the queries and K rows staged by other threads are needed from here on
     __syncthreads();
-    // thread t's K row (the fold path's thread of position p takes the rotated own K row)
-    uint4 kr[U4];
-#pragma unroll
-    for (int k = 0; k < U4; ++k) kr[k] = *reinterpret_cast<const uint4*>(vs + (t * U4 + (k ^ (t % U4))) * 4);
-    if (own_here && t == nj - 1) {
-#pragma unroll
-        for (int k = 0; k < U4; ++k) kr[k] = reinterpret_cast<const uint4*>(kown)[k];
-    }
 
-    // ---- scores: position t, all heads of the group at once (K in registers), computed
-    // while the V requests are still in flight
-
+    // ---- scores: position j, heads hg + HGN u (the fold path's thread of position p takes
+    // the rotated own K row from kown), computed while the V requests are still in flight
     const float scale = attn_scale(HD);
-    if (t < nj) {
-        float sc[GP];
+    const int j = t % ATT_MAXC, hg = t / ATT_MAXC;
+    float sc[HG];
 #pragma unroll
-        for (int h = 0; h < GP; ++h) sc[h] = 0.0f;
+    for (int u = 0; u < HG; ++u) sc[u] = 0.0f;
+    const bool live = j < nj;
+    if (live) {
+        const bool from_own = own_here && j == nj - 1;
 #pragma unroll
         for (int k = 0; k < U4; ++k) {
-            const float kf[8] = {bf_lo(kr[k].x), bf_hi(kr[k].x), bf_lo(kr[k].y), bf_hi(kr[k].y),
-                                 bf_lo(kr[k].z), bf_hi(kr[k].z), bf_lo(kr[k].w), bf_hi(kr[k].w)};
+            const uint4 kp = from_own ? reinterpret_cast<const uint4*>(kown)[k]
+                                      : *reinterpret_cast<const uint4*>(vs + (j * U4 + (k ^ (j % U4))) * 4);
+            const float kf[8] = {bf_lo(kp.x), bf_hi(kp.x), bf_lo(kp.y), bf_hi(kp.y),
+                                 bf_lo(kp.z), bf_hi(kp.z), bf_lo(kp.w), bf_hi(kp.w)};
 #pragma unroll
-            for (int h = 0; h < GP; ++h) {
-                {
+            for (int u = 0; u < HG; ++u) {
+                const int h = hg + HGN * u;
+                if (h < G) {
                     const float4 q0 = *reinterpret_cast<const float4*>(qs + h * HD + 8 * k);
                     const float4 q1 = *reinterpret_cast<const float4*>(qs + h * HD + 8 * k + 4);
-                    float s = sc[h];
+                    float s = sc[u];
                     s = __builtin_fmaf(q0.x, kf[0], s);
                     s = __builtin_fmaf(q0.y, kf[1], s);
                     s = __builtin_fmaf(q0.z, kf[2], s);
@@ -222,93 +227,94 @@ __global__ __launch_bounds__(256) void attn_canon_kernel(AttnArgs a) {
                     s = __builtin_fmaf(q1.y, kf[5], s);
                     s = __builtin_fmaf(q1.z, kf[6], s);
                     s = __builtin_fmaf(q1.w, kf[7], s);
-                    sc[h] = s;
+                    sc[u] = s;
                 }
             }
         }
 #pragma unroll
-        for (int h = 0; h < GP; ++h) ps[h * ATT_MAXC + t] = sc[h] * scale;
+        for (int u = 0; u < HG; ++u) sc[u] = sc[u] * scale;
     }
-    // every K read is done before V takes the LDS space
+    // chunk max: each wave's max of its positions, per head (waves of a head group cover
+    // 64 positions each)
+#pragma unroll
+    for (int u = 0; u < HG; ++u) {
+        const int h = hg + HGN * u;
+        const float mx = wave_max(live ? sc[u] : -__builtin_inff());
+        if (h < G && lane == 0) wmx[h][(j >> 6)] = mx;
+    }
+    // every K read is done and every wave max is in before V takes the LDS space
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < NLD; ++k) {
-        const int e = t + 256 * k;
+        const int e = t + NT * k;
         *reinterpret_cast<u32x4*>(vs + (e / U4) * HP + (e % U4) * 4) = vr[k];
     }
-
-    // ---- chunk max and exponentials (scores only: no barrier needed after the V stores)
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {
-        const int h = wave + 4 * hh;
+    for (int u = 0; u < HG; ++u) {
+        const int h = hg + HGN * u;
         if (h < G) {
-            float mx = -__builtin_inff();
-            for (int j = lane; j < nj; j += 64) mx = fmaxf(mx, ps[h * ATT_MAXC + j]);
-            mx = wave_max(mx);
-            for (int j = lane; j < nj; j += 64) ps[h * ATT_MAXC + j] = canon_exp(ps[h * ATT_MAXC + j] - mx);
-            if (lane == 0) red[h][0] = mx;
+            const float mx = fmaxf(fmaxf(wmx[h][0], wmx[h][1]), fmaxf(wmx[h][2], wmx[h][3]));
+            if (live) ps[h * ATT_MAXC + j] = canon_exp(sc[u] - mx);
+            if (j == 0) red[h] = mx;
         }
     }
     __syncthreads();
 
-    // ---- the weighted values, with l (the sequential sum of e_j in position order) carried
-    // along in the same loop: every thread of head h forms the same l, the d-pair-0 thread
-    // stores it
-    const int nb = nj / UB * UB;  // positions handled in whole batches
-    const int dp = t % HP, hg = t / HP;
-    constexpr int NH = (GP + HPT - 1) / HPT;  // heads per thread
-    float acc[NH][2], lsum[NH];
+    // ---- the weighted values: thread (h, d); l on a thread of its own (or the d = 0 thread)
+    const int vh = t / HD, vd = t % HD;
+    const bool vthr = t < G * HD;
+    const int lh = t - G * HD;  // the head whose l this spare thread forms
+    const bool lthr = LS_SPARE ? (lh >= 0 && lh < G) : (vthr && vd == 0);
+    const int eh = vthr ? vh : (LS_SPARE && lthr ? lh : 0);
+    float acc = 0.0f, lsum = 0.0f;
+    if (vthr || lthr) {
+        const int nb = nj / UB * UB;  // positions handled in whole batches
+        const float* eh_row = ps + eh * ATT_MAXC;
+        const int vw_i = vd >> 1;
+        // this thread's bf16 of a V word moved to the top half with zeros below (one v_perm)
+        const uint32_t vsel = (vd & 1) ? 0x03020c0cu : 0x01000c0cu;
+        for (int jb = 0; jb < nb; jb += UB) {
+            float e[UB];
 #pragma unroll
-    for (int u = 0; u < NH; ++u) acc[u][0] = acc[u][1] = lsum[u] = 0.0f;
-    for (int j = 0; j < nb; j += UB) {
-        uint32_t vw[UB];
+            for (int q4 = 0; q4 < UB / 4; ++q4) {
+                const float4 t4 = *reinterpret_cast<const float4*>(eh_row + jb + 4 * q4);
+                e[4 * q4] = t4.x; e[4 * q4 + 1] = t4.y; e[4 * q4 + 2] = t4.z; e[4 * q4 + 3] = t4.w;
+            }
+            if (vthr) {
+                uint32_t vw[UB];
 #pragma unroll
-        for (int b = 0; b < UB; ++b) vw[b] = vs[(j + b) * HP + dp];
+                for (int b = 0; b < UB; ++b) vw[b] = vs[(jb + b) * HP + vw_i];
 #pragma unroll
-        for (int u = 0; u < NH; ++u) {
-            const int h = hg + HPT * u;
-            if (h < G) {
-                float e[UB];
+                for (int b = 0; b < UB; ++b)
+                    acc = __builtin_fmaf(e[b], __uint_as_float(__builtin_amdgcn_perm(vw[b], vw[b], vsel)), acc);
+            }
+            if (lthr) {
 #pragma unroll
-                for (int q4 = 0; q4 < UB / 4; ++q4) {
-                    const float4 t4 = *reinterpret_cast<const float4*>(ps + h * ATT_MAXC + j + 4 * q4);
-                    e[4 * q4] = t4.x; e[4 * q4 + 1] = t4.y; e[4 * q4 + 2] = t4.z; e[4 * q4 + 3] = t4.w;
-                }
-#pragma unroll
-                for (int b = 0; b < UB; ++b) {
-                    lsum[u] = lsum[u] + e[b];
-                    acc[u][0] = __builtin_fmaf(e[b], bf_lo(vw[b]), acc[u][0]);
-                    acc[u][1] = __builtin_fmaf(e[b], bf_hi(vw[b]), acc[u][1]);
-                }
+                for (int b = 0; b < UB; ++b) lsum = lsum + e[b];
             }
         }
-    }
-    for (int j = nb; j < nj; ++j) {
-        const uint32_t vw = vs[j * HP + dp];
-#pragma unroll
-        for (int u = 0; u < NH; ++u) {
-            const int h = hg + HPT * u;
-            if (h < G) {
-                const float e = ps[h * ATT_MAXC + j];
-                lsum[u] = lsum[u] + e;
-                acc[u][0] = __builtin_fmaf(e, bf_lo(vw), acc[u][0]);
-                acc[u][1] = __builtin_fmaf(e, bf_hi(vw), acc[u][1]);
+        for (int jj = nb; jj < nj; ++jj) {
+            const float e = eh_row[jj];
+            if (vthr) {
+                const uint32_t vw = vs[jj * HP + vw_i];
+                acc = __builtin_fmaf(e, __uint_as_float(__builtin_amdgcn_perm(vw, vw, vsel)), acc);
             }
+            if (lthr) lsum = lsum + e;
         }
     }
     constexpr int stride = HD + 2;
-#pragma unroll
-    for (int u = 0; u < NH; ++u) {
-        const int h = hg + HPT * u;
-        if (h < G) {
-            float* dst = a.part + (((size_t)i * m.Hq + kh * G + h) * a.max_chunks + c) * stride;
-            if (dp == 0) {
-                dst[0] = red[h][0];
-                dst[1] = lsum[u];
-            }
-            dst[2 + 2 * dp] = acc[u][0];
-            dst[3 + 2 * dp] = acc[u][1];
+    if (vthr) {
+        float* dst = a.part + (((size_t)i * m.Hq + kh * G + vh) * a.max_chunks + c) * stride;
+        dst[2 + vd] = acc;
+        if (!LS_SPARE && lthr) {
+            dst[0] = red[vh];
+            dst[1] = lsum;
         }
+    }
+    if (LS_SPARE && lthr) {
+        float* dst = a.part + (((size_t)i * m.Hq + kh * G + lh) * a.max_chunks + c) * stride;
+        dst[0] = red[lh];
+        dst[1] = lsum;
     }
 }
 
@@ -318,7 +324,7 @@ __global__ void attn_combine_kernel(AttnArgs a) {
     const int h = blockIdx.x, d = threadIdx.x;
     const int hd = a.m.hd;
     if (d >= hd) return;
-    const int p = items_pos(a.it, i);
+    const int p = a.itab ? a.itab[(size_t)i * (1 + a.m.max_pages_per_row)] : items_pos(a.it, i);
     const int S = (p + 1 + a.chunk - 1) / a.chunk;
     const int stride = hd + 2;
     const float* base = a.part + ((size_t)i * a.m.Hq + h) * a.max_chunks * stride;
@@ -358,18 +364,42 @@ __global__ void attn_combine_kernel(AttnArgs a) {
     a.out[(size_t)i * a.m.Hq * hd + (size_t)h * hd + d] = (uint16_t)f2bf(ieee_div(O, L));
 }
 
+// 1024 threads per block (measured at the Llama-8B shape, 13 rows: 25k vs 31k cycles per
+// block with 512)
+template <int HD, int G>
+static void launch_canon_gt(const AttnArgs& a, dim3 g1, hipStream_t s) {
+    constexpr int NT = 1024;
+    hipLaunchKernelGGL((attn_canon_kernel<HD, G, NT>), g1, dim3(NT), 0, s, a);
+}
 template <int HD>
 static void launch_canon_g(const AttnArgs& a, int G, dim3 g1, hipStream_t s) {
     switch (G) {
-        case 1: hipLaunchKernelGGL((attn_canon_kernel<HD, 1>), g1, dim3(256), 0, s, a); break;
-        case 2: hipLaunchKernelGGL((attn_canon_kernel<HD, 2>), g1, dim3(256), 0, s, a); break;
-        case 3: hipLaunchKernelGGL((attn_canon_kernel<HD, 3>), g1, dim3(256), 0, s, a); break;
-        case 4: hipLaunchKernelGGL((attn_canon_kernel<HD, 4>), g1, dim3(256), 0, s, a); break;
-        case 5: hipLaunchKernelGGL((attn_canon_kernel<HD, 5>), g1, dim3(256), 0, s, a); break;
-        case 6: hipLaunchKernelGGL((attn_canon_kernel<HD, 6>), g1, dim3(256), 0, s, a); break;
-        case 7: hipLaunchKernelGGL((attn_canon_kernel<HD, 7>), g1, dim3(256), 0, s, a); break;
-        default: hipLaunchKernelGGL((attn_canon_kernel<HD, 8>), g1, dim3(256), 0, s, a); break;
+        case 1: launch_canon_gt<HD, 1>(a, g1, s); break;
+        case 2: launch_canon_gt<HD, 2>(a, g1, s); break;
+        case 3: launch_canon_gt<HD, 3>(a, g1, s); break;
+        case 4: launch_canon_gt<HD, 4>(a, g1, s); break;
+        case 5: launch_canon_gt<HD, 5>(a, g1, s); break;
+        case 6: launch_canon_gt<HD, 6>(a, g1, s); break;
+        case 7: launch_canon_gt<HD, 7>(a, g1, s); break;
+        default: launch_canon_gt<HD, 8>(a, g1, s); break;
     }
+}
+
+// item i: tab[i][0] = its position p, tab[i][1 + k] = its row's page of slot min(k, p / 16)
+__global__ __launch_bounds__(256) void item_table_kernel(Items it, int mpr, int32_t* __restrict__ tab) {
+    const int i = blockIdx.x;
+    if (i >= items_n(it)) return;
+    const int r = items_row(it, i), p = items_pos(it, i);
+    const int32_t* ptab = it.page_table + (size_t)r * mpr;
+    int32_t* tb = tab + (size_t)i * (1 + mpr);
+    if (threadIdx.x == 0) tb[0] = p;
+    for (int k = threadIdx.x; k < mpr; k += 256) tb[1 + k] = ptab[min(k, p >> 4)];
+}
+
+hipError_t launch_item_table(const Items& it, const ModelDims& m, int32_t* itab, hipStream_t s) {
+    if (it.n_host <= 0) return hipSuccess;
+    hipLaunchKernelGGL(item_table_kernel, dim3(it.n_host), dim3(256), 0, s, it, m.max_pages_per_row, itab);
+    return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s) {

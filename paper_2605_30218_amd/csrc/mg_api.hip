@@ -26,7 +26,7 @@ constexpr size_t ALIGN = 256;
 size_t up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 struct Plan {
-    size_t rope, x, h, qkv, qrot, att, act, attn_part, gemm_part, top2_ws, vlog, vrows, total;
+    size_t rope, x, h, qkv, qrot, att, act, attn_part, itab, gemm_part, top2_ws, vlog, vrows, total;
     int rows_cap, max_pos, chunks_canon;
 };
 
@@ -76,6 +76,7 @@ Plan make_plan(const mg_model_cfg* c, int n_cu) {
     p.act = o; o += up(R * (size_t)F * 2);
     const size_t ap_canon = R * Hq * (size_t)p.chunks_canon * (hd + 2);
     p.attn_part = o; o += up(ap_canon * sizeof(float));
+    p.itab = o; o += up(R * (1 + (size_t)c->max_pages_per_row) * sizeof(int32_t));
     ProjShape ps[5];
     fast_projs(c, ps);
     // split-K partial tiles of the QKV, O, gate/up and down projections: S * M * N
@@ -249,6 +250,8 @@ mg_status canon_forward(mg_ctx* c, const Items& it, uint16_t* own_col, float* lo
     uint16_t* qrot = c->at<uint16_t>(c->plan.qrot);
     uint16_t* att = c->at<uint16_t>(c->plan.att);
     uint16_t* act = c->at<uint16_t>(c->plan.act);
+    int32_t* itab = c->at<int32_t>(c->plan.itab);
+    HIPCHK(launch_item_table(it, m, itab, s));
     HIPCHK(launch_embed(it, c->W(0), d, x, s));
     for (int l = 0; l < g.n_layers; ++l) {
         HIPCHK(launch_rmsnorm(x, c->LW(l, 0), n, nd, cap, d, g.rms_eps, h, s));
@@ -276,6 +279,7 @@ mg_status canon_forward(mg_ctx* c, const Items& it, uint16_t* own_col, float* lo
             a.chunk = CANON_CHUNK;
             a.max_chunks = c->plan.chunks_canon;
             a.out = att;
+            a.itab = itab;
             ProfScope ps(c, MG_KIND_CANON_ATTN, s, 0.0);
             HIPCHK(launch_attention(a, 1, s));
         }

@@ -127,8 +127,13 @@ struct AttnArgs {
     int chunk;                 // positions per chunk (canonical: 256)
     int max_chunks;
     uint16_t* out;             // [n][Hq*hd]
+    // item table (or NULL): per item, its position then the page of every page slot of its row
+    // clamped to the position's page, [n][1 + max_pages_per_row]; written once per forward by
+    // launch_item_table, so a block finds its position and pages in one memory round trip
+    const int32_t* itab;
 };
 hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s);  // canonical (canon = 1) only
+hipError_t launch_item_table(const Items& it, const ModelDims& m, int32_t* itab, hipStream_t s);
 
 // fast path: QKV split sum + bias + RoPE + tentative K/V append + attention, one block
 // per (row, KV head); rows 0..B-1 of the step batch

@@ -24,14 +24,17 @@ import os
 import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-# kernel name prefix -> source file (bench names: fast_gemm, canon_gemv)
-SOURCES = {"fast_gemm": "k_gemm.hip", "canon_gemv": "k_gemv.hip"}
+# kernel name prefix -> source files (bench names: fast_gemm, canon_gemv; the canonical GEMV
+# has a vector-fma kernel and a matrix-core kernel, canon_gemv_kernel and canon_gemv_mfma_kernel)
+SOURCES = {"fast_gemm": ("k_gemm.hip",), "canon_gemv": ("k_gemv.hip", "k_gemv_mfma.hip")}
 DECODE_START = "resid_norm_kernel"
 
 
 def source_sha(kernel: str) -> str:
-    path = os.path.join(HERE, "csrc", SOURCES[kernel])
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in SOURCES[kernel]:
+        h.update(open(os.path.join(HERE, "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def _decode_window(rows, key):
@@ -47,7 +50,7 @@ def _short(name: str) -> str:
     return n.replace("void ", "").replace("mg::", "")
 
 
-MODE_KERNELS = ("fast_gemm_kernel", "canon_gemv_kernel", "attn_fast_fused_kernel", "attn_canon_kernel")
+MODE_KERNELS = ("fast_gemm_kernel", "canon_gemv", "attn_fast_fused_kernel", "attn_canon_kernel")
 
 
 def _mode_tables(rows, modes):
@@ -96,9 +99,9 @@ def trace(trace_csv: str, out: str, command: str, modes: str = "") -> None:
             lines.append(f"{k[:44]:44s} {','.join(g):>22s} {len(v):7d} {sum(v) / len(v) / 1e3:9.1f}")
     lines.append("")
     for kn in SOURCES:
-        fg = [d for k, v in by.items() if k.startswith(kn + "_kernel") for d in v]
+        fg = [d for k, v in by.items() if k.startswith(kn) for d in v]
         if fg:
-            lines.append(f"{kn}_kernel, all shapes: {len(fg)} launches, average {sum(fg) / len(fg) / 1e3:.1f} us")
+            lines.append(f"{kn} kernels, all shapes: {len(fg)} launches, average {sum(fg) / len(fg) / 1e3:.1f} us")
     if modes:
         lines += _mode_tables(rows, modes.split(","))
     open(out, "w").write("\n".join(lines) + "\n")
@@ -120,9 +123,9 @@ def traffic(kernel, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_b
     cw = [v for vs in _per_dispatch(copy_write_csv, "copy16", False).values() for v in vs]
     f_scale = copy_bytes / (sum(cf[1:]) / len(cf[1:]) if len(cf) > 1 else cf[0])
     w_scale = copy_bytes / (sum(cw[1:]) / len(cw[1:]) if len(cw) > 1 else cw[0])
-    fe = _per_dispatch(fetch_csv, kernel + "_kernel")
-    wr = _per_dispatch(write_csv, kernel + "_kernel")
-    lines = [f"kernel: {kernel}_kernel (decode window)", f"command (FETCH_SIZE, then WRITE_SIZE): {command}",
+    fe = _per_dispatch(fetch_csv, kernel)
+    wr = _per_dispatch(write_csv, kernel)
+    lines = [f"kernel: {kernel} kernels (decode window)", f"command (FETCH_SIZE, then WRITE_SIZE): {command}",
              f"copy calibration: {copy_command}",
              f"copy kernel reads and writes {copy_bytes / 2**20:.0f} MiB: FETCH_SIZE scale {f_scale:.4f}, "
              f"WRITE_SIZE scale {w_scale:.4f}",
