@@ -485,4 +485,26 @@ hipError_t launch_probe_divsqrt(int64_t n, const float* a, const float* b, float
     return hipGetLastError();
 }
 
+typedef float probe_v16f __attribute__((ext_vector_type(16)));
+
+// The instruction the matrix-core canonical GEMV (k_gemv_mfma.hip) relies on, bare: per instance t (one wave),
+// D = v_mfma_f32_16x16x1_4b_f32(a[t][lane], b[t][lane], C) with C and D [t][register][lane]
+__global__ __launch_bounds__(64) void probe_mfma_fma_kernel(const float* __restrict__ a, const float* __restrict__ b,
+                                                            const float* __restrict__ c, float* __restrict__ d) {
+    const size_t t = blockIdx.x;
+    const int lane = threadIdx.x;
+    probe_v16f acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = c[(t * 16 + r) * 64 + lane];
+    acc = __builtin_amdgcn_mfma_f32_16x16x1f32(a[t * 64 + lane], b[t * 64 + lane], acc, 0, 0, 0);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) d[(t * 16 + r) * 64 + lane] = acc[r];
+}
+
+hipError_t launch_probe_mfma_fma(int n_inst, const float* a, const float* b, const float* c, float* d, hipStream_t s) {
+    if (n_inst <= 0) return hipSuccess;
+    hipLaunchKernelGGL(probe_mfma_fma_kernel, dim3(n_inst), dim3(64), 0, s, a, b, c, d);
+    return hipGetLastError();
+}
+
 }  // namespace mg

@@ -65,6 +65,7 @@ SIGNATURES = {
     "mg_op_probe_bf16": (I, [I64, P, P, P]),
     "mg_op_probe_exp": (I, [I64, P, P, P]),
     "mg_op_probe_divsqrt": (I, [I64, P, P, P, P, P]),
+    "mg_op_probe_mfma_fma": (I, [I, P, P, P, P, P]),
     "mg_op_linear_workspace_bytes": (SZ, [I, I, I]),
     "mg_op_linear": (I, [I, I, I, I, P, P, P, P, P, SZ, P]),
     "mg_op_fast_gemm_config": (I, [I, I, I, I, P, P]),
@@ -273,6 +274,13 @@ def op_probe_divsqrt(a, b):
     _check("mg_op_probe_divsqrt", load().mg_op_probe_divsqrt(a.numel(), a.data_ptr(), b.data_ptr(), q.data_ptr(),
                                                              r.data_ptr(), _stream()))
     return q, r
+
+
+def op_probe_mfma_fma(a, b, c):
+    d = torch.empty_like(c)
+    _check("mg_op_probe_mfma_fma", load().mg_op_probe_mfma_fma(a.shape[0], a.data_ptr(), b.data_ptr(), c.data_ptr(),
+                                                               d.data_ptr(), _stream()))
+    return d
 
 
 def op_linear(canon, X, W):

@@ -74,6 +74,8 @@ def test_null_arguments_are_rejected_before_any_work():
     assert lib.mg_op_linear(4, 4, 16, 8, 1, 1, None, 1, None, 0, None) == -1   # no such kernel
     assert lib.mg_op_linear(-1, 4, 16, 8, 1, 1, None, 1, None, 0, None) == -1
     assert lib.mg_op_probe_exp(-1, None, None, None) == -1
+    assert lib.mg_op_probe_mfma_fma(-1, None, None, None, None, None) == -1
+    assert lib.mg_op_probe_mfma_fma(2, None, None, None, None, None) == -1
 
 
 def test_create_rejects_small_buffers_and_missing_weights():

@@ -141,3 +141,44 @@ def test_bandwidth_references_touch_every_word(n_words):
     folded = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
     expect = np.bitwise_xor.reduce(src_np.view(np.uint32)) if n_words else np.uint32(0)
     assert folded == expect
+
+
+def test_fp32_mfma_k1_is_a_fused_multiply_add():
+    """v_mfma_f32_16x16x1_4b_f32, on which the matrix-core canonical GEMV runs CDOT's fma
+    chains: every output element equals fmaf(a, b, c) of its operands (one rounding), for
+    random values over a wide exponent range, subnormals, signed zeros, infinities and
+    cancellation against the product, in the lane and register layout mg_ops.h states."""
+    import ctypes
+    import ctypes.util
+    rng = np.random.default_rng(16)
+    n = 48
+
+    def mixed(shape):
+        x = (rng.standard_normal(shape) * np.exp2(rng.integers(-40, 40, shape))).astype(np.float32)
+        u, m = x.view(np.uint32), rng.random(shape)
+        u[m < 0.04] = rng.integers(1, 0x800000, int((m < 0.04).sum()), dtype=np.uint32)
+        u[(m >= 0.04) & (m < 0.06)] = 0x80000000
+        u[(m >= 0.06) & (m < 0.08)] = 0
+        x[(m >= 0.08) & (m < 0.09)] = np.inf
+        x[(m >= 0.09) & (m < 0.10)] = -np.inf
+        return x
+
+    a, b, c = mixed((n, 64)), mixed((n, 64)), mixed((n, 16, 64))
+    r = np.arange(16)[:, None]
+    l = np.arange(64)[None, :]
+    ia, ib = 16 * (r // 4) + 4 * (l // 16) + r % 4, 16 * (r // 4) + l % 16
+    ae, be = a[:, ia], b[:, ib]
+    # a third of the accumulators cancel the product to within a few ulps
+    sel = rng.random((n, 16, 64)) < 0.3
+    prod = (ae.astype(np.float64) * be.astype(np.float64)).astype(np.float32)
+    with np.errstate(all="ignore"):
+        c[sel] = -prod[sel] * np.float32(1 + 2 ** -20)
+    d = mg.op_probe_mfma_fma(*(torch.from_numpy(np.ascontiguousarray(x)).to(DEV) for x in (a, b, c))).cpu().numpy()
+    libm = ctypes.CDLL(ctypes.util.find_library("m"))
+    libm.fmaf.restype = ctypes.c_float
+    libm.fmaf.argtypes = [ctypes.c_float] * 3
+    ref = np.array([libm.fmaf(float(x), float(y), float(z)) for x, y, z in zip(ae.ravel(), be.ravel(), c.ravel())],
+                   np.float32).reshape(d.shape)
+    both_nan = np.isnan(d) & np.isnan(ref)
+    assert np.array_equal(np.isnan(d), np.isnan(ref))
+    assert np.array_equal(d.view(np.uint32)[~both_nan], ref.view(np.uint32)[~both_nan])

@@ -28,7 +28,8 @@ def test_traffic_summary_round_trip(tmp_path):
 def test_trace_mode_windows_are_named_from_the_last_decode_windows():
     """The kernel-trace summary splits the decode window at the long KV-restore copies; the
     modes are the last windows that run decode kernels (a restore after the last mode that
-    runs none, like the CPU baseline's, is skipped)."""
+    runs none, like the CPU baseline's, is skipped).  The canonical GEMV's two kernels count
+    as one kind."""
     from paper_2605_30218_amd import profsum
     t = [0]
 
@@ -42,15 +43,16 @@ def test_trace_mode_windows_are_named_from_the_last_decode_windows():
     rows = [row("resid_norm_kernel"), row("fast_gemm_kernel")]            # tau calibration
     rows += [restore(), row("canon_gemv_kernel"), row("fast_gemm_kernel")]  # recipe run 1
     rows += [restore(), row("fast_gemm_kernel")]                           # off
-    rows += [restore(), row("fast_gemm_kernel"), row("canon_gemv_kernel", 30_000)]  # gated
+    rows += [restore(), row("fast_gemm_kernel"), row("canon_gemv_kernel", 30_000),
+             row("canon_gemv_mfma_kernel", 50_000)]                       # gated
     rows += [restore(), row("fast_gemm_kernel"), row("canon_gemv_kernel", 70_000)]  # always
     rows += [restore(), row("copy_to_host")]                               # no decode kernels
     lines = profsum._mode_tables(rows, ["off", "gated", "always"])
     got = {(ln[:16].strip(), ln[17:39].strip()): float(ln.split()[-2]) for ln in lines[3:]}
-    assert got[("gated", "canon_gemv_kernel")] == 30.0
-    assert got[("always", "canon_gemv_kernel")] == 70.0
-    assert ("off", "canon_gemv_kernel") not in got
-    assert ("recipe run 1", "canon_gemv_kernel") in got
+    assert got[("gated", "canon_gemv")] == 40.0
+    assert got[("always", "canon_gemv")] == 70.0
+    assert ("off", "canon_gemv") not in got
+    assert ("recipe run 1", "canon_gemv") in got
 
 
 def test_forward_bytes_of_the_llama8b_shape():
