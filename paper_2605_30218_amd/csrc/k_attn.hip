@@ -206,7 +206,9 @@ __global__ __launch_bounds__(NT) void attn_canon_kernel(AttnArgs a) {
     const bool live = j < nj;
     if (live) {
         const bool from_own = own_here && j == nj - 1;
-#pragma unroll
+        // (unrolled by 4 pieces: fully unrolled, the compiler hoists every K and query read of
+        // two heads and spills)
+#pragma unroll 4
         for (int k = 0; k < U4; ++k) {
             const uint4 kp = from_own ? reinterpret_cast<const uint4*>(kown)[k]
                                       : *reinterpret_cast<const uint4*>(vs + (j * U4 + (k ^ (j % U4))) * 4);
