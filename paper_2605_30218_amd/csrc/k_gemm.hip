@@ -403,10 +403,17 @@ __global__ __launch_bounds__(64 * NW) void fast_gemm_kernel(FastGemmArgs a) {
         __syncthreads();
         Top2* states = reinterpret_cast<Top2*>(a.part);
         for (int row = threadIdx.x; row < 16 * MT && row < M; row += 64 * NW) {
-            Top2 st = wst[0][row];
+            // (states moved as 16-byte words: field-wise struct copies through memory would
+            // otherwise be staged in scratch)
+            auto ld = [&](int w) {
+                const uint4 u = *reinterpret_cast<const uint4*>(&wst[w][row]);
+                return Top2{__uint_as_float(u.x), __uint_as_float(u.y), (int)u.z, (int)u.w};
+            };
+            Top2 st = ld(0);
 #pragma unroll
-            for (int w = 1; w < NW; ++w) st = top2_merge(st, wst[w][row]);
-            states[(size_t)row * gridDim.x + nb] = st;
+            for (int w = 1; w < NW; ++w) st = top2_merge(st, ld(w));
+            reinterpret_cast<uint4*>(states)[(size_t)row * gridDim.x + nb] =
+                make_uint4(__float_as_uint(st.v1), __float_as_uint(st.v2), (uint32_t)st.i1, (uint32_t)st.nan);
         }
         return;
     } else {
@@ -430,7 +437,10 @@ __global__ __launch_bounds__(256) void top1_rows_kernel(const Top2* __restrict__
                                                         int32_t* __restrict__ top1) {
     const int r = blockIdx.x, t = threadIdx.x;
     Top2 st{-__builtin_inff(), -__builtin_inff(), -1, 0};
-    for (int k = t; k < nblk; k += 256) st = top2_merge(st, states[(size_t)r * nblk + k]);
+    for (int k = t; k < nblk; k += 256) {
+        const uint4 u = reinterpret_cast<const uint4*>(states)[(size_t)r * nblk + k];  // one 16-byte load
+        st = top2_merge(st, Top2{__uint_as_float(u.x), __uint_as_float(u.y), (int)u.z, (int)u.w});
+    }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) st = top2_merge(st, top2_shfl(st, o));
     __shared__ Top2 ws[4];
