@@ -366,24 +366,31 @@ __global__ void attn_combine_kernel(AttnArgs a) {
     a.out[(size_t)i * a.m.Hq * hd + (size_t)h * hd + d] = (uint16_t)f2bf(ieee_div(O, L));
 }
 
-// 1024 threads per block (measured at the Llama-8B shape, 13 rows: 25k vs 31k cycles per
-// block with 512)
+// 1024 threads per block where the grid gives each CU about one block (a block's latency is
+// the kernel's: measured at the Llama-8B shape, 13 rows: 25k vs 31k cycles per block with 512);
+// 512 where each CU has several blocks to run and G * HD <= 512, so two blocks share a CU and
+// one block's loads overlap the other's chains
 template <int HD, int G>
-static void launch_canon_gt(const AttnArgs& a, dim3 g1, hipStream_t s) {
-    constexpr int NT = 1024;
-    hipLaunchKernelGGL((attn_canon_kernel<HD, G, NT>), g1, dim3(NT), 0, s, a);
+static void launch_canon_gt(const AttnArgs& a, dim3 g1, bool many, hipStream_t s) {
+    if constexpr (G * HD <= 512) {
+        if (many) {
+            hipLaunchKernelGGL((attn_canon_kernel<HD, G, 512>), g1, dim3(512), 0, s, a);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((attn_canon_kernel<HD, G, 1024>), g1, dim3(1024), 0, s, a);
 }
 template <int HD>
-static void launch_canon_g(const AttnArgs& a, int G, dim3 g1, hipStream_t s) {
+static void launch_canon_g(const AttnArgs& a, int G, dim3 g1, bool many, hipStream_t s) {
     switch (G) {
-        case 1: launch_canon_gt<HD, 1>(a, g1, s); break;
-        case 2: launch_canon_gt<HD, 2>(a, g1, s); break;
-        case 3: launch_canon_gt<HD, 3>(a, g1, s); break;
-        case 4: launch_canon_gt<HD, 4>(a, g1, s); break;
-        case 5: launch_canon_gt<HD, 5>(a, g1, s); break;
-        case 6: launch_canon_gt<HD, 6>(a, g1, s); break;
-        case 7: launch_canon_gt<HD, 7>(a, g1, s); break;
-        default: launch_canon_gt<HD, 8>(a, g1, s); break;
+        case 1: launch_canon_gt<HD, 1>(a, g1, many, s); break;
+        case 2: launch_canon_gt<HD, 2>(a, g1, many, s); break;
+        case 3: launch_canon_gt<HD, 3>(a, g1, many, s); break;
+        case 4: launch_canon_gt<HD, 4>(a, g1, many, s); break;
+        case 5: launch_canon_gt<HD, 5>(a, g1, many, s); break;
+        case 6: launch_canon_gt<HD, 6>(a, g1, many, s); break;
+        case 7: launch_canon_gt<HD, 7>(a, g1, many, s); break;
+        default: launch_canon_gt<HD, 8>(a, g1, many, s); break;
     }
 }
 
@@ -411,10 +418,13 @@ hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s) {
     dim3 g1(a.max_chunks, a.m.Hkv, n), g2(a.m.Hq, n);
     const int G = a.m.Hq / a.m.Hkv;
     if (G < 1 || G > ATT_MAXG) return hipErrorInvalidValue;
+    // blocks of the launch (an upper bound: chunks past a row's position exit at once)
+    const long blocks = (long)n * a.m.Hkv * a.max_chunks;
+    const bool many = blocks >= 4L * (a.n_cu > 0 ? a.n_cu : 256);
     if (a.m.hd == 128)
-        launch_canon_g<128>(a, G, g1, s);
+        launch_canon_g<128>(a, G, g1, many, s);
     else
-        launch_canon_g<64>(a, G, g1, s);
+        launch_canon_g<64>(a, G, g1, many, s);
     hipLaunchKernelGGL(attn_combine_kernel, g2, dim3(a.m.hd), 0, s, a);
     return hipGetLastError();
 }

@@ -280,6 +280,7 @@ mg_status canon_forward(mg_ctx* c, const Items& it, uint16_t* own_col, float* lo
             a.max_chunks = c->plan.chunks_canon;
             a.out = att;
             a.itab = itab;
+            a.n_cu = c->n_cu;
             ProfScope ps(c, MG_KIND_CANON_ATTN, s, 0.0);
             HIPCHK(launch_attention(a, 1, s));
         }

@@ -131,6 +131,7 @@ struct AttnArgs {
     // clamped to the position's page, [n][1 + max_pages_per_row]; written once per forward by
     // launch_item_table, so a block finds its position and pages in one memory round trip
     const int32_t* itab;
+    int n_cu;                  // compute units of the device (chooses the block size)
 };
 hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s);  // canonical (canon = 1) only
 hipError_t launch_item_table(const Items& it, const ModelDims& m, int32_t* itab, hipStream_t s);
