@@ -371,15 +371,25 @@ hipError_t launch_canon_gemv_valu(const GemvArgs& a, int epi, hipStream_t s) {
 }
 
 // Which of the two bit-identical kernels runs: the matrix-core one (k_gemv_mfma.hip) where it
-// was measured faster -- a host count of 12..16 rows (one 16-row tile with few dead rows) or
-// more than 24 (32-row tiles), and device counts that may exceed 24 -- the fma kernel above
-// otherwise (its exact 4..24-row tiles waste fewer lanes on small and mid counts).  Measured
-// per projection shape at 1, 8, 12, 16, 20, 32 and 64 rows (Llama-8B shapes): e.g. gate/up at
-// 16 rows 47.6 vs 63.2 us, LM head at 64 rows 825 vs 1167 us; at 8 rows 46.8 vs 40.9 and 241.5
-// vs 182.9.
+// was measured faster, the fma kernel above otherwise (its exact 4..24-row tiles waste fewer
+// lanes on small and mid counts; the matrix-core time is flat within a 16-row tile).  The
+// matrix-core kernel takes host counts of 13..16 rows, 9..12 rows on outputs of fewer than
+// MG_GEMV_VOCAB_N features (all but a vocabulary-sized LM head), more than 24 rows (32-row
+// tiles), and device counts that may exceed 24.  Measured in the decode loop (kernel trace of
+// gated Llama-8B steps, us, fma / matrix-core): at 9..12 rows O and down 14.5 and 34.0 /
+// 22.6 on average (the matrix-core launch has one block per CU there and a deep ring),
+// gate/up 63.8 / 53.9, LM head 222 / 239; at 13..16 rows the matrix-core kernel is faster on
+// every shape; at 8 rows the fma kernel is (with the caches flushed before each launch: O
+// 13.8 / 15.0, gate/up 46.2 / 53.7, LM head 182 / 236 us).
+#ifndef MG_GEMV_VOCAB_N
+#define MG_GEMV_VOCAB_N 65536
+#endif
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
-    const bool mfma = a.n_dev ? rows > MG_GEMV_EXACT_MAX : (rows >= 12 && rows <= 16) || rows > MG_GEMV_EXACT_MAX;
+    const int Nf = epi == EPI_SWIGLU ? 2 * a.N : a.N;  // weight rows streamed
+    const bool mid = rows >= 13 && rows <= 16;
+    const bool low_narrow = rows >= 9 && rows <= 12 && Nf < MG_GEMV_VOCAB_N;
+    const bool mfma = a.n_dev ? rows > MG_GEMV_EXACT_MAX : mid || low_narrow || rows > MG_GEMV_EXACT_MAX;
     return mfma ? launch_canon_gemv_mfma(a, epi, s) : launch_canon_gemv_valu(a, epi, s);
 }
 

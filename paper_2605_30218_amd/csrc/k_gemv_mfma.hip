@@ -313,14 +313,23 @@ static hipError_t launch_mfma_cfg(const GemvArgs& a, int epi, int rows, hipStrea
 }
 
 template <bool RG>
-static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool wide, hipStream_t s) {
-    if (rows > 16) return wide ? launch_mfma_cfg<2, 8, 2, 2, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 3, RG>(a, epi, rows, s);
-    return wide ? launch_mfma_cfg<2, 4, 1, 3, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 1, 2, RG>(a, epi, rows, s);
+static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool wide, bool deep, hipStream_t s) {
+    if (rows > 16) {
+        if (wide) return launch_mfma_cfg<2, 8, 2, 2, RG>(a, epi, rows, s);
+        return deep ? launch_mfma_cfg<1, 8, 2, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 3, RG>(a, epi, rows, s);
+    }
+    if (wide) return launch_mfma_cfg<2, 4, 1, 3, RG>(a, epi, rows, s);
+    return deep ? launch_mfma_cfg<1, 8, 1, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 1, 2, RG>(a, epi, rows, s);
 }
 
 // Launch rule: one 16-row tile per block up to 16 rows, two above (their MFMAs share the
 // weight operand); two feature groups per block where that leaves every CU at least four
 // blocks, else one group served by 8 waves, so the narrow outputs still fill the chip.
+// Ring depth: a launch with at most one block per CU (the 4096-feature outputs) has nothing
+// else on the CU to cover a stage's memory latency, so it keeps three stages in flight
+// (depth 4: in the decode loop the O and down projections at 12-16 rows took 21.9 against
+// 29.3 us with depth 2); launches with several blocks per CU keep the shallow ring, which
+// leaves room for more blocks (gate/up at 12-16 rows: 52.9 us at depth 2, 57.9 at 4).
 hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
@@ -328,7 +337,8 @@ hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s) {
     const int n_cu = a.n_cu > 0 ? a.n_cu : 256;
     const int n_rt = rows > 16 ? (rows + 31) / 32 : 1;
     const bool wide = (long)(n_fg / 2) * n_rt >= 4L * n_cu;
-    return a.K % 256 ? launch_mfma_rg<true>(a, epi, rows, wide, s) : launch_mfma_rg<false>(a, epi, rows, wide, s);
+    const bool deep = (long)n_fg * n_rt <= n_cu;
+    return a.K % 256 ? launch_mfma_rg<true>(a, epi, rows, wide, deep, s) : launch_mfma_rg<false>(a, epi, rows, wide, deep, s);
 }
 
 }  // namespace mg

@@ -55,14 +55,16 @@ def test_division_and_sqrt_are_ieee():
 # which balances the CUs), several 16-row tiles (a multiple of 16, and a ragged count with a
 # partial last tile); and every launch of the matrix-core kernel: one or two 16-row tiles per
 # block, one or two feature groups per block (two from 32768 features at one 32-row tile),
-# K a multiple of 256 or not (groups past K), several blocks of row tiles.  K covers several
+# K a multiple of 256 or not (groups past K), several blocks of row tiles, the deep ring (at
+# most one block per CU: up to 256 feature groups) and the shallow one (6144 and 4608
+# features, with one and two 16-row tiles).  K covers several
 # 512-element chunks and a partial last chunk.  kernel: 1 = the verifier's choice for n rows,
 # 2 = the vector-fma kernel, 3 = the matrix-core kernel.
 GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
               (24, 16, 512), (5, 4096, 256), (10, 32, 1032), (12, 48, 4096), (19, 32, 688),
               (21, 16, 1544), (25, 32, 1032), (32, 16, 2056), (47, 16, 520),
               (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096), (7, 6144, 520),
-              (12, 4608, 1032), (16, 6144, 264), (14, 32784, 264), (15, 32768, 512),
+              (12, 4608, 1032), (16, 6144, 264), (20, 6144, 520), (14, 32784, 264), (15, 32768, 512),
               (40, 32784, 520), (29, 32768, 256), (64, 96, 4096), (100, 48, 264)]
 
 
