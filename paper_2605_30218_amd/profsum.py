@@ -4,6 +4,7 @@
     python -m paper_2605_30218_amd.profsum traffic <kernel> <fetch_csv> <write_csv> <copy_fetch_csv> \
         <copy_write_csv> <copy_bytes> <out.txt> "<command>" "<copy command>"
     python -m paper_2605_30218_amd.profsum util <counter_collection.csv> <out.txt> "<command>" <k1,k2,..>
+    python -m paper_2605_30218_amd.profsum shapes <csv1,csv2,..> <out.txt> "<command>" <k1,k2,..>
 
 Both summaries cover the decode window only: the dispatches from the first fast-path
 residual/RMSNorm kernel on (the canonical prompt prefill before it uses other kernels).
@@ -163,6 +164,52 @@ def util(pmc_csv: str, out: str, command: str, kernels: str) -> None:
     open(out, "w").write("\n".join(lines) + "\n")
 
 
+def shapes(pmc_csvs: str, out: str, command: str, kernels: str) -> None:
+    """Per launch shape (kernel instance and grid) of the named kernels: dispatches, mean
+    duration and the mean of each SQ counter per dispatch (counter passes in separate CSVs),
+    with the ratios that name a stall: the share of wave time waiting to issue (WAIT_INST_ANY),
+    issuing VALU, LDS and vector memory instructions (ACTIVE_INST_*), LDS bank-conflict cycles
+    per LDS instruction, and the matrix-core busy share of the launch's SIMD-cycles (256 CUs x
+    4 SIMDs at 2.4 GHz)."""
+    names = kernels.split(",")
+    cnt = collections.defaultdict(lambda: collections.defaultdict(list))
+    dur = collections.defaultdict(list)
+    for path in pmc_csvs.split(","):
+        rows = _decode_window(list(csv.DictReader(open(path))), "Dispatch_Id")
+        seen = set()
+        for r in rows:
+            kn = r["Kernel_Name"]
+            if not any(k in kn for k in names):
+                continue
+            key = (kn.replace("void ", "").replace("mg::", "").split("(")[0], int(r["Grid_Size"]))
+            cnt[key][r["Counter_Name"]].append(float(r["Counter_Value"]))
+            did = (path, r["Dispatch_Id"])
+            if did not in seen:
+                seen.add(did)
+                dur[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1000.0)
+
+    def mean(key, c):
+        v = cnt[key].get(c)
+        return sum(v) / len(v) if v else float("nan")
+
+    lines = [f"command: {command}", "window: decode steps; per launch shape, mean over its dispatches",
+             "ratios: wait, valu, lds, vmem = share of wave-cycles (SQ_WAVE_CYCLES) waiting to issue / issuing "
+             "VALU / LDS / vector-memory instructions; conf = SQ_LDS_BANK_CONFLICT per SQ_INSTS_LDS; "
+             "mfma = SQ_VALU_MFMA_BUSY_CYCLES over the launch's SIMD-cycles", "",
+             f"{'kernel':58s} {'grid':>9s} {'n':>5s} {'us':>7s} {'wait':>6s} {'valu':>6s} {'lds':>6s} "
+             f"{'vmem':>6s} {'conf':>6s} {'mfma':>6s}"]
+    for key in sorted(cnt, key=lambda k: -sum(dur[k])):
+        wc = mean(key, "SQ_WAVE_CYCLES")
+        us = sum(dur[key]) / max(len(dur[key]), 1)
+        ratio = lambda c: mean(key, c) / wc if wc == wc and wc > 0 else float("nan")
+        conf = mean(key, "SQ_LDS_BANK_CONFLICT") / mean(key, "SQ_INSTS_LDS") if mean(key, "SQ_INSTS_LDS") else float("nan")
+        mfma = mean(key, "SQ_VALU_MFMA_BUSY_CYCLES") / (us * 1e-6 * 2.4e9 * 1024) if us > 0 else float("nan")
+        lines.append(f"{key[0][:58]:58s} {key[1]:9d} {len(dur[key]) // max(len(pmc_csvs.split(',')), 1):5d} {us:7.1f} "
+                     f"{ratio('SQ_WAIT_INST_ANY'):6.2f} {ratio('SQ_ACTIVE_INST_VALU'):6.2f} "
+                     f"{ratio('SQ_ACTIVE_INST_LDS'):6.2f} {ratio('SQ_ACTIVE_INST_VMEM'):6.2f} {conf:6.2f} {mfma:6.2f}")
+    open(out, "w").write("\n".join(lines) + "\n")
+
+
 def read_traffic(path: str):
     """(bytes per launch, source sha) from a traffic summary, or None."""
     if not os.path.exists(path):
@@ -183,5 +230,7 @@ if __name__ == "__main__":
         traffic(*sys.argv[2:11])
     elif sys.argv[1] == "util":
         util(*sys.argv[2:6])
+    elif sys.argv[1] == "shapes":
+        shapes(*sys.argv[2:6])
     else:
         raise SystemExit(__doc__)
