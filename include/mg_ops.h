@@ -45,6 +45,13 @@ mg_status mg_op_probe_divsqrt(int64_t n, const float* a, const float* b, float* 
  * k's B; register r of lane l holds block r / 4, row 4 (l / 16) + r % 4, column l % 16.
  * The test compares d with fmaf of the matching operands. */
 mg_status mg_op_probe_mfma_fma(int n_inst, const float* a, const float* b, const float* c, float* d, void* stream);
+/* One v_mfma_f32_4x4x1_16b_f32 per instance t < n_inst (one wave each), the instruction the
+ * matrix-core GEMV runs the fma chains of rows past the first 16-row tile on: a, b fp32
+ * [n_inst][64] (the lane's A and B operand), c, d fp32 [n_inst][4][64] (accumulator register
+ * r of lane l in and out).  Lane l = 4 k + i supplies row i of block k's A and column i of
+ * block k's B; register r of lane l holds block l / 4, row r, column l % 4.  The test
+ * compares d with fmaf of the matching operands. */
+mg_status mg_op_probe_mfma4_fma(int n_inst, const float* a, const float* b, const float* c, float* d, void* stream);
 
 /* Y[r][j] = sum_k X[r][k] * W[j][k] in fp32 (no bias, no rounding to bf16), for
  * r < n <= 256, N % 16 == 0, K % 8 == 0.  canon = 1: the verifier's canonical

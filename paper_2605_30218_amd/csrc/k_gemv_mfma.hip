@@ -43,6 +43,7 @@
 namespace mg {
 
 typedef float mg_v16f __attribute__((ext_vector_type(16)));
+typedef float mg_v4f __attribute__((ext_vector_type(4)));
 typedef uint32_t mg_u32x4 __attribute__((ext_vector_type(4)));
 
 // one 8-element group of bf16 -0 (weights) and of +0 (activations) for groups past K
@@ -77,16 +78,35 @@ __device__ __forceinline__ void gv_lds_wait(mg_u32x4 (&av)[NQ], mg_u32x4 (&bv)[T
         asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(av[0]), "+v"(bv[0][0]), "+v"(bv[1][0]) : : "memory");
     }
 }
+// the same for one 16-row tile plus XQ 4-row quads (one quad of the stage per wave)
+template <int XQ>
+__device__ __forceinline__ void gv_lds_wait_x(mg_u32x4& av, mg_u32x4& bv, mg_u32x4 (&bx)[XQ]) {
+    if constexpr (XQ == 1) {
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(av), "+v"(bv), "+v"(bx[0]) : : "memory");
+    } else {
+        static_assert(XQ == 2, "4-row quads past the first tile");
+        asm volatile("s_waitcnt lgkmcnt(0)" : "+v"(av), "+v"(bv), "+v"(bx[0]), "+v"(bx[1]) : : "memory");
+    }
+}
 
-template <int FG, int NWB, int T, int EPI, int D, bool RAGGED>
+// XQ > 0 (with T = 2 and one quad per wave): rows 16 .. 16 + 4 XQ - 1 of the block's 32-row
+// tile run on v_mfma_f32_4x4x1_16b_f32 instead of a second 16x16x1 tile.  Its 16 blocks of
+// 4 x 4 are the 4 chains x 4 feature quads: lane 16 c + 4 q + i supplies feature 4 q + i of
+// chain c (the very A operand of the 16x16x1 instruction) and row 4 rq + i of the quad's B,
+// and register r of lane 16 c + 4 q + j holds (chain c, feature 4 q + r, row 4 rq + j); an
+// fma step of 16 x 4 rows costs a quarter of a 16 x 16 one.
+template <int FG, int NWB, int T, int XQ, int EPI, int D, bool RAGGED>
 __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4)) void canon_gemv_mfma_kernel(GemvArgs a, int n_fg, int n_rt) {
     constexpr int NW = FG * NWB;
     constexpr int NQ = 8 / NWB;                 // quads of a wave per stage
     constexpr int SROWS = 16 * FG + 16 * T;     // rows of a stage: weights, then activations
     constexpr int NLD = SROWS / 2;              // direct-to-LDS loads per stage
     constexpr int IPW = NLD / NW;               // loads per wave per stage
+    constexpr int TM = XQ ? 1 : T;              // 16-row tiles on the 16x16x1 instruction
+    constexpr int XA = XQ ? XQ : 1;             // (array extent)
     static_assert(NWB == 4 || NWB == 8, "waves per feature group");
     static_assert(2 * NQ * T <= 4, "accumulators");
+    static_assert(XQ == 0 || (T == 2 && NQ == 1 && XQ <= 2 && XQ <= NWB), "4-row quads: second tile, one quad per wave");
     static_assert(NLD % NW == 0, "every wave issues the same loads (exact waits)");
     const int b = blockIdx.x;
     const int xcd = b & 7, slot = b >> 3;
@@ -143,26 +163,38 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
         }
     };
 
-    mg_v16f acc[T][2 * NQ];  // [row tile][2 qi + p] (qi: the wave's quad of a stage, p: stage parity)
+    mg_v16f acc[TM][2 * NQ];  // [row tile][2 qi + p] (qi: the wave's quad of a stage, p: stage parity)
 #pragma unroll
-    for (int t = 0; t < T; ++t)
+    for (int t = 0; t < TM; ++t)
 #pragma unroll
         for (int k = 0; k < 2 * NQ; ++k)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[t][k][r] = 0.0f;
+    mg_v4f accx[XA][2];  // 4-row quads: [quad][stage parity]
+#pragma unroll
+    for (int q = 0; q < XA; ++q)
+#pragma unroll
+        for (int k = 0; k < 2; ++k)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) accx[q][k][r] = 0.0f;
 
     // operand slots of quad qi (group of the stage: NWB = 4: 16 qi + 4 wb + bk; NWB = 8: 4 wb + bk)
-    int aslot[NQ], bslot[T][NQ];
+    int aslot[NQ], bslot[TM][NQ], bxslot[XA];
 #pragma unroll
     for (int qi = 0; qi < NQ; ++qi) {
         const int lg = (NWB == 4 ? 16 * qi : 0) + 4 * wb + bk;
         aslot[qi] = 32 * (16 * fgw + ii) + (lg ^ ii);
 #pragma unroll
-        for (int t = 0; t < T; ++t) bslot[t][qi] = 32 * (16 * FG + 16 * t + ii) + (lg ^ ii);
+        for (int t = 0; t < TM; ++t) bslot[t][qi] = 32 * (16 * FG + 16 * t + ii) + (lg ^ ii);
+    }
+#pragma unroll
+    for (int q = 0; q < XA; ++q) {  // row 4 q + (lane mod 4) of the second tile, the lane's chain
+        const int lg = 4 * wb + bk, rr = 4 * q + (lane & 3);
+        bxslot[q] = 32 * (16 * FG + 16 + rr) + (lg ^ rr);
     }
     // operand reads of stage s (raw bf16 groups), waited for one stage later
     struct Ops {
-        mg_u32x4 a[NQ], b[T][NQ];
+        mg_u32x4 a[NQ], b[TM][NQ], bx[XA];
     };
     auto read_ops = [&](int s, Ops& o) {
         const uint4* buf = ring[s % D];
@@ -170,7 +202,11 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
         for (int qi = 0; qi < NQ; ++qi) {
             gv_lds_read(o.a[qi], buf + aslot[qi]);
 #pragma unroll
-            for (int t = 0; t < T; ++t) gv_lds_read(o.b[t][qi], buf + bslot[t][qi]);
+            for (int t = 0; t < TM; ++t) gv_lds_read(o.b[t][qi], buf + bslot[t][qi]);
+        }
+        if constexpr (XQ > 0) {
+#pragma unroll
+            for (int q = 0; q < XQ; ++q) gv_lds_read(o.bx[q], buf + bxslot[q]);
         }
     };
     // the MFMAs of one stage into the accumulators of parity P (a compile-time index, so the
@@ -181,18 +217,28 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
         // conversion waits on an MFMA still reading the register it would overwrite
 #pragma unroll
         for (int qi = 0; qi < NQ; ++qi) {
-            float fa[8], fx[T][8];
+            float fa[8], fx[TM][8], fq[XA][8];
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
                 fa[e] = bfe(o.a[qi], e);
 #pragma unroll
-                for (int t = 0; t < T; ++t) fx[t][e] = bfe(o.b[t][qi], e);
+                for (int t = 0; t < TM; ++t) fx[t][e] = bfe(o.b[t][qi], e);
+                if constexpr (XQ > 0) {
+#pragma unroll
+                    for (int q = 0; q < XQ; ++q) fq[q][e] = bfe(o.bx[q], e);
+                }
             }
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
+            for (int e = 0; e < 8; ++e) {
 #pragma unroll
-                for (int t = 0; t < T; ++t)
+                for (int t = 0; t < TM; ++t)
                     acc[t][2 * qi + p] = __builtin_amdgcn_mfma_f32_16x16x1f32(fa[e], fx[t][e], acc[t][2 * qi + p], 0, 0, 0);
+                if constexpr (XQ > 0) {
+#pragma unroll
+                    for (int q = 0; q < XQ; ++q)
+                        accx[q][p] = __builtin_amdgcn_mfma_f32_4x4x1f32(fa[e], fq[q][e], accx[q][p], 0, 0, 0);
+                }
+            }
         }
     };
     // One stage: its operands (read one stage earlier) are waited for; then, if a stage
@@ -202,7 +248,8 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
     // s finished, the loads of stage s + D go to the buffer of s, and the operands of s + 1 are
     // requested; then the MFMAs of stage s run from registers.
     auto step = [&](int s, Ops& cur, Ops& nxt, auto P) {
-        gv_lds_wait<NQ, T>(cur.a, cur.b);
+        if constexpr (XQ > 0) gv_lds_wait_x<XQ>(cur.a[0], cur.b[0][0], cur.bx);
+        else gv_lds_wait<NQ, T>(cur.a, cur.b);
         if (s + 1 < nst) {
             if (s + D - 1 < nst) gv_wait_vmcnt<IPW * (D - 2)>();
             else gv_wait_vmcnt<0>();
@@ -235,9 +282,9 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
     float* red = reinterpret_cast<float*>(&ring[0][0]);  // [NW][16][64]
     static_assert(NW * 16 * 64 * 4 <= D * SROWS * 32 * 16, "the reduction fits in the ring");
     const int col = wb & 3;  // register column i % 4 that waves wb < 4 finish
-    float vt[T];
+    float vt[TM];
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
+    for (int t = 0; t < TM; ++t) {
         mg_v16f tot;
         if constexpr (NQ == 2) {
             tot = (acc[t][0] + acc[t][1]) + (acc[t][2] + acc[t][3]);
@@ -262,26 +309,48 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
         }
         vt[t] = (s4[0] + s4[2]) + (s4[1] + s4[3]);  // block bits: offsets 2 then 1
     }
+    // the 4-row quads: the same pairings, the wave bits through LDS (wave wb < XQ finishes quad
+    // wb), then the chain's low bits, which sit in lane bits 5 and 4 here: offsets 2 then 1
+    float vq[4];
+    if constexpr (XQ > 0) {
+        gv_barrier();  // every wave is past its reads of the last tile
+#pragma unroll
+        for (int q = 0; q < XQ; ++q) {
+            const mg_v4f totq = accx[q][0] + accx[q][1];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) red[(wave * 16 + 4 * q + r) * 64 + lane] = totq[r];
+        }
+        __syncthreads();
+        const int q = wb < XQ ? wb : 0;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            float v[NWB];
+#pragma unroll
+            for (int w = 0; w < NWB; ++w) v[w] = red[((fgw * NWB + w) * 16 + 4 * q + r) * 64 + lane];
+#pragma unroll
+            for (int h = NWB / 2; h >= 1; h >>= 1)
+#pragma unroll
+                for (int w = 0; w < h; ++w) v[w] = v[w] + v[w + h];
+            float x = v[0];
+            x = x + __shfl_xor(x, 32, MG_WAVE);
+            x = x + __shfl_xor(x, 16, MG_WAVE);
+            vq[r] = x;
+        }
+    }
     if (wb >= 4) return;
 
-    // epilogue: lane 16 (i / 4) + j holds feature i = 4 (lane / 16) + col, row j = lane % 16
+    // epilogue: output (feature i of the group, row) = v; upv: the matching up row's sum
     const int fgl = fb * FG + fgw;
-    const int i = 4 * (lane >> 4) + col;
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
-        const float v = vt[t];
-        const int row = r0 + 16 * t + (lane & 15);
+    auto emit = [&](float v, float upv, int i, int row, bool live) {
         if constexpr (EPI == EPI_SWIGLU) {
-            // gate outputs sit in lanes 0..31 (i < 8), their up rows 32 lanes higher
-            const float upv = __shfl_xor(v, 32, MG_WAVE);
             const int pj = fgl * 8 + i;
-            if (lane >= 32 || row >= n || pj >= a.N) continue;
+            if (!live || i >= 8 || row >= n || pj >= a.N) return;
             const float g = bf2f(f2bf(v)), up = bf2f(f2bf(upv));
             const float sg = ieee_div(g, 1.0f + canon_exp(-g));
             reinterpret_cast<uint16_t*>(a.Y)[(size_t)row * a.N + pj] = (uint16_t)f2bf(sg * up);
         } else {
             const int j = fgl * 16 + i;
-            if (row >= n || j >= a.N) continue;
+            if (!live || row >= n || j >= a.N) return;
             if (EPI == EPI_F32) {
                 reinterpret_cast<float*>(a.Y)[(size_t)row * a.N + j] = v;
             } else if (EPI == EPI_BF16) {
@@ -294,36 +363,58 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
                 *xp = (uint16_t)f2bf(bf2f(*xp) + bf2f(f2bf(v)));
             }
         }
+    };
+    // 16-row tiles: lane 16 (i / 4) + j holds feature i = 4 (lane / 16) + col, row j = lane % 16
+    // (a SwiGLU group's gate features i < 8 sit in lanes 0..31, their up rows 32 lanes higher)
+#pragma unroll
+    for (int t = 0; t < TM; ++t) {
+        const float upv = EPI == EPI_SWIGLU ? __shfl_xor(vt[t], 32, MG_WAVE) : 0.0f;
+        emit(vt[t], upv, 4 * (lane >> 4) + col, r0 + 16 * t + (lane & 15), true);
+    }
+    // 4-row quad wb: lanes 4 q + j (chain 0) hold feature 4 q + r in register r, row 16 + 4 wb + j
+    // (gate features in lanes 0..7, their up rows 8 lanes higher)
+    if constexpr (XQ > 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const float upv = EPI == EPI_SWIGLU ? __shfl_xor(vq[r], 8, MG_WAVE) : 0.0f;
+            emit(vq[r], upv, 4 * ((lane >> 2) & 3) + r, r0 + 16 + 4 * wb + (lane & 3), wb < XQ && lane < 16);
+        }
     }
 }
 
-template <int FG, int NWB, int T, int D, bool RG>
+template <int FG, int NWB, int T, int D, bool RG, int XQ = 0>
 static hipError_t launch_mfma_cfg(const GemvArgs& a, int epi, int rows, hipStream_t s) {
     const int n_fg = epi == EPI_SWIGLU ? (a.N + 7) / 8 : (a.N + 15) / 16;
     const int n_fb = (n_fg + FG - 1) / FG;
     const int n_rt = (rows + 16 * T - 1) / (16 * T);
     const dim3 grid(8 * ((n_fb + 7) / 8) * n_rt), block(64 * FG * NWB);
     switch (epi) {
-        case EPI_SWIGLU: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_SWIGLU, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
-        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_BF16, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
-        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_RESID, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
-        default: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, EPI_F32, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+        case EPI_SWIGLU: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, XQ, EPI_SWIGLU, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+        case EPI_BF16: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, XQ, EPI_BF16, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+        case EPI_RESID: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, XQ, EPI_RESID, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
+        default: hipLaunchKernelGGL((canon_gemv_mfma_kernel<FG, NWB, T, XQ, EPI_F32, D, RG>), grid, block, 0, s, a, n_fg, n_rt); break;
     }
     return hipGetLastError();
 }
 
+template <bool RG, int XQ>
+static hipError_t launch_mfma_t2(const GemvArgs& a, int epi, int rows, bool wide, bool deep, hipStream_t s) {
+    if (wide) return launch_mfma_cfg<2, 8, 2, 2, RG, XQ>(a, epi, rows, s);
+    return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, XQ>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 3, RG, XQ>(a, epi, rows, s);
+}
+
 template <bool RG>
 static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool wide, bool deep, hipStream_t s) {
-    if (rows > 16) {
-        if (wide) return launch_mfma_cfg<2, 8, 2, 2, RG>(a, epi, rows, s);
-        return deep ? launch_mfma_cfg<1, 8, 2, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 3, RG>(a, epi, rows, s);
-    }
+    if (rows > 24) return launch_mfma_t2<RG, 0>(a, epi, rows, wide, deep, s);
+    if (rows > 20) return launch_mfma_t2<RG, 2>(a, epi, rows, wide, deep, s);
+    if (rows > 16) return launch_mfma_t2<RG, 1>(a, epi, rows, wide, deep, s);
     if (wide) return launch_mfma_cfg<2, 4, 1, 3, RG>(a, epi, rows, s);
     return deep ? launch_mfma_cfg<1, 8, 1, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 1, 2, RG>(a, epi, rows, s);
 }
 
-// Launch rule: one 16-row tile per block up to 16 rows, two above (their MFMAs share the
-// weight operand); two feature groups per block where that leaves every CU at least four
+// Launch rule: one 16-row tile per block up to 16 rows, one tile and one or two 4-row quads
+// up to 24, two tiles above (their MFMAs share the weight operand); two feature groups per
+// block where that leaves every CU at least four
 // blocks, else one group served by 8 waves, so the narrow outputs still fill the chip.
 // Ring depth: a launch with at most one block per CU (the 4096-feature outputs) has nothing
 // else on the CU to cover a stage's memory latency, so it keeps three stages in flight

@@ -507,4 +507,24 @@ hipError_t launch_probe_mfma_fma(int n_inst, const float* a, const float* b, con
     return hipGetLastError();
 }
 
+// one v_mfma_f32_4x4x1_16b_f32 per wave: a, b [n][64], c, d [n][4][64]
+typedef float probe_v4f __attribute__((ext_vector_type(4)));
+__global__ __launch_bounds__(64) void probe_mfma4_fma_kernel(const float* __restrict__ a, const float* __restrict__ b,
+                                                             const float* __restrict__ c, float* __restrict__ d) {
+    const size_t t = blockIdx.x;
+    const int lane = threadIdx.x;
+    probe_v4f acc;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[r] = c[(t * 4 + r) * 64 + lane];
+    acc = __builtin_amdgcn_mfma_f32_4x4x1f32(a[t * 64 + lane], b[t * 64 + lane], acc, 0, 0, 0);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) d[(t * 4 + r) * 64 + lane] = acc[r];
+}
+
+hipError_t launch_probe_mfma4_fma(int n_inst, const float* a, const float* b, const float* c, float* d, hipStream_t s) {
+    if (n_inst <= 0) return hipSuccess;
+    hipLaunchKernelGGL(probe_mfma4_fma_kernel, dim3(n_inst), dim3(64), 0, s, a, b, c, d);
+    return hipGetLastError();
+}
+
 }  // namespace mg

@@ -688,6 +688,12 @@ mg_status mg_op_probe_mfma_fma(int n_inst, const float* a, const float* b, const
                                                                                                      : MG_ERR_HIP;
 }
 
+mg_status mg_op_probe_mfma4_fma(int n_inst, const float* a, const float* b, const float* c, float* d, void* stream) {
+    if (n_inst < 0 || (n_inst && (!a || !b || !c || !d))) return MG_ERR_ARG;
+    return launch_probe_mfma4_fma(n_inst, a, b, c, d, static_cast<hipStream_t>(stream)) == hipSuccess ? MG_OK
+                                                                                                      : MG_ERR_HIP;
+}
+
 size_t mg_op_linear_workspace_bytes(int n, int N, int K) {
     if (n <= 0 || N <= 0 || K <= 0) return 0;
     const int S = fast_gemm_splits(n, N, K, device_cu_count());

@@ -194,5 +194,6 @@ hipError_t launch_probe_bf16(int64_t n, const float* in, uint16_t* out, hipStrea
 hipError_t launch_probe_exp(int64_t n, const float* in, float* out, hipStream_t s);
 hipError_t launch_probe_divsqrt(int64_t n, const float* a, const float* b, float* q, float* r, hipStream_t s);
 hipError_t launch_probe_mfma_fma(int n_inst, const float* a, const float* b, const float* c, float* d, hipStream_t s);
+hipError_t launch_probe_mfma4_fma(int n_inst, const float* a, const float* b, const float* c, float* d, hipStream_t s);
 
 }  // namespace mg

@@ -66,6 +66,7 @@ SIGNATURES = {
     "mg_op_probe_exp": (I, [I64, P, P, P]),
     "mg_op_probe_divsqrt": (I, [I64, P, P, P, P, P]),
     "mg_op_probe_mfma_fma": (I, [I, P, P, P, P, P]),
+    "mg_op_probe_mfma4_fma": (I, [I, P, P, P, P, P]),
     "mg_op_linear_workspace_bytes": (SZ, [I, I, I]),
     "mg_op_linear": (I, [I, I, I, I, P, P, P, P, P, SZ, P]),
     "mg_op_fast_gemm_config": (I, [I, I, I, I, P, P]),
@@ -280,6 +281,13 @@ def op_probe_mfma_fma(a, b, c):
     d = torch.empty_like(c)
     _check("mg_op_probe_mfma_fma", load().mg_op_probe_mfma_fma(a.shape[0], a.data_ptr(), b.data_ptr(), c.data_ptr(),
                                                                d.data_ptr(), _stream()))
+    return d
+
+
+def op_probe_mfma4_fma(a, b, c):
+    d = torch.empty_like(c)
+    _check("mg_op_probe_mfma4_fma", load().mg_op_probe_mfma4_fma(a.shape[0], a.data_ptr(), b.data_ptr(), c.data_ptr(),
+                                                                 d.data_ptr(), _stream()))
     return d
 
 

@@ -76,6 +76,8 @@ def test_null_arguments_are_rejected_before_any_work():
     assert lib.mg_op_probe_exp(-1, None, None, None) == -1
     assert lib.mg_op_probe_mfma_fma(-1, None, None, None, None, None) == -1
     assert lib.mg_op_probe_mfma_fma(2, None, None, None, None, None) == -1
+    assert lib.mg_op_probe_mfma4_fma(-1, None, None, None, None, None) == -1
+    assert lib.mg_op_probe_mfma4_fma(2, None, None, None, None, None) == -1
 
 
 def test_create_rejects_small_buffers_and_missing_weights():

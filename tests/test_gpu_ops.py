@@ -57,7 +57,8 @@ def test_division_and_sqrt_are_ieee():
 # block, one or two feature groups per block (two from 32768 features at one 32-row tile),
 # K a multiple of 256 or not (groups past K), several blocks of row tiles, the deep ring (at
 # most one block per CU: up to 256 feature groups) and the shallow one (6144 and 4608
-# features, with one and two 16-row tiles).  K covers several
+# features, with one and two 16-row tiles), and 17..24 rows as one 16-row tile plus one or two
+# 4-row quads on narrow and wide outputs.  K covers several
 # 512-element chunks and a partial last chunk.  kernel: 1 = the verifier's choice for n rows,
 # 2 = the vector-fma kernel, 3 = the matrix-core kernel.
 GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
@@ -65,7 +66,7 @@ GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 
               (21, 16, 1544), (25, 32, 1032), (32, 16, 2056), (47, 16, 520),
               (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096), (7, 6144, 520),
               (12, 4608, 1032), (16, 6144, 264), (20, 6144, 520), (14, 32784, 264), (15, 32768, 512),
-              (40, 32784, 520), (29, 32768, 256), (64, 96, 4096), (100, 48, 264)]
+              (40, 32784, 520), (29, 32768, 256), (18, 32768, 256), (23, 32784, 520), (64, 96, 4096), (100, 48, 264)]
 
 
 @pytest.mark.parametrize("kernel", [1, 2, 3])
@@ -176,6 +177,46 @@ def test_fp32_mfma_k1_is_a_fused_multiply_add():
     with np.errstate(all="ignore"):
         c[sel] = -prod[sel] * np.float32(1 + 2 ** -20)
     d = mg.op_probe_mfma_fma(*(torch.from_numpy(np.ascontiguousarray(x)).to(DEV) for x in (a, b, c))).cpu().numpy()
+    libm = ctypes.CDLL(ctypes.util.find_library("m"))
+    libm.fmaf.restype = ctypes.c_float
+    libm.fmaf.argtypes = [ctypes.c_float] * 3
+    ref = np.array([libm.fmaf(float(x), float(y), float(z)) for x, y, z in zip(ae.ravel(), be.ravel(), c.ravel())],
+                   np.float32).reshape(d.shape)
+    both_nan = np.isnan(d) & np.isnan(ref)
+    assert np.array_equal(np.isnan(d), np.isnan(ref))
+    assert np.array_equal(d.view(np.uint32)[~both_nan], ref.view(np.uint32)[~both_nan])
+
+
+def test_fp32_mfma_4x4x1_is_a_fused_multiply_add():
+    """v_mfma_f32_4x4x1_16b_f32, which carries the fma chains of the rows past the first 16-row
+    tile: every output element equals fmaf(a, b, c) of its operands (one rounding), over the same
+    operand mix as the 16x16x1 test, in the lane and register layout mg_ops.h states."""
+    import ctypes
+    import ctypes.util
+    rng = np.random.default_rng(17)
+    n = 48
+
+    def mixed(shape):
+        x = (rng.standard_normal(shape) * np.exp2(rng.integers(-40, 40, shape))).astype(np.float32)
+        u, m = x.view(np.uint32), rng.random(shape)
+        u[m < 0.04] = rng.integers(1, 0x800000, int((m < 0.04).sum()), dtype=np.uint32)
+        u[(m >= 0.04) & (m < 0.06)] = 0x80000000
+        u[(m >= 0.06) & (m < 0.08)] = 0
+        x[(m >= 0.08) & (m < 0.09)] = np.inf
+        x[(m >= 0.09) & (m < 0.10)] = -np.inf
+        return x
+
+    a, b, c = mixed((n, 64)), mixed((n, 64)), mixed((n, 4, 64))
+    r = np.arange(4)[:, None]
+    l = np.arange(64)[None, :]
+    ia, ib = 4 * (l // 4) + r, l + 0 * r
+    ae, be = a[:, ia], b[:, ib]
+    # a third of the accumulators cancel the product to within a few ulps
+    sel = rng.random((n, 4, 64)) < 0.3
+    prod = (ae.astype(np.float64) * be.astype(np.float64)).astype(np.float32)
+    with np.errstate(all="ignore"):
+        c[sel] = -prod[sel] * np.float32(1 + 2 ** -20)
+    d = mg.op_probe_mfma4_fma(*(torch.from_numpy(np.ascontiguousarray(x)).to(DEV) for x in (a, b, c))).cpu().numpy()
     libm = ctypes.CDLL(ctypes.util.find_library("m"))
     libm.fmaf.restype = ctypes.c_float
     libm.fmaf.argtypes = [ctypes.c_float] * 3
