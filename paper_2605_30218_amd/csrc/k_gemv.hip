@@ -373,25 +373,18 @@ hipError_t launch_canon_gemv_valu(const GemvArgs& a, int epi, hipStream_t s) {
 // Which of the two bit-identical kernels runs: the matrix-core one (k_gemv_mfma.hip) where it
 // was measured faster, the fma kernel above otherwise (its exact 4..24-row tiles waste fewer
 // lanes at small counts; the matrix-core time is flat within a 16-row tile and grows by a
-// quarter tile per 4-row quad past it).  The matrix-core kernel takes host counts above 12
-// rows, 9..12 rows on outputs of fewer than MG_GEMV_VOCAB_N features (all but a
-// vocabulary-sized LM head), and device counts that may exceed 24.  Measured in the decode
-// loop (kernel trace of gated Llama-8B steps, us, fma / matrix-core): at 9..12 rows O and down
-// 14.5 and 34.0 / 22.6 on average (the matrix-core launch has one block per CU there and a
-// deep ring), gate/up 63.8 / 53.9, LM head 222 / 239; at 8 rows the fma kernel is faster on
-// every shape (with the caches flushed before each launch: O 13.8 / 15.0, gate/up 46.2 / 53.7,
-// LM head 182 / 236 us).  Above 12 rows the matrix-core kernel is faster on the projections of
-// the Llama-8B, Qwen2.5-7B and 14B shapes (flushed caches, e.g. at 20 rows gate/up 90.4 /
-// 77.6, down 51.3 / 43.5, LM head 379 / 331; at 24 rows 103.2 / 91.3 and 434 / 400; the
-// Qwen2.5-14B O and down projections at 21..24 rows within 2%).
-#ifndef MG_GEMV_VOCAB_N
-#define MG_GEMV_VOCAB_N 65536
-#endif
+// quarter tile per 4-row quad past it).  The matrix-core kernel takes host counts above 8 rows
+// and device counts that may exceed 24.  Measured in the decode loop (kernel trace of gated
+// Llama-8B steps, us, fma / matrix-core): at 9..12 rows O and down 14.5 and 34.0 / 22.6 on
+// average (the matrix-core launch has one block per CU there and a deep ring), gate/up 63.8 /
+// 53.9; with the caches flushed before each launch the LM heads at 12 rows take 264 / 242
+// (Llama-8B), 246 / 229 and 337 / 314 us (Qwen2.5-7B and 14B); at 8 rows the fma kernel is
+// faster on every shape (O 13.8 / 15.0, gate/up 46.2 / 53.7, LM head 188 / 234 us).  Above 12
+// rows the matrix-core kernel is faster on the projections of the Llama-8B, Qwen2.5-7B and 14B
+// shapes (flushed caches, e.g. at 20 rows gate/up 90.4 / 77.6, down 51.3 / 43.5).
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
-    const int Nf = epi == EPI_SWIGLU ? 2 * a.N : a.N;  // weight rows streamed
-    const bool low_narrow = rows >= 9 && rows <= 12 && Nf < MG_GEMV_VOCAB_N;
-    const bool mfma = a.n_dev ? rows > MG_GEMV_EXACT_MAX : rows > 12 || low_narrow;
+    const bool mfma = a.n_dev ? rows > MG_GEMV_EXACT_MAX : rows > 8;
     return mfma ? launch_canon_gemv_mfma(a, epi, s) : launch_canon_gemv_valu(a, epi, s);
 }
 

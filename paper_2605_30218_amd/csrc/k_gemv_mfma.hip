@@ -213,8 +213,11 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
     // accumulators stay in registers)
     auto mfmas = [&](const Ops& o, auto P) {
         constexpr int p = decltype(P)::value;
-        // a quad's operands converted into their own registers before its MFMAs, so no
-        // conversion waits on an MFMA still reading the register it would overwrite
+        // a quad's operands converted before its MFMAs; with a deep ring (one block per CU, two
+        // waves per SIMD) all sixteen are held in registers of their own so that the stage's
+        // MFMAs issue back to back (down projection at 16 rows 33.3 against 34.7 us); elsewhere
+        // the compiler may reuse two registers, which keeps the VGPR count at 61 and four 8-wave
+        // blocks per CU (gate/up at 16 rows 53.2 against 58.3 us with the sixteen registers)
 #pragma unroll
         for (int qi = 0; qi < NQ; ++qi) {
             float fa[8], fx[TM][8], fq[XA][8];
@@ -227,6 +230,10 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
 #pragma unroll
                     for (int q = 0; q < XQ; ++q) fq[q][e] = bfe(o.bx[q], e);
                 }
+            }
+            if constexpr (D >= 4 && TM == 1 && XQ == 0) {
+                asm volatile("" : "+v"(fa[0]), "+v"(fa[1]), "+v"(fa[2]), "+v"(fa[3]), "+v"(fa[4]), "+v"(fa[5]), "+v"(fa[6]), "+v"(fa[7]),
+                             "+v"(fx[0][0]), "+v"(fx[0][1]), "+v"(fx[0][2]), "+v"(fx[0][3]), "+v"(fx[0][4]), "+v"(fx[0][5]), "+v"(fx[0][6]), "+v"(fx[0][7]));
             }
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -397,39 +404,42 @@ static hipError_t launch_mfma_cfg(const GemvArgs& a, int epi, int rows, hipStrea
     return hipGetLastError();
 }
 
-template <bool RG, int XQ>
-static hipError_t launch_mfma_t2(const GemvArgs& a, int epi, int rows, bool wide, bool deep, hipStream_t s) {
-    if (wide) return launch_mfma_cfg<2, 8, 2, 2, RG, XQ>(a, epi, rows, s);
-    return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, XQ>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 3, RG, XQ>(a, epi, rows, s);
-}
-
 template <bool RG>
-static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool wide, bool deep, hipStream_t s) {
-    if (rows > 24) return launch_mfma_t2<RG, 0>(a, epi, rows, wide, deep, s);
-    if (rows > 20) return launch_mfma_t2<RG, 2>(a, epi, rows, wide, deep, s);
-    if (rows > 16) return launch_mfma_t2<RG, 1>(a, epi, rows, wide, deep, s);
-    if (wide) return launch_mfma_cfg<2, 4, 1, 3, RG>(a, epi, rows, s);
+static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool deep, hipStream_t s) {
+    if (rows > 16 && rows <= 24) {
+        if (rows > 20) return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, 2>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG, 2>(a, epi, rows, s);
+        return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, 1>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG, 1>(a, epi, rows, s);
+    }
+    if (rows > 48) return deep ? launch_mfma_cfg<1, 8, 2, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG>(a, epi, rows, s);
     return deep ? launch_mfma_cfg<1, 8, 1, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 1, 2, RG>(a, epi, rows, s);
 }
 
-// Launch rule: one 16-row tile per block up to 16 rows, one tile and one or two 4-row quads
-// up to 24, two tiles above (their MFMAs share the weight operand); two feature groups per
-// block where that leaves every CU at least four
-// blocks, else one group served by 8 waves, so the narrow outputs still fill the chip.
+// Launch rule: one feature group per block served by 8 waves (two groups per block, sharing
+// the activation stages, measured slower on every shape once the outputs were wide enough to
+// fill the chip: LM head at 16 rows 238 against 206 us, at 20 rows 331 against 302 us, with
+// the caches flushed before each launch).  Row tiles: one 16-row tile per block up to 16 rows;
+// one tile and one or two 4-row quads up to 24; above that 16-row tiles in separate blocks of
+// the same feature group, which the block order puts on one XCD so that the weights come from
+// HBM once and from its L2 after (against two tiles sharing the weight operand: at 32 rows
+// LM head 350 against 368 us, Qwen2.5-7B gate/up 103 against 112, Llama-8B gate/up equal; at
+// 48 rows, where the shared pair is half empty, 556 against 724 and 150 against 188); above 48
+// rows two tiles per block again (equal on gate/up, 81 against 88 us on the down projection
+// at 64 rows).
 // Ring depth: a launch with at most one block per CU (the 4096-feature outputs) has nothing
 // else on the CU to cover a stage's memory latency, so it keeps three stages in flight
 // (depth 4: in the decode loop the O and down projections at 12-16 rows took 21.9 against
 // 29.3 us with depth 2); launches with several blocks per CU keep the shallow ring, which
-// leaves room for more blocks (gate/up at 12-16 rows: 52.9 us at depth 2, 57.9 at 4).
+// leaves room for more blocks (gate/up at 12-16 rows: 52.9 us at depth 2, 57.9 at 4; at
+// 20 rows 80.6 us at depth 2, 84.9 at 3).
 hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
     const int n_fg = epi == EPI_SWIGLU ? (a.N + 7) / 8 : (a.N + 15) / 16;
     const int n_cu = a.n_cu > 0 ? a.n_cu : 256;
-    const int n_rt = rows > 16 ? (rows + 31) / 32 : 1;
-    const bool wide = (long)(n_fg / 2) * n_rt >= 4L * n_cu;
+    const int tile = (rows > 16 && rows <= 24) || rows > 48 ? 32 : 16;
+    const int n_rt = (rows + tile - 1) / tile;
     const bool deep = (long)n_fg * n_rt <= n_cu;
-    return a.K % 256 ? launch_mfma_rg<true>(a, epi, rows, wide, deep, s) : launch_mfma_rg<false>(a, epi, rows, wide, deep, s);
+    return a.K % 256 ? launch_mfma_rg<true>(a, epi, rows, deep, s) : launch_mfma_rg<false>(a, epi, rows, deep, s);
 }
 
 }  // namespace mg

@@ -53,12 +53,12 @@ def test_division_and_sqrt_are_ieee():
 # 16, 20 or 24 rows (9..16 rows of a wide output, N >= 16384, with 3 features per wave and a
 # ragged last feature block; 5..16 rows of 4608 or 6144 features with 3 features per wave,
 # which balances the CUs), several 16-row tiles (a multiple of 16, and a ragged count with a
-# partial last tile); and every launch of the matrix-core kernel: one or two 16-row tiles per
-# block, one or two feature groups per block (two from 32768 features at one 32-row tile),
-# K a multiple of 256 or not (groups past K), several blocks of row tiles, the deep ring (at
-# most one block per CU: up to 256 feature groups) and the shallow one (6144 and 4608
-# features, with one and two 16-row tiles), and 17..24 rows as one 16-row tile plus one or two
-# 4-row quads on narrow and wide outputs.  K covers several
+# partial last tile); and every launch of the matrix-core kernel: one 16-row tile per block
+# up to 16 rows and from 25 to 48 (several blocks of row tiles on one feature group), two
+# 16-row tiles per block from 49 rows, 17..24 rows as one 16-row tile plus one or two 4-row
+# quads, each with the deep ring (at most one block per CU: up to 256 feature groups) and the
+# shallow one (6144, 8208, 16384 and 32768 features), K a multiple of 256 or not (groups
+# past K).  K covers several
 # 512-element chunks and a partial last chunk.  kernel: 1 = the verifier's choice for n rows,
 # 2 = the vector-fma kernel, 3 = the matrix-core kernel.
 GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
@@ -66,7 +66,8 @@ GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 
               (21, 16, 1544), (25, 32, 1032), (32, 16, 2056), (47, 16, 520),
               (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096), (7, 6144, 520),
               (12, 4608, 1032), (16, 6144, 264), (20, 6144, 520), (14, 32784, 264), (15, 32768, 512),
-              (40, 32784, 520), (29, 32768, 256), (18, 32768, 256), (23, 32784, 520), (64, 96, 4096), (100, 48, 264)]
+              (40, 32784, 520), (29, 32768, 256), (18, 32768, 256), (23, 32784, 520), (64, 96, 4096), (100, 48, 264),
+              (64, 8208, 264), (56, 4112, 512)]
 
 
 @pytest.mark.parametrize("kernel", [1, 2, 3])
