@@ -76,12 +76,13 @@ def test_full_verifier_bitexact_and_invariant(full):
     np.testing.assert_array_equal(vl.view(np.uint32), rl.view(np.uint32))
     np.testing.assert_array_equal(vt, rt)
     np.testing.assert_array_equal(vc, rc)
-    # the same row inside 9..64 rows, at several places (each GEMV kernel and tile the launcher
+    # the same row inside 8..64 rows, at several places (each GEMV kernel and tile the launcher
     # takes: the vector kernel's exact tiles, the matrix-core 16-row tile, the 16-row tile with
-    # one or two 4-row quads (places 16..23 fall in a quad), two 16-row tiles)
+    # one or two 4-row quads (places 16..23 fall in a quad), 16-row tiles in separate blocks
+    # (25..48 rows: places in the second and third tile), two 16-row tiles per block)
     rng = np.random.default_rng(0)
     for n, place in ((12, 0), (12, 11), (12, 5), (8, 7), (9, 8), (16, 15), (17, 16), (20, 18), (23, 21),
-                     (24, 19), (64, 63), (64, 30)):
+                     (24, 19), (25, 24), (33, 20), (48, 47), (49, 48), (64, 63), (64, 30)):
         others = rng.choice(np.setdiff1d(np.arange(B), [37]), n - 1, replace=False)
         rr = list(others[:place]) + [37] + list(others[place:])
         l2, t2, c2 = run(rr)
