@@ -28,7 +28,10 @@
 // every wait for the loads are explicit.
 // Chain bits of wave w of its feature group (NWB = 4: l = 32 p + 16 qq + 4 w + bk; NWB = 8:
 // l = 32 p + 4 w + bk): the bits above the wave bits are the wave's own, then come the wave
-// bits, then the instruction's blocks.  Butterfly, in the order of the offsets: the wave's
+// bits, then the instruction's blocks.  NWB = 16 puts the stage parity on the waves as well
+// (l = 4 w + bk): a step is then a pair of stages (512 elements, 1 KiB runs), wave w < 8 takes
+// the even stage's chains and wave w + 8 the odd one's, one accumulator each, and the whole
+// butterfly above the block bits goes through LDS.  Butterfly, in the order of the offsets: the wave's
 // own bits by register adds, the wave bits through LDS, the block bits by register adds of
 // the four block registers of a lane.  IEEE addition is commutative, so pairing operands in
 // either order gives the same bits as the single-lane butterfly.
@@ -98,14 +101,17 @@ __device__ __forceinline__ void gv_lds_wait_x(mg_u32x4& av, mg_u32x4& bv, mg_u32
 template <int FG, int NWB, int T, int XQ, int EPI, int D, bool RAGGED>
 __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4)) void canon_gemv_mfma_kernel(GemvArgs a, int n_fg, int n_rt) {
     constexpr int NW = FG * NWB;
-    constexpr int NQ = 8 / NWB;                 // quads of a wave per stage
+    constexpr bool PW = NWB == 16;              // stage parity on the waves: a step is a stage pair
+    constexpr int SG = PW ? 64 : 32;            // groups of a step (slots of a ring row)
+    constexpr int NQ = PW ? 1 : 8 / NWB;        // quads of a wave per stage
+    constexpr int NACC = PW ? 1 : 2;            // accumulators per quad (stage parity)
     constexpr int SROWS = 16 * FG + 16 * T;     // rows of a stage: weights, then activations
-    constexpr int NLD = SROWS / 2;              // direct-to-LDS loads per stage
+    constexpr int NLD = PW ? SROWS : SROWS / 2; // direct-to-LDS loads per step (one row of 64 slots, or two of 32)
     constexpr int IPW = NLD / NW;               // loads per wave per stage
     constexpr int TM = XQ ? 1 : T;              // 16-row tiles on the 16x16x1 instruction
     constexpr int XA = XQ ? XQ : 1;             // (array extent)
-    static_assert(NWB == 4 || NWB == 8, "waves per feature group");
-    static_assert(2 * NQ * T <= 4, "accumulators");
+    static_assert(NWB == 4 || NWB == 8 || (NWB == 16 && FG == 1 && XQ == 0), "waves per feature group");
+    static_assert(NACC * NQ * T <= 4, "accumulators");
     static_assert(XQ == 0 || (T == 2 && NQ == 1 && XQ <= 2 && XQ <= NWB), "4-row quads: second tile, one quad per wave");
     static_assert(NLD % NW == 0, "every wave issues the same loads (exact waits)");
     const int b = blockIdx.x;
@@ -121,19 +127,20 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
     const int fgw = wave / NWB, wb = wave % NWB;
     const int bk = lane >> 4, ii = lane & 15;
     const int K = a.K, G = K >> 3;
-    const int nst = (G + 31) >> 5;
+    const int nst = PW ? (G + 63) >> 6 : (G + 31) >> 5;
 
-    __shared__ __attribute__((aligned(16))) uint4 ring[D][SROWS * 32];
+    __shared__ __attribute__((aligned(16))) uint4 ring[D][SROWS * SG];
 
     // the rows this lane loads: load m = wave + NW t of a stage covers stage rows 2m, 2m+1;
-    // this lane's half is row 2m + (lane >> 5), its slot lane & 31
+    // this lane's half is row 2m + (lane >> 5), its slot lane & 31 (NWB = 16: load m is row m
+    // of the stage pair, slot lane)
     const uint16_t* src_row[IPW];
     int sw[IPW];
     bool is_w[IPW];
 #pragma unroll
     for (int t = 0; t < IPW; ++t) {
         const int m = wave + NW * t;
-        const int r = 2 * m + (lane >> 5);
+        const int r = PW ? m : 2 * m + (lane >> 5);
         is_w[t] = r < 16 * FG;
         if (r < 16 * FG) {
             const int fgl = fb * FG + r / 16, i = r % 16;
@@ -148,7 +155,7 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
         } else {
             src_row[t] = a.X + (size_t)min(r0 + r - 16 * FG, n - 1) * K;
         }
-        sw[t] = (lane & 31) ^ (r & 15);  // the group this lane's slot holds
+        sw[t] = (PW ? lane : lane & 31) ^ (r & 15);  // the group this lane's slot holds
     }
     // the loads of stage s into buffer s % D (clamped to the last stage)
     auto issue = [&](int s) {
@@ -156,18 +163,18 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
         uint4* buf = ring[s % D];
 #pragma unroll
         for (int t = 0; t < IPW; ++t) {
-            const int g = sc * 32 + sw[t];
+            const int g = sc * SG + sw[t];
             const uint16_t* src = src_row[t] + (size_t)g * 8;
             if constexpr (RAGGED) src = g < G ? src : (is_w[t] ? k_neg_zero_group : k_pos_zero_group);
             __builtin_amdgcn_global_load_lds(src, buf + 64 * (wave + NW * t), 16, 0, 0);
         }
     };
 
-    mg_v16f acc[TM][2 * NQ];  // [row tile][2 qi + p] (qi: the wave's quad of a stage, p: stage parity)
+    mg_v16f acc[TM][NACC * NQ];  // [row tile][NACC qi + p] (qi: the wave's quad of a stage, p: stage parity)
 #pragma unroll
     for (int t = 0; t < TM; ++t)
 #pragma unroll
-        for (int k = 0; k < 2 * NQ; ++k)
+        for (int k = 0; k < NACC * NQ; ++k)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[t][k][r] = 0.0f;
     mg_v4f accx[XA][2];  // 4-row quads: [quad][stage parity]
@@ -182,10 +189,10 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
     int aslot[NQ], bslot[TM][NQ], bxslot[XA];
 #pragma unroll
     for (int qi = 0; qi < NQ; ++qi) {
-        const int lg = (NWB == 4 ? 16 * qi : 0) + 4 * wb + bk;
-        aslot[qi] = 32 * (16 * fgw + ii) + (lg ^ ii);
+        const int lg = PW ? 32 * (wb >> 3) + 4 * (wb & 7) + bk : (NWB == 4 ? 16 * qi : 0) + 4 * wb + bk;
+        aslot[qi] = SG * (16 * fgw + ii) + (lg ^ ii);
 #pragma unroll
-        for (int t = 0; t < TM; ++t) bslot[t][qi] = 32 * (16 * FG + 16 * t + ii) + (lg ^ ii);
+        for (int t = 0; t < TM; ++t) bslot[t][qi] = SG * (16 * FG + 16 * t + ii) + (lg ^ ii);
     }
 #pragma unroll
     for (int q = 0; q < XA; ++q) {  // row 4 q + (lane mod 4) of the second tile, the lane's chain
@@ -212,7 +219,7 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
     // the MFMAs of one stage into the accumulators of parity P (a compile-time index, so the
     // accumulators stay in registers)
     auto mfmas = [&](const Ops& o, auto P) {
-        constexpr int p = decltype(P)::value;
+        constexpr int p = PW ? 0 : decltype(P)::value;
         // a quad's operands converted before its MFMAs; with a deep ring (one block per CU, two
         // waves per SIMD) all sixteen are held in registers of their own so that the stage's
         // MFMAs issue back to back (down projection at 16 rows 33.3 against 34.7 us); elsewhere
@@ -239,7 +246,7 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
             for (int e = 0; e < 8; ++e) {
 #pragma unroll
                 for (int t = 0; t < TM; ++t)
-                    acc[t][2 * qi + p] = __builtin_amdgcn_mfma_f32_16x16x1f32(fa[e], fx[t][e], acc[t][2 * qi + p], 0, 0, 0);
+                    acc[t][NACC * qi + p] = __builtin_amdgcn_mfma_f32_16x16x1f32(fa[e], fx[t][e], acc[t][NACC * qi + p], 0, 0, 0);
                 if constexpr (XQ > 0) {
 #pragma unroll
                     for (int q = 0; q < XQ; ++q)
@@ -287,13 +294,15 @@ __global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4
     // then the wave bits through LDS (the ring is free once every wave is past its last read),
     // one row tile at a time; then the block bits
     float* red = reinterpret_cast<float*>(&ring[0][0]);  // [NW][16][64]
-    static_assert(NW * 16 * 64 * 4 <= D * SROWS * 32 * 16, "the reduction fits in the ring");
+    static_assert(NW * 16 * 64 * 4 <= D * SROWS * SG * 16, "the reduction fits in the ring");
     const int col = wb & 3;  // register column i % 4 that waves wb < 4 finish
     float vt[TM];
 #pragma unroll
     for (int t = 0; t < TM; ++t) {
         mg_v16f tot;
-        if constexpr (NQ == 2) {
+        if constexpr (PW) {
+            tot = acc[t][0];
+        } else if constexpr (NQ == 2) {
             tot = (acc[t][0] + acc[t][1]) + (acc[t][2] + acc[t][3]);
         } else {
             tot = acc[t][0] + acc[t][1];
@@ -430,7 +439,15 @@ static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool deep
 // (depth 4: in the decode loop the O and down projections at 12-16 rows took 21.9 against
 // 29.3 us with depth 2); launches with several blocks per CU keep the shallow ring, which
 // leaves room for more blocks (gate/up at 12-16 rows: 52.9 us at depth 2, 57.9 at 4; at
-// 20 rows 80.6 us at depth 2, 84.9 at 3).
+// 20 rows 80.6 us at depth 2, 84.9 at 3).  A deep launch over a long K (the down projections)
+// runs 16 waves with the stage parity on the waves, so four waves per SIMD share the matrix
+// core and a barrier covers two stages (down at 16 rows 31.7 against 33.4 us, Qwen2.5-7B down
+// 38.0 against 40.8); over a short K its 16-wave butterfly costs more than it saves (O 15.2
+// against 14.9 us).  Its steps are 512 elements, so it takes the ragged form unless 512
+// divides K.
+#ifndef MG_GEMV_PW_MIN_K
+#define MG_GEMV_PW_MIN_K 8192
+#endif
 hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
@@ -439,6 +456,9 @@ hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s) {
     const int tile = (rows > 16 && rows <= 24) || rows > 48 ? 32 : 16;
     const int n_rt = (rows + tile - 1) / tile;
     const bool deep = (long)n_fg * n_rt <= n_cu;
+    // a deep ring over a long K: 16 waves, the two stage parities on separate waves
+    if (deep && tile == 16 && a.K >= MG_GEMV_PW_MIN_K)
+        return a.K % 512 ? launch_mfma_cfg<1, 16, 1, 4, true>(a, epi, rows, s) : launch_mfma_cfg<1, 16, 1, 4, false>(a, epi, rows, s);
     return a.K % 256 ? launch_mfma_rg<true>(a, epi, rows, deep, s) : launch_mfma_rg<false>(a, epi, rows, deep, s);
 }
 

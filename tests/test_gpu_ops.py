@@ -58,7 +58,8 @@ def test_division_and_sqrt_are_ieee():
 # 16-row tiles per block from 49 rows, 17..24 rows as one 16-row tile plus one or two 4-row
 # quads, each with the deep ring (at most one block per CU: up to 256 feature groups) and the
 # shallow one (6144, 8208, 16384 and 32768 features), K a multiple of 256 or not (groups
-# past K).  K covers several
+# past K); the deep ring over K >= 8192 with the stage parity on 16 waves, K a multiple of 512,
+# of 256 only, or of neither, at one and two 16-row tiles.  K covers several
 # 512-element chunks and a partial last chunk.  kernel: 1 = the verifier's choice for n rows,
 # 2 = the vector-fma kernel, 3 = the matrix-core kernel.
 GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 14336),
@@ -67,7 +68,7 @@ GEMV_CASES = [(1, 16, 8), (3, 48, 688), (8, 64, 4096), (13, 80, 1032), (16, 32, 
               (9, 16384, 264), (12, 16400, 1032), (16, 16432, 4096), (7, 6144, 520),
               (12, 4608, 1032), (16, 6144, 264), (20, 6144, 520), (14, 32784, 264), (15, 32768, 512),
               (40, 32784, 520), (29, 32768, 256), (18, 32768, 256), (23, 32784, 520), (64, 96, 4096), (100, 48, 264),
-              (64, 8208, 264), (56, 4112, 512)]
+              (64, 8208, 264), (56, 4112, 512), (12, 64, 8200), (16, 48, 8448), (30, 64, 8704)]
 
 
 @pytest.mark.parametrize("kernel", [1, 2, 3])
