@@ -23,17 +23,17 @@
 // read (16 rows, one group) hits 16 distinct bank groups.  The stages form a ring of D
 // buffers (stage s + D is requested into the buffer of stage s once every wave holds stage
 // s's operands in registers; the operands of stage s + 1 are read while the MFMAs of stage s
-// run); the loads of a stage are shared by all waves, so each stage starts on a block barrier.  The compiler does not count
-// direct-to-LDS loads when it places waits, so the operand reads, their waits, the barrier and
-// every wait for the loads are explicit.
+// run); the loads of a stage are shared by all waves, so each stage starts on a block
+// barrier.  The compiler does not count direct-to-LDS loads when it places waits, so the
+// operand reads, their waits, the barrier and every wait for the loads are explicit.
 // Chain bits of wave w of its feature group (NWB = 4: l = 32 p + 16 qq + 4 w + bk; NWB = 8:
 // l = 32 p + 4 w + bk): the bits above the wave bits are the wave's own, then come the wave
 // bits, then the instruction's blocks.  NWB = 16 puts the stage parity on the waves as well
 // (l = 4 w + bk): a step is then a pair of stages (512 elements, 1 KiB runs), wave w < 8 takes
 // the even stage's chains and wave w + 8 the odd one's, one accumulator each, and the whole
-// butterfly above the block bits goes through LDS.  Butterfly, in the order of the offsets: the wave's
-// own bits by register adds, the wave bits through LDS, the block bits by register adds of
-// the four block registers of a lane.  IEEE addition is commutative, so pairing operands in
+// butterfly above the block bits goes through LDS.  Butterfly, in the order of the offsets:
+// the wave's own bits by register adds, the wave bits through LDS, the block bits by register
+// adds of the four block registers of a lane.  IEEE addition is commutative, so pairing operands in
 // either order gives the same bits as the single-lane butterfly.
 // Groups past K read a group of -0 weights and +0 activations: fma(-0, +0, c) = c + (-0) = c
 // for every c, so those chains are left unchanged.  Rows past the count compute on a copy of
@@ -99,7 +99,7 @@ __device__ __forceinline__ void gv_lds_wait_x(mg_u32x4& av, mg_u32x4& bv, mg_u32
 // and register r of lane 16 c + 4 q + j holds (chain c, feature 4 q + r, row 4 rq + j); an
 // fma step of 16 x 4 rows costs a quarter of a 16 x 16 one.
 template <int FG, int NWB, int T, int XQ, int EPI, int D, bool RAGGED>
-__global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : (FG * NWB >= 16 ? 4 : 4)) void canon_gemv_mfma_kernel(GemvArgs a, int n_fg, int n_rt) {
+__global__ __launch_bounds__(64 * FG * NWB, RAGGED ? 1 : 4) void canon_gemv_mfma_kernel(GemvArgs a, int n_fg, int n_rt) {
     constexpr int NW = FG * NWB;
     constexpr bool PW = NWB == 16;              // stage parity on the waves: a step is a stage pair
     constexpr int SG = PW ? 64 : 32;            // groups of a step (slots of a ring row)
