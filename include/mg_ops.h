@@ -70,6 +70,17 @@ mg_status mg_op_linear(int canon, int n, int N, int K, const uint16_t* X, const 
  * 8).  Host logic only (no device call); the same limits on n, N and K as above,
  * n_cu > 0, else MG_ERR_ARG. */
 mg_status mg_op_fast_gemm_config(int n, int N, int K, int n_cu, int* S, int* waves);
+/* The launch the verifier's canonical GEMV makes for n host-counted rows of an N x K
+ * projection (swiglu != 0: the gate/up pair of N features each, served as 8-pair groups)
+ * on a device of n_cu compute units: *kernel = 2 for the vector-fma kernel (the other
+ * outputs 0) or 3 for the matrix-core kernel with *tile_rows rows per block tile (16, or 32
+ * as one 16-row tile plus *quads 4-row quads), *waves per feature group (8, or 16 with the
+ * stage parity on the waves) and a ring *depth stages deep.  The choice never changes the
+ * result bits (Sec. 3.2's verifier contract: the row result is independent of n).  Host
+ * logic only (no device call); 0 < n <= 256, N > 0, K > 0, K % 8 == 0, n_cu > 0 and
+ * non-NULL outputs, else MG_ERR_ARG. */
+mg_status mg_op_canon_gemv_config(int n, int N, int K, int swiglu, int n_cu, int* kernel, int* tile_rows, int* quads,
+                                  int* waves, int* depth);
 
 /* y[r] = RMSNorm(x[r]) * gamma with the canonical sum of squares (one wave per
  * row, CDOT order), r < n; d % 8 == 0.  bf16 in, bf16 out. */

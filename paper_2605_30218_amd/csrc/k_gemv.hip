@@ -382,10 +382,12 @@ hipError_t launch_canon_gemv_valu(const GemvArgs& a, int epi, hipStream_t s) {
 // faster on every shape (O 13.8 / 15.0, gate/up 46.2 / 53.7, LM head 188 / 234 us).  Above 12
 // rows the matrix-core kernel is faster on the projections of the Llama-8B, Qwen2.5-7B and 14B
 // shapes (flushed caches, e.g. at 20 rows gate/up 90.4 / 77.6, down 51.3 / 43.5).
+bool canon_gemv_on_mfma(int rows, bool device_count) { return device_count ? rows > MG_GEMV_EXACT_MAX : rows > 8; }
+
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
-    const bool mfma = a.n_dev ? rows > MG_GEMV_EXACT_MAX : rows > 8;
-    return mfma ? launch_canon_gemv_mfma(a, epi, s) : launch_canon_gemv_valu(a, epi, s);
+    return canon_gemv_on_mfma(rows, a.n_dev != nullptr) ? launch_canon_gemv_mfma(a, epi, s)
+                                                         : launch_canon_gemv_valu(a, epi, s);
 }
 
 }  // namespace mg

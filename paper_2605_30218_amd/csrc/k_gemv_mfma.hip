@@ -414,12 +414,14 @@ static hipError_t launch_mfma_cfg(const GemvArgs& a, int epi, int rows, hipStrea
 }
 
 template <bool RG>
-static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool deep, hipStream_t s) {
-    if (rows > 16 && rows <= 24) {
-        if (rows > 20) return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, 2>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG, 2>(a, epi, rows, s);
-        return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, 1>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG, 1>(a, epi, rows, s);
+static hipError_t launch_mfma_sel(const GemvArgs& a, int epi, int rows, const MfmaLaunch& c, hipStream_t s) {
+    const bool deep = c.depth == 4;
+    if (c.waves == 16) return launch_mfma_cfg<1, 16, 1, 4, RG>(a, epi, rows, s);
+    if (c.tile_rows == 32) {
+        if (c.quads == 2) return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, 2>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG, 2>(a, epi, rows, s);
+        if (c.quads == 1) return deep ? launch_mfma_cfg<1, 8, 2, 4, RG, 1>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG, 1>(a, epi, rows, s);
+        return deep ? launch_mfma_cfg<1, 8, 2, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG>(a, epi, rows, s);
     }
-    if (rows > 48) return deep ? launch_mfma_cfg<1, 8, 2, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 2, 2, RG>(a, epi, rows, s);
     return deep ? launch_mfma_cfg<1, 8, 1, 4, RG>(a, epi, rows, s) : launch_mfma_cfg<1, 8, 1, 2, RG>(a, epi, rows, s);
 }
 
@@ -448,18 +450,25 @@ static hipError_t launch_mfma_rg(const GemvArgs& a, int epi, int rows, bool deep
 #ifndef MG_GEMV_PW_MIN_K
 #define MG_GEMV_PW_MIN_K 8192
 #endif
+MfmaLaunch choose_mfma_launch(int rows, int n_fg, int K, int n_cu) {
+    MfmaLaunch c{};
+    c.tile_rows = (rows > 16 && rows <= 24) || rows > 48 ? 32 : 16;
+    c.quads = c.tile_rows == 32 && rows <= 24 ? (rows > 20 ? 2 : 1) : 0;
+    const int n_rt = (rows + c.tile_rows - 1) / c.tile_rows;
+    const bool deep = (long)n_fg * n_rt <= (n_cu > 0 ? n_cu : 256);
+    c.depth = deep ? 4 : 2;
+    // a deep ring over a long K: 16 waves, the two stage parities on separate waves
+    c.waves = deep && c.tile_rows == 16 && K >= MG_GEMV_PW_MIN_K ? 16 : 8;
+    c.ragged = K % (c.waves == 16 ? 512 : 256) != 0;
+    return c;
+}
+
 hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s) {
     const int rows = a.n_dev ? a.cap : a.n_host;
     if (rows <= 0 || a.N <= 0) return hipSuccess;
     const int n_fg = epi == EPI_SWIGLU ? (a.N + 7) / 8 : (a.N + 15) / 16;
-    const int n_cu = a.n_cu > 0 ? a.n_cu : 256;
-    const int tile = (rows > 16 && rows <= 24) || rows > 48 ? 32 : 16;
-    const int n_rt = (rows + tile - 1) / tile;
-    const bool deep = (long)n_fg * n_rt <= n_cu;
-    // a deep ring over a long K: 16 waves, the two stage parities on separate waves
-    if (deep && tile == 16 && a.K >= MG_GEMV_PW_MIN_K)
-        return a.K % 512 ? launch_mfma_cfg<1, 16, 1, 4, true>(a, epi, rows, s) : launch_mfma_cfg<1, 16, 1, 4, false>(a, epi, rows, s);
-    return a.K % 256 ? launch_mfma_rg<true>(a, epi, rows, deep, s) : launch_mfma_rg<false>(a, epi, rows, deep, s);
+    const MfmaLaunch c = choose_mfma_launch(rows, n_fg, a.K, a.n_cu);
+    return c.ragged ? launch_mfma_sel<true>(a, epi, rows, c, s) : launch_mfma_sel<false>(a, epi, rows, c, s);
 }
 
 }  // namespace mg

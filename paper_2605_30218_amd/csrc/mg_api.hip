@@ -746,6 +746,25 @@ mg_status mg_op_fast_gemm_config(int n, int N, int K, int n_cu, int* S, int* wav
     return MG_OK;
 }
 
+mg_status mg_op_canon_gemv_config(int n, int N, int K, int swiglu, int n_cu, int* kernel, int* tile_rows, int* quads,
+                                  int* waves, int* depth) {
+    if (n <= 0 || n > 256 || N <= 0 || K <= 0 || K % 8 || n_cu <= 0 || !kernel || !tile_rows || !quads || !waves ||
+        !depth)
+        return MG_ERR_ARG;
+    if (!canon_gemv_on_mfma(n, false)) {
+        *kernel = 2;
+        *tile_rows = *quads = *waves = *depth = 0;
+        return MG_OK;
+    }
+    const MfmaLaunch c = choose_mfma_launch(n, swiglu ? (N + 7) / 8 : (N + 15) / 16, K, n_cu);
+    *kernel = 3;
+    *tile_rows = c.tile_rows;
+    *quads = c.quads;
+    *waves = c.waves;
+    *depth = c.depth;
+    return MG_OK;
+}
+
 mg_status mg_op_decode_step_taps(mg_ctx* c, int B, const int32_t* tokens, const int32_t* positions,
                                  const int32_t* page_table, float* logits, uint16_t* x_taps, void* stream) {
     if (!c || !tokens || !positions || !page_table || !logits || !x_taps) return MG_ERR_ARG;

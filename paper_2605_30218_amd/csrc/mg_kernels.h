@@ -60,6 +60,16 @@ struct GemvArgs {
 hipError_t launch_canon_gemv(const GemvArgs& a, int epi, hipStream_t s);
 hipError_t launch_canon_gemv_valu(const GemvArgs& a, int epi, hipStream_t s);
 hipError_t launch_canon_gemv_mfma(const GemvArgs& a, int epi, hipStream_t s);
+// the kernel launch_canon_gemv takes for a row count (host count, or the cap of a device count)
+bool canon_gemv_on_mfma(int rows, bool device_count);
+// the matrix-core kernel's launch for a row count, n_fg feature groups (16 features, or 8
+// gate/up pairs) and K: rows per tile (16, or 32 with 4-row quads past 16), 4-row quads, waves
+// per block (8, or 16 with the stage parity on the waves), ring depth, groups past K
+struct MfmaLaunch {
+    int tile_rows, quads, waves, depth;
+    bool ragged;
+};
+MfmaLaunch choose_mfma_launch(int rows, int n_fg, int K, int n_cu);
 
 // ---------------------------------------------------------------- fast MFMA GEMM
 enum { FEPI_BF16 = 0, FEPI_PART = 1, FEPI_F32 = 2, FEPI_SWIGLU = 3, FEPI_TOP2 = 4 };

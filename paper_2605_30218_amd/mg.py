@@ -70,6 +70,7 @@ SIGNATURES = {
     "mg_op_linear_workspace_bytes": (SZ, [I, I, I]),
     "mg_op_linear": (I, [I, I, I, I, P, P, P, P, P, SZ, P]),
     "mg_op_fast_gemm_config": (I, [I, I, I, I, P, P]),
+    "mg_op_canon_gemv_config": (I, [I, I, I, I, I, P, P, P, P, P]),
     "mg_op_rmsnorm": (I, [I, I, P, P, F, P, P]),
     "mg_op_decode_step_taps": (I, [P, I, P, P, P, P, P, P]),
 }
@@ -309,6 +310,17 @@ def fast_gemm_config(n, N, K, n_cu=256):
     S, w = C.c_int(0), C.c_int(0)
     _check("mg_op_fast_gemm_config", load().mg_op_fast_gemm_config(n, N, K, n_cu, C.byref(S), C.byref(w)))
     return S.value, w.value
+
+
+def canon_gemv_config(n, N, K, swiglu=False, n_cu=256):
+    """(kernel, rows per tile, 4-row quads, waves per feature group, ring depth) of the
+    verifier's canonical GEMV for n rows of an N x K projection (kernel 2: the vector-fma
+    kernel, the rest 0; 3: the matrix-core kernel) on a device of n_cu compute units (host
+    logic, no device call)."""
+    out = [C.c_int(0) for _ in range(5)]
+    _check("mg_op_canon_gemv_config",
+           load().mg_op_canon_gemv_config(n, N, K, int(bool(swiglu)), n_cu, *[C.byref(o) for o in out]))
+    return tuple(o.value for o in out)
 
 
 def op_rmsnorm(x, gamma, eps):

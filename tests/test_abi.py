@@ -125,3 +125,36 @@ def test_fast_gemm_launch_rule():
         == [4, 4, 4, 4]
     with pytest.raises(Exception):
         mg.fast_gemm_config(0, 64, 512)
+
+
+def test_canon_gemv_launch_rule():
+    """The verifier's canonical GEMV launch, host logic only: the vector-fma kernel up to 8
+    rows, the matrix-core kernel above; one 16-row tile up to 16 rows and from 25 to 48, a
+    16-row tile plus one 4-row quad at 17..20 rows and two at 21..24, two 16-row tiles per
+    block above 48; the 4-stage ring where the launch has at most one block per CU (else 2);
+    16 waves with the stage parity on the waves only for such a launch over K >= 8192 with
+    16-row tiles.  Llama-3.1-8B projections at 12 rows take the launches measured fastest."""
+    assert [mg.canon_gemv_config(n, 4096, 4096)[0] for n in range(1, 10)] == [2] * 8 + [3]
+    assert mg.canon_gemv_config(8, 4096, 4096) == (2, 0, 0, 0, 0)
+    tiles = {9: (16, 0), 16: (16, 0), 17: (32, 1), 20: (32, 1), 21: (32, 2), 24: (32, 2), 25: (16, 0),
+             48: (16, 0), 49: (32, 0), 64: (32, 0), 256: (32, 0)}
+    for n, (tr, q) in tiles.items():
+        assert mg.canon_gemv_config(n, 28672, 4096)[1:3] == (tr, q), n
+    llama12 = {(6144, 4096, False): (3, 16, 0, 8, 2), (4096, 4096, False): (3, 16, 0, 8, 4),
+               (14336, 4096, True): (3, 16, 0, 8, 2), (4096, 14336, False): (3, 16, 0, 16, 4),
+               (128256, 4096, False): (3, 16, 0, 8, 2)}
+    for (N, K, sw), want in llama12.items():
+        assert mg.canon_gemv_config(12, N, K, sw) == want, (N, K, sw)
+    # the deep ring needs every block resident at once: 256 feature groups on 256 CUs, not 257
+    assert mg.canon_gemv_config(12, 4096, 4096, n_cu=256)[4] == 4
+    assert mg.canon_gemv_config(12, 4112, 4096, n_cu=256)[4] == 2
+    assert mg.canon_gemv_config(12, 4096, 4096, n_cu=128)[4] == 2
+    # two 16-row tiles at 30 rows double the blocks; 32-row tiles keep 8 waves over a long K
+    assert mg.canon_gemv_config(30, 2048, 14336) == (3, 16, 0, 16, 4)
+    assert mg.canon_gemv_config(30, 4096, 14336) == (3, 16, 0, 8, 2)
+    assert mg.canon_gemv_config(20, 4096, 14336) == (3, 32, 1, 8, 4)
+    assert mg.canon_gemv_config(12, 4096, 8184)[3] == 8 and mg.canon_gemv_config(12, 4096, 8192)[3] == 16
+    with pytest.raises(Exception):
+        mg.canon_gemv_config(0, 4096, 4096)
+    with pytest.raises(Exception):
+        mg.canon_gemv_config(12, 4096, 4100)
