@@ -60,9 +60,12 @@ __global__ __launch_bounds__(NT) void attn_canon_kernel(AttnArgs a) {
     __shared__ float red[GP];
     __shared__ __attribute__((aligned(16))) uint16_t kown[HD];
 
-    const int i = blockIdx.z;
+    // chunk-major block order (item fastest, chunk slowest): every item's full leading chunks
+    // are dispatched before the short last ones, so a launch of more blocks than CUs runs its
+    // long blocks in the first wave of blocks
+    const int i = blockIdx.x;
     if (i >= items_n(a.it)) return;
-    const int kh = blockIdx.y, c = blockIdx.x;
+    const int kh = blockIdx.y, c = blockIdx.z;
     const ModelDims& m = a.m;
     const int j0 = c * ATT_MAXC;
     // position and page indices of the chunk (uniform, read through the scalar cache); entries
@@ -415,7 +418,7 @@ hipError_t launch_attention(const AttnArgs& a, int canon, hipStream_t s) {
     const int n = a.it.n_host;
     if (n <= 0) return hipSuccess;
     if (!canon || a.chunk != ATT_MAXC) return hipErrorInvalidValue;  // the fast path has its own kernel
-    dim3 g1(a.max_chunks, a.m.Hkv, n), g2(a.m.Hq, n);
+    dim3 g1(n, a.m.Hkv, a.max_chunks), g2(a.m.Hq, n);
     const int G = a.m.Hq / a.m.Hkv;
     if (G < 1 || G > ATT_MAXG) return hipErrorInvalidValue;
     // blocks of the launch (an upper bound: chunks past a row's position exit at once)
